@@ -1,0 +1,193 @@
+"""Oracle decode loop (test infrastructure only; see ``oracle/__init__``).
+
+One sequence is decoded as a state machine over generation blocks, following
+the engine description of the paper:
+
+* Block slots (App. G): a generation block is a placeholder (all mask, not
+  admitted), active (admitted, being denoised), committed and awaiting its
+  cache write, or cached.  Here a committed block waiting for its cache write
+  is called *pending*.
+* Commit rule (benchmark spec; single-block form in App. B.2): every
+  masked position of an active block whose confidence is at least ``tau`` is
+  committed; when none clears ``tau`` the single most confident position is
+  committed (lowest position among equals).
+* Commit sweep (App. C.2, part 1): blocks are visited oldest first; a complete
+  active block whose predecessors are all committed becomes committed, chains
+  commit in one step, and the sweep stops at the first incomplete block.
+* One-step cache write (App. G.2): a committed block's K/V are recomputed
+  from its clean tokens in the next forward, where its rows ride along in
+  front of the active blocks; after that forward it is cached.
+* Admission: with no admission threshold, freed slots are refilled at the end
+  of the step until ``n_inflight`` blocks are active (reading of App. G).
+* TPF (§2.1): tokens committed per model forward; a forward is a step in
+  which the sequence has at least one active block.  Prefill is not counted
+  (App. G.1).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Callable, List, Optional
+
+import numpy as np
+
+from .model import OracleModel, lm_stats
+
+PLACEHOLDER, ACTIVE, PENDING, CACHED = 0, 1, 2, 3
+
+__all__ = ["SeqDecoder", "commit_set", "decode_batch", "PLACEHOLDER", "ACTIVE", "PENDING", "CACHED"]
+
+
+def commit_set(conf: np.ndarray, tau: float) -> np.ndarray:
+    """Boolean commit mask over masked positions listed in position order.
+    conf >= tau (inclusive, tau held as float32); at least the argmax."""
+    t = float(np.float32(tau))
+    s = conf >= t
+    if not s.any():
+        s[int(np.argmax(conf))] = True          # first maximum = lowest position
+    return s
+
+
+@dataclass
+class StepRecord:
+    step: int
+    masked: np.ndarray          # absolute positions that were masked in active blocks
+    conf: np.ndarray
+    tok: np.ndarray
+    p2: np.ndarray
+    committed: np.ndarray       # absolute positions committed this step
+    status_after: np.ndarray    # block slot states after the sweep and admission
+
+
+class SeqDecoder:
+    """Decoder state of one sequence: prompt ``[0, P)``, ``G`` generated
+    positions in ``G // B`` blocks, at most ``n_inflight`` active blocks."""
+
+    def __init__(self, model: OracleModel, prompt: np.ndarray, G: int, B: int, n_inflight: int,
+                 tau: float):
+        P = len(prompt)
+        if B < 1 or n_inflight < 1 or P % B or G % B:
+            raise ValueError("need B >= 1, n_inflight >= 1, P % B == 0 and G % B == 0")
+        self.model, self.P, self.G, self.B, self.nb, self.tau = model, P, G, B, n_inflight, tau
+        self.mask_id = model.mask_id
+        self.tokens = np.concatenate([np.asarray(prompt, dtype=np.int64),
+                                      np.full(G, self.mask_id, dtype=np.int64)])
+        self.status = np.full(G // B, PLACEHOLDER, dtype=np.int64)
+        self.cache = model.kv_cache(P + G)
+        self.cache_len = 0
+        self.forwards = 0
+        self.commit_step = np.full(G, -1, dtype=np.int64)
+        self.records: List[StepRecord] = []
+        self.keep_records = False
+
+    # -- slots --------------------------------------------------------------
+    def _admit(self):
+        while np.count_nonzero(self.status == ACTIVE) < self.nb:
+            free = np.nonzero(self.status == PLACEHOLDER)[0]
+            if free.size == 0:
+                break
+            self.status[free[0]] = ACTIVE
+
+    @property
+    def done(self) -> bool:
+        return not np.any((self.status == ACTIVE) | (self.status == PLACEHOLDER))
+
+    def window(self):
+        """Absolute positions [start, end) of this step's forward: pending
+        blocks (clean rows for their cache write) followed by active blocks."""
+        live = np.nonzero((self.status == PENDING) | (self.status == ACTIVE))[0]
+        return self.cache_len, self.P + self.B * (int(live[-1]) + 1)
+
+    # -- prefill --------------------------------------------------------------
+    def prefill(self):
+        """Encode the prompt (no LM head) and admit the first blocks."""
+        if self.P > 0:
+            self.model.forward(self.tokens, 0, self.P, self.cache, self.B)
+        self.cache_len = self.P
+        self._admit()
+
+    # -- one denoising step -------------------------------------------------
+    def forward_step(self):
+        """Forward over the window; statistics for every masked position."""
+        s, e = self.window()
+        h = self.model.forward(self.tokens, s, e, self.cache, self.B)
+        masked = np.nonzero(self.tokens[s:e] == self.mask_id)[0] + s
+        z = self.model.logits(h[masked - s])
+        conf, tok, p2 = lm_stats(z)
+        return masked, conf, tok, p2
+
+    def apply(self, positions: np.ndarray, toks: np.ndarray, step: int):
+        """Commit ``toks`` at ``positions``; cache write, sweep, admission."""
+        # Pending blocks had their K/V written by this step's forward.
+        for b in np.nonzero(self.status == PENDING)[0]:
+            self.status[b] = CACHED
+            self.cache_len += self.B
+        self.tokens[positions] = toks
+        self.commit_step[positions - self.P] = step
+        # In-order sweep over the block buffer, oldest block first.
+        for b in range(len(self.status)):
+            if self.status[b] in (CACHED, PENDING):
+                continue
+            if self.status[b] != ACTIVE:
+                break
+            lo = self.P + b * self.B
+            if np.any(self.tokens[lo:lo + self.B] == self.mask_id):
+                break
+            self.status[b] = PENDING
+        self._admit()
+        self.forwards += 1
+
+    def step(self, step: int, decide: Optional[Callable] = None):
+        masked, conf, tok, p2 = self.forward_step()
+        own = commit_set(conf, self.tau)
+        if decide is None:
+            sel = own
+            toks = tok[sel]
+            positions = masked[sel]
+        else:
+            positions, toks = decide(self, step, masked, conf, tok, p2, own)
+        self.apply(np.asarray(positions, dtype=np.int64), np.asarray(toks, dtype=np.int64), step)
+        if self.keep_records:
+            self.records.append(StepRecord(step, masked, conf, tok, p2, np.asarray(positions),
+                                           self.status.copy()))
+
+
+@dataclass
+class BatchResult:
+    tokens: np.ndarray          # [b][G] generated tokens
+    commit_step: np.ndarray     # [b][G] step index at which each position committed
+    forwards: np.ndarray        # [b]
+    steps: int
+
+    @property
+    def tpf(self) -> float:
+        """Tokens per forward: sum of generated tokens over sum of forwards."""
+        return float(self.tokens.size) / float(np.sum(self.forwards))
+
+
+def decode_batch(model: OracleModel, prompts: np.ndarray, G: int, B: int, n_inflight: int,
+                 tau: float, decide: Optional[Callable] = None, max_steps: int | None = None,
+                 keep_records: bool = False) -> BatchResult:
+    """Decode independent sequences; batch rows never interact, so each runs
+    its own state machine and the global step index equals its forward index
+    while it is active."""
+    b = prompts.shape[0]
+    toks = np.zeros((b, G), dtype=np.int64)
+    cs = np.zeros((b, G), dtype=np.int64)
+    fw = np.zeros(b, dtype=np.int64)
+    steps = 0
+    for i in range(b):
+        d = SeqDecoder(model, prompts[i], G, B, n_inflight, tau)
+        d.keep_records = keep_records
+        d.seq_index = i
+        d.prefill()
+        s = 0
+        while not d.done:
+            if max_steps is not None and s >= max_steps:
+                raise RuntimeError("decode did not finish within max_steps")
+            d.step(s, decide)
+            s += 1
+        steps = max(steps, s)
+        toks[i] = d.tokens[d.P:]
+        cs[i] = d.commit_step
+        fw[i] = d.forwards
+    return BatchResult(toks, cs, fw, steps)

@@ -1,0 +1,268 @@
+"""Pins of the decode oracle: closed forms, brute force, textbook special
+cases and invariants (block size 1 = causal decoding; cached step = full
+recompute; at least one token per step; tau > 1 gives one token per step;
+maximal exact commit)."""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.model import OracleModel, round_bf16, lm_stats
+from oracle.decode import (SeqDecoder, decode_batch, commit_set, ACTIVE, PENDING, CACHED,
+                           PLACEHOLDER)
+from tests.refmodels import TinyCfg, tiny_weights, scalar_forward, torch_causal_logits, brute_decode
+
+
+# ---------------------------------------------------------------- numerics pieces
+def test_round_bf16_matches_torch():
+    rng = np.random.default_rng(1)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000),
+                        [1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 0.0, 65504.0]])
+    want = torch.tensor(x, dtype=torch.float64).to(torch.float32).to(torch.bfloat16).to(torch.float64)
+    np.testing.assert_array_equal(round_bf16(x), want.numpy())
+    assert round_bf16(np.array([1.0 + 2 ** -8]))[0] == 1.0              # tie -> even
+    assert round_bf16(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+
+
+def _model(cfg=None, seed=0, precision="f64", std=0.3):
+    cfg = cfg or TinyCfg()
+    return cfg, tiny_weights(cfg, seed, std), OracleModel(cfg, tiny_weights(cfg, seed, std), precision)
+
+
+def test_rope_is_complex_rotation_and_relative():
+    cfg, _, m = _model(TinyCfg(head_dim=8))
+    rng = np.random.default_rng(2)
+    q = rng.standard_normal((5, 2, 8))
+    pos = np.array([0, 1, 7, 100, 9000])
+    got = m.rope(q, pos)
+    z = (q[..., :4] + 1j * q[..., 4:]) * np.exp(1j * pos[:, None, None] * 1e4 ** (-np.arange(4) * 2 / 8))
+    np.testing.assert_allclose(got, np.concatenate([z.real, z.imag], -1), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(m.rope(q[:1], np.array([0])), q[:1], atol=0)
+    # the score between a rotated query and key depends only on the offset
+    a, b = rng.standard_normal((1, 1, 8)), rng.standard_normal((1, 1, 8))
+    s = lambda i, j: float(np.sum(m.rope(a, np.array([i])) * m.rope(b, np.array([j]))))
+    assert s(10, 3) == pytest.approx(s(107, 100), abs=1e-9)
+
+
+def test_rmsnorm_unit_rms():
+    from oracle.model import _rmsnorm
+    x = np.random.default_rng(3).standard_normal((4, 64)) * 7
+    y = _rmsnorm(x, np.ones(64), 0.0)
+    np.testing.assert_allclose(np.sqrt(np.mean(y * y, -1)), 1.0, rtol=1e-12)
+
+
+@pytest.mark.parametrize("B,causal", [(64, False), (1, True)])
+def test_attention_special_cases_match_torch(B, causal):
+    """One block covering everything = full attention; B = 1 = causal attention."""
+    cfg, _, m = _model(TinyCfg(n_heads=4, n_kv_heads=2, head_dim=8))
+    rng = np.random.default_rng(4)
+    T = 12
+    q, k, v = rng.standard_normal((T, 4, 8)), rng.standard_normal((T, 2, 8)), rng.standard_normal((T, 2, 8))
+    got = m.attention(q, np.arange(T), k, v, B)
+    tq = torch.tensor(q).transpose(0, 1)
+    tk = torch.tensor(k).repeat_interleave(2, 1).transpose(0, 1)
+    tv = torch.tensor(v).repeat_interleave(2, 1).transpose(0, 1)
+    want = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, is_causal=causal)
+    np.testing.assert_allclose(got, want.transpose(0, 1).numpy(), atol=1e-12)
+
+
+def test_lm_stats_identities():
+    """conf = max softmax probability in (0, 1]; shift invariance; the
+    suppressed mask column never wins; lowest id among equal maxima."""
+    rng = np.random.default_rng(5)
+    z = rng.standard_normal((50, 33)) * 5
+    conf, tok, p2 = lm_stats(z)
+    e = np.exp(z - z.max(1, keepdims=True))
+    prob = e / e.sum(1, keepdims=True)
+    np.testing.assert_allclose(conf, prob.max(1), rtol=1e-14)
+    np.testing.assert_array_equal(tok, prob.argmax(1))
+    np.testing.assert_allclose(p2, np.sort(prob, 1)[:, -2], rtol=1e-13)
+    c2, t2, _ = lm_stats(z + 123.25)
+    np.testing.assert_allclose(c2, conf, rtol=1e-12)
+    np.testing.assert_array_equal(t2, tok)
+    assert np.all((conf > 0) & (conf <= 1))
+    tie = np.array([[0.0, 3.0, 1.0, 3.0]])
+    assert lm_stats(tie)[1][0] == 1
+    cfg, _, m = _model()
+    h = np.zeros((1, cfg.d_model))
+    h[0, 0] = 1.0
+    m.lm_head[:] = 0.0
+    m.lm_head[cfg.mask_id, 0] = 100.0        # mask column would win without suppression
+    m.lm_head[3, 0] = 0.5
+    zz = m.logits(h)
+    assert zz[0, cfg.mask_id] == -np.inf and lm_stats(zz)[1][0] == 3
+
+
+def test_commit_rule():
+    assert commit_set(np.array([0.2, 0.95, 0.9, 0.91]), 0.9).tolist() == [False, True, True, True]
+    assert commit_set(np.array([0.2, 0.5, 0.5]), 0.9).tolist() == [False, True, False]
+    assert commit_set(np.array([1.0, 1.0]), 2.0).tolist() == [True, False]
+    assert commit_set(np.array([0.1, 0.3]), 0.0).all()
+
+
+# ---------------------------------------------------------------- P5: brute force
+@pytest.mark.parametrize("B", [1, 2, 4, 8])
+def test_forward_matches_scalar_loops(B):
+    cfg, ws, m = _model(TinyCfg())
+    toks = np.array([3, 1, 4, 1, 5, 9, 2, cfg.mask_id])
+    want = scalar_forward(cfg, ws, list(toks), B)
+    cache = m.kv_cache(8)
+    got = m.logits(m.forward(toks, 0, 8, cache, B))
+    np.testing.assert_allclose(got, want, atol=1e-10)
+
+
+def test_moe_forward_matches_scalar_loops():
+    cfg, ws, m = _model(TinyCfg(n_experts=4, top_k=2, expert_ffn=6, n_shared=1, ffn_dim=0))
+    toks = np.array([3, 1, 4, 1, 5, 9, 2, 6])
+    got = m.logits(m.forward(toks, 0, 8, m.kv_cache(8), 2))
+    np.testing.assert_allclose(got, scalar_forward(cfg, ws, list(toks), 2), atol=1e-10)
+
+
+def test_moe_all_experts_is_dense_mixture():
+    cfg, ws, m = _model(TinyCfg(n_experts=3, top_k=3, expert_ffn=5, n_shared=1, ffn_dim=0))
+    L = m.layers[0]
+    a = np.random.default_rng(6).standard_normal((7, cfg.d_model))
+    lg = a @ L["w_router"].T
+    pr = np.exp(lg - lg.max(1, keepdims=True))
+    pr /= pr.sum(1, keepdims=True)
+    silu = lambda x: x / (1 + np.exp(-x))
+    want = sum(pr[:, e:e + 1] * ((silu(a @ L["w_gate_e"][e].T) * (a @ L["w_up_e"][e].T)) @ L["w_down_e"][e].T)
+               for e in range(3))
+    want = want + (silu(a @ L["w_gate_s"].T) * (a @ L["w_up_s"].T)) @ L["w_down_s"].T
+    np.testing.assert_allclose(m.moe_ffn(a, L), want, atol=1e-12)
+
+
+CASES = [(P, B, nb, tau) for B in (1, 2, 4, 8) for P in range(0, 8, B)
+         for nb in (1, 2, 3) for tau in (0.0, 0.5, 0.9, 2.0)]
+
+
+@pytest.mark.parametrize("P,B,nb,tau", CASES)
+def test_decode_matches_brute_force(P, B, nb, tau):
+    """2-layer model, 8 tokens, vocabulary 11: the cached oracle decode equals
+    full recomputation with independently restated rules."""
+    G = 8 - P
+    cfg, ws, m = _model(TinyCfg())
+    prompt = np.random.default_rng(P * 100 + B).integers(0, cfg.vocab - 1, P)
+    bt, bs, bsteps = brute_decode(cfg, ws, list(prompt), G, B, nb, tau)
+    r = decode_batch(m, prompt[None, :], G, B, nb, tau)
+    np.testing.assert_array_equal(r.tokens[0], bt)
+    np.testing.assert_array_equal(r.commit_step[0], bs)
+    assert r.forwards[0] == bsteps
+
+
+# ---------------------------------------------------------------- P2: causal decoding
+def test_block_size_one_is_greedy_causal_decoding():
+    cfg, ws, m = _model(TinyCfg(vocab=23, n_kv_heads=2), seed=3)
+    P, G = 5, 9
+    prompt = list(np.random.default_rng(9).integers(0, cfg.vocab - 1, P))
+    toks = list(prompt)
+    for p in range(P, P + G):
+        z = torch_causal_logits(cfg, ws, toks + [cfg.mask_id])[p]
+        toks.append(int(np.argmax(z)))
+    for tau in (0.0, 0.7, 2.0):
+        r = decode_batch(m, np.array([prompt]), G, 1, 1, tau)
+        assert r.tokens[0].tolist() == toks[P:]
+        assert r.forwards[0] == G
+
+
+# ---------------------------------------------------------------- P1: cache = recompute
+@pytest.mark.parametrize("precision", ["f64", "bf16"])
+def test_cached_step_equals_full_recompute(precision):
+    cfg = TinyCfg(n_layers=3, d_model=32, n_heads=4, n_kv_heads=2, head_dim=8, ffn_dim=48, vocab=37)
+    ws = tiny_weights(cfg, 11, 0.2)
+    m = OracleModel(cfg, ws, precision)
+    P, G, B, nb = 8, 24, 4, 2
+    prompt = np.random.default_rng(12).integers(0, cfg.vocab - 1, P)
+    d = SeqDecoder(m, prompt, G, B, nb, 0.6)
+    d.prefill()
+    checked = 0
+    step = 0
+    while not d.done:
+        s, e = d.window()
+        fresh = m.kv_cache(P + G)
+        full = m.forward(d.tokens, 0, e, fresh, B)[s:]
+        cached = m.forward(d.tokens, s, e, d.cache, B)
+        tol = 1e-12 if precision == "f64" else 1e-6
+        np.testing.assert_allclose(cached, full, atol=tol, rtol=0)
+        checked += 1
+        d.step(step)
+        step += 1
+    assert checked == d.forwards and checked >= 3
+
+
+# ---------------------------------------------------------------- P3 / P4: closed forms
+@pytest.mark.parametrize("nb", [1, 2, 3])
+def test_tau_above_one_commits_one_token_per_step(nb):
+    cfg, ws, m = _model(TinyCfg(vocab=29))
+    P, G, B = 4, 24, 4
+    prompts = np.random.default_rng(13).integers(0, cfg.vocab - 1, (2, P))
+    r = decode_batch(m, prompts, G, B, nb, 2.0)
+    assert r.forwards.tolist() == [G, G] and r.tpf == 1.0
+    for i in range(2):
+        assert sorted(r.commit_step[i].tolist()) == list(range(G))
+
+
+@pytest.mark.parametrize("nb", [1, 2, 3])
+def test_tau_zero_resolves_each_block_in_one_step(nb):
+    cfg, ws, m = _model(TinyCfg(vocab=29))
+    P, G, B = 4, 28, 4
+    prompts = np.random.default_rng(14).integers(0, cfg.vocab - 1, (1, P))
+    r = decode_batch(m, prompts, G, B, nb, 0.0)
+    nblk = G // B
+    assert r.forwards[0] == math.ceil(nblk / nb)
+    assert r.tpf == G / math.ceil(nblk / nb)
+    np.testing.assert_array_equal(r.commit_step[0], np.repeat(np.arange(nblk) // nb, B))
+
+
+# ---------------------------------------------------------------- P6: invariants
+@pytest.mark.parametrize("tau,nb", [(0.3, 3), (0.6, 2), (0.9, 3), (0.99, 1)])
+def test_commit_invariants(tau, nb):
+    cfg, ws, m = _model(TinyCfg(vocab=31), seed=5, std=0.4)
+    P, G, B = 4, 32, 4
+    prompt = np.random.default_rng(15).integers(0, cfg.vocab - 1, P)
+    d = SeqDecoder(m, prompt, G, B, nb, tau)
+    d.keep_records = True
+    d.prefill()
+    s = 0
+    while not d.done:
+        before = d.status.copy()
+        d.step(s)
+        rec = d.records[-1]
+        assert len(rec.committed) >= 1                       # at least one token per step
+        st = rec.status_after
+        # slot order: cached / pending blocks form a prefix, then active, then placeholders
+        order = [{CACHED: 0, PENDING: 0, ACTIVE: 1, PLACEHOLDER: 2}[x] for x in st]
+        assert order == sorted(order)
+        # maximal exact commit: no active complete block preceded only by committed blocks
+        first_active = next((b for b in range(len(st)) if st[b] == ACTIVE), None)
+        if first_active is not None:
+            lo = P + first_active * B
+            assert np.any(d.tokens[lo:lo + B] == cfg.mask_id)
+        assert np.count_nonzero(st == ACTIVE) <= nb
+        # transitions are one-way: placeholder -> active -> pending -> cached
+        rank = {PLACEHOLDER: 0, ACTIVE: 1, PENDING: 2, CACHED: 3}
+        assert all(rank[a] <= rank[b] for a, b in zip(before, st))
+        s += 1
+    cs = d.commit_step
+    assert np.all(cs >= 0) and np.all(d.tokens != cfg.mask_id)
+    assert sum(len(r.committed) for r in d.records) == G
+    # blocks enter the cache in order
+    done_step = [cs[b * B:(b + 1) * B].max() for b in range(G // B)]
+    assert all(np.maximum.accumulate(done_step) >= done_step)
+
+
+def test_bf16_mode_differs_only_at_storage_points(monkeypatch):
+    """With the storage rounding switched off, bf16 mode equals f64 mode up to
+    float32 matmul accumulation."""
+    import oracle.model as om
+    cfg = TinyCfg(n_layers=2, d_model=32, n_heads=4, n_kv_heads=2, head_dim=8, ffn_dim=48, vocab=37)
+    ws = [np.float32(w).astype(np.float64) for w in tiny_weights(cfg, 21, 0.2)]
+    toks = np.array([1, 2, 3, 4, 5, 6, 7, 8])
+    a = OracleModel(cfg, ws, "f64")
+    za = a.logits(a.forward(toks, 0, 8, a.kv_cache(8), 4))
+    monkeypatch.setattr(om, "round_bf16", lambda x: np.asarray(x, dtype=np.float64))
+    b = OracleModel(cfg, ws, "bf16")
+    zb = b.logits(b.forward(toks, 0, 8, b.kv_cache(8), 4))
+    np.testing.assert_allclose(zb, za, atol=2e-4)
