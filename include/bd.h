@@ -1,0 +1,227 @@
+/*
+ * bd.h -- C ABI of the MI355X (gfx950) block-diffusion decoding library.
+ *
+ * The library runs the block-diffusion denoising step of a decoder LM: one
+ * forward over a window of in-flight blocks against a KV-cached committed
+ * prefix, under the block-causal mask (paper §2.1: bidirectional inside a
+ * block, causal across blocks and to the prefix), a mask-suppressed LM-head
+ * softmax per masked position giving confidence and argmax (App. B.1), and
+ * the threshold commit rule with in-order block commit and a one-step cache
+ * write (App. C, App. G).  It also exports the host-side Redline selection
+ * test (§4.2, App. A).
+ *
+ * Conventions
+ *  - Every call returns a bd_status and never throws.  On failure,
+ *    bd_last_error() returns a thread-local message describing the cause.
+ *  - "_dev" pointers are HIP device pointers; all other pointers are host.
+ *  - All device work is asynchronous on the stream given to bd_init_model.
+ *    Only bd_decode (on return), bd_commit with a non-NULL all_done_host,
+ *    and bd_state_read synchronise that stream.
+ *  - Matrices are row-major; weight matrices are stored [out][in].
+ *  - Tokens are int32 ids in [0, vocab); mask_id is the placeholder token,
+ *    whose LM-head column is suppressed before the softmax.
+ *  - Prompt length P and generation length G must be multiples of the block
+ *    size; the block grid is aligned at absolute position 0.
+ */
+#ifndef BD_H
+#define BD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BD_OK = 0,
+    BD_EINVAL = -1,        /* invalid argument or configuration */
+    BD_ENOMEM = -2,        /* device or host allocation failed */
+    BD_EHIP = -3,          /* a HIP runtime call failed */
+    BD_ESTATE = -4,        /* call not valid in the object's current state */
+    BD_EUNSUPPORTED = -5   /* valid but not supported by this build */
+} bd_status;
+
+typedef enum { BD_F32 = 0, BD_BF16 = 1 } bd_dtype;
+
+/* Model architecture.  n_experts == 0 selects a dense SwiGLU FFN of width
+ * ffn_dim; n_experts > 0 a top_k-of-n_experts SwiGLU MoE of width expert_ffn
+ * plus n_shared always-on shared experts of the same width. */
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+    int32_t n_experts, top_k, expert_ffn, n_shared;
+    float rms_eps;         /* RMSNorm epsilon */
+    float rope_theta;      /* RoPE base; rotate-half pairs (i, i + head_dim/2) */
+    float logit_scale;     /* LM-head logits are multiplied by this */
+    int32_t mask_id;       /* placeholder token id, in [0, vocab) */
+    int32_t dtype;         /* bd_dtype of matrices, activations and KV cache */
+} bd_model_cfg;
+
+/* One serving configuration: the paper's operating point lambda (§2.1 and
+ * the notation table): accept threshold, in-flight block count, block size. */
+typedef struct {
+    float tau;             /* commit positions with confidence >= tau (float32
+                              compare); tau > 1 commits one token per step */
+    int32_t n_inflight;    /* maximum number of active blocks, >= 1 */
+    int32_t block_size;    /* B >= 1 */
+} bd_decode_cfg;
+
+typedef struct bd_model bd_model;
+typedef struct bd_state bd_state;
+
+/*
+ * bd_init_model -- bind a model to its weights.
+ *  weights_dev: n_weights device pointers, in this order (d = d_model,
+ *   hd = head_dim, H = n_heads, Hkv = n_kv_heads, E = n_experts,
+ *   Fe = expert_ffn, Fs = n_shared * expert_ffn); "mat" tensors are in the
+ *   model dtype (bf16 or f32), norm gains and the router are float32:
+ *     tok_embed [vocab][d]                                   mat
+ *     per layer:
+ *       attn_norm [d]                                        f32
+ *       w_qkv [(H + 2 Hkv) hd][d]  (q heads, k heads, v heads) mat
+ *       w_o [d][H hd]                                        mat
+ *       ffn_norm [d]                                         f32
+ *       dense:  w_gate [ffn][d], w_up [ffn][d], w_down [d][ffn]          mat
+ *       MoE:    w_router [E][d] (f32), w_gate_e [E][Fe][d], w_up_e [E][Fe][d],
+ *               w_down_e [E][d][Fe], w_gate_s [Fs][d], w_up_s [Fs][d],
+ *               w_down_s [d][Fs]                                          mat
+ *     final_norm [d]                                         f32
+ *     lm_head [vocab][d]                                     mat
+ *  The caller keeps the weights alive until bd_model_free; the library may
+ *  keep private repacked copies, which it frees.
+ *  stream: a hipStream_t (NULL = default stream).
+ *  Errors: BD_EINVAL for inconsistent dimensions (head_dim not 64 or 128,
+ *  n_heads not a multiple of n_kv_heads, mask_id out of range, wrong
+ *  n_weights), BD_ENOMEM, BD_EHIP.
+ */
+bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev, int32_t n_weights,
+                        void* stream, bd_model** out);
+
+/*
+ * bd_prefill -- encode b prompts and create a decode state.
+ *  prompt_dev: int32 [b][P] device.  The prompt forward runs under the same
+ *  block-causal mask with no LM head (prompt steps are not counted as
+ *  forwards, App. G.1).  Afterwards the first min(n_inflight, G/B) blocks of
+ *  every sequence are active and fully masked.
+ *  Errors: BD_EINVAL if b < 1, P < 0, G < 1, B < 1, n_inflight < 1,
+ *  P % B != 0, G % B != 0, tau is NaN, or a prompt id is outside [0, vocab)
+ *  (checked on the device; reported by the next synchronising call).
+ */
+bd_status bd_prefill(bd_model* model, const int32_t* prompt_dev, int32_t b, int32_t P, int32_t G,
+                     const bd_decode_cfg* cfg, bd_state** out);
+
+/*
+ * bd_denoise_step -- one decoder forward over every sequence's window
+ *  (committed blocks awaiting their cache write, then the active blocks),
+ *  followed by the LM head on the masked positions.  Window K/V are written
+ *  into the cache at their absolute positions.
+ *  Optional debug outputs (NULL to skip), indexed by generated position:
+ *   conf_dev [b][G] float32: confidence of every position masked this step,
+ *   tok_dev [b][G] int32: its argmax;
+ *   logits_dev [b][G][vocab] float32: scaled, mask-suppressed logits (-inf in
+ *   the mask column) of those positions, from a separate debug kernel.
+ *  Positions not masked this step are left untouched.
+ *  Errors: BD_ESTATE when the previous step was not committed.
+ */
+bd_status bd_denoise_step(bd_model* model, bd_state* st, float* conf_dev, int32_t* tok_dev,
+                          float* logits_dev);
+
+/*
+ * bd_commit -- apply the commit rule to the last step's statistics: commit
+ *  every masked position with confidence >= tau, at least the most confident
+ *  one of the sequence (lowest position on ties); sweep blocks oldest first
+ *  committing every complete block whose predecessors are committed (App.
+ *  C.2); mark blocks written by the last forward as cached; admit new blocks
+ *  up to n_inflight; count the forward.  all_done_host (optional) receives 1
+ *  when every sequence is finished, which synchronises the stream.
+ *  Errors: BD_ESTATE when no step is pending.
+ */
+bd_status bd_commit(bd_model* model, bd_state* st, int32_t* all_done_host);
+
+/*
+ * bd_state_read -- copy the decode trace to device buffers (any may be NULL):
+ *  tokens_dev [b][G] int32 (mask_id where not yet committed),
+ *  commit_step_dev [b][G] int32 (0-based step of the commit, -1 if none),
+ *  forwards_dev [b] int32 (forwards with at least one active block).
+ *  Synchronises the stream.
+ */
+bd_status bd_state_read(bd_model* model, bd_state* st, int32_t* tokens_dev, int32_t* commit_step_dev,
+                        int32_t* forwards_dev);
+
+/*
+ * bd_decode -- prefill, then denoise/commit until every sequence has
+ *  committed its G tokens, then write the trace (see bd_state_read).
+ *  Synchronises on return.  TPF = b*G / sum(forwards).
+ */
+bd_status bd_decode(bd_model* model, const int32_t* prompt_dev, int32_t b, int32_t P, int32_t G,
+                    const bd_decode_cfg* cfg, int32_t* tokens_dev, int32_t* commit_step_dev,
+                    int32_t* forwards_dev);
+
+/*
+ * bd_state_reset -- return a state to the moment right after its prefill
+ *  (the prompt cache is kept), so that a decode can be repeated without
+ *  re-encoding the prompts.  Asynchronous.
+ */
+bd_status bd_state_reset(bd_model* model, bd_state* st);
+
+/* bd_state_steps -- number of denoising steps run on the state so far. */
+bd_status bd_state_steps(const bd_state* st, int32_t* steps_out);
+
+/*
+ * bd_state_stats -- work counters accumulated over the steps run since the
+ *  prefill (or the last reset), copied to host out[0..n), n <= 8:
+ *   [0] forwards executed (steps with at least one row), [1] window rows
+ *   forwarded (sum of M), [2] LM-head rows (masked positions), [3] visible
+ *   query-key pairs per head (block-causal), [4] keys read per kv head
+ *   (prefix + window, summed over sequences), [5] tokens committed.
+ *  Synchronises the stream.
+ */
+bd_status bd_state_stats(bd_model* model, bd_state* st, int64_t* out, int32_t n);
+
+/* Kernel classes timed by bd_profile / bd_profile_read. */
+enum {
+    BD_PROF_EMBED = 0, BD_PROF_NORM = 1, BD_PROF_GEMM_QKV = 2, BD_PROF_ROPE = 3, BD_PROF_ATTN = 4,
+    BD_PROF_GEMM_O = 5, BD_PROF_GEMM_GU = 6, BD_PROF_GEMM_DOWN = 7, BD_PROF_LM_HEAD = 8,
+    BD_PROF_COMMIT = 9, BD_PROF_KINDS = 10
+};
+
+/*
+ * bd_profile -- enable (1) or disable (0) per-launch HIP-event timing of every
+ *  kernel class on the model's stream; clears the accumulated totals.
+ * bd_profile_read -- resolve the recorded events (synchronises) and return
+ *  the accumulated milliseconds and launch counts per class
+ *  (ms_out[BD_PROF_KINDS], count_out[BD_PROF_KINDS]; either may be NULL).
+ */
+bd_status bd_profile(bd_model* model, int32_t enable);
+bd_status bd_profile_read(bd_model* model, double* ms_out, int32_t* count_out);
+
+bd_status bd_state_free(bd_state* st);
+bd_status bd_model_free(bd_model* model);
+
+/* Thread-local description of the last failure ("" if none). */
+const char* bd_last_error(void);
+
+/*
+ * rl_risk_select -- Redline selection (§4.2 steps (ii)-(iv), App. A).
+ *  correct: [m][n] uint8, 1 if configuration j answered prompt i correctly.
+ *  cost: [m], larger is better (TPF).  ref_index: the reference row.
+ *  For each configuration: V[j] = #{i : correct[ref][i] && !correct[j][i]},
+ *  p[j] = Pr[Bin(n, alpha) <= V[j]] (exact binomial tail, App. A.2);
+ *  Holm step-down at level delta (sort p ascending, reject while
+ *  p_(i) <= delta / (m - i + 1), stop at the first failure; App. A.3) marks
+ *  valid[j]; selected = the valid configuration with the largest cost (lowest
+ *  index on ties), or ref_index when none is valid.
+ *  Host-only; touches only the caller's arrays.  Outputs may be NULL except
+ *  selected_out.  Errors: BD_EINVAL when n < 1, m < 1, ref_index outside
+ *  [0, m), alpha outside (0, 1), delta outside (0, 1] or a NULL input.
+ *  near_ties_out (optional) receives the number of Holm comparisons whose
+ *  ratio p / threshold lies within 1e-9 of 1.
+ */
+bd_status rl_risk_select(int32_t n, int32_t m, int32_t ref_index, const uint8_t* correct,
+                         const double* cost, double alpha, double delta, int32_t* V_out,
+                         double* p_out, uint8_t* valid_out, int32_t* selected_out,
+                         int32_t* near_ties_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BD_H */

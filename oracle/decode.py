@@ -106,13 +106,16 @@ class SeqDecoder:
         self._admit()
 
     # -- one denoising step -------------------------------------------------
-    def forward_step(self):
-        """Forward over the window; statistics for every masked position."""
+    def forward_step(self, with_logits: bool = False):
+        """Forward over the window; statistics for every masked position
+        (and their logits when ``with_logits``)."""
         s, e = self.window()
         h = self.model.forward(self.tokens, s, e, self.cache, self.B)
         masked = np.nonzero(self.tokens[s:e] == self.mask_id)[0] + s
         z = self.model.logits(h[masked - s])
         conf, tok, p2 = lm_stats(z)
+        if with_logits:
+            return masked, conf, tok, p2, z
         return masked, conf, tok, p2
 
     def apply(self, positions: np.ndarray, toks: np.ndarray, step: int):

@@ -17,14 +17,15 @@ What is computed, and where it comes from:
 
 Precision modes
   ``"f64"``  every operand and every operation in float64.
-  ``"bf16"`` bfloat16 *storage* emulation: weights are bf16-valued, and the
-             operands that a bf16 kernel stores are rounded (fp64 -> fp32 ->
-             bf16, nearest-even) at exactly these points: RMSNorm outputs that
-             feed a matmul, Q/K/V after RoPE (the KV cache), the attention
-             output before the O projection, the SwiGLU product before the down
-             projection, and the final-norm output before the LM head.  Matmuls
-             on bf16-valued operands run as float32 BLAS (products are exact in
-             fp32); residual stream, softmax, norms and router in float64.
+  ``"bf16"`` bf16 weights with the storage points of the bf16 kernels:
+             * Q, K and V after RoPE are stored as bfloat16 (the KV cache):
+               fp64 -> fp32 -> bf16, nearest-even;
+             * every matmul activation operand (RMSNorm outputs, attention
+               output, SwiGLU product, final-norm output) is carried as fp32
+               and fed as the bf16 pair hi = bf16(x), lo = bf16(x - hi), i.e.
+               x to 16 significant bits;
+             matmuls run as float32 BLAS on those operands; residual stream,
+             attention softmax, norms and router in float64.
 """
 from __future__ import annotations
 
@@ -32,7 +33,7 @@ import math
 
 import numpy as np
 
-__all__ = ["round_bf16", "OracleModel", "KVCache", "lm_stats"]
+__all__ = ["round_bf16", "split_bf16x2", "OracleModel", "KVCache", "lm_stats"]
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:
@@ -46,6 +47,14 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     x32 = np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
     m, e = np.frexp(x32)
     return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)
+
+
+def split_bf16x2(x: np.ndarray) -> np.ndarray:
+    """Value of the bf16 pair (hi, lo) that carries fp32(x): hi = bf16(x),
+    lo = bf16(x - hi) (the difference is exact), returned as hi + lo."""
+    x32 = np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+    hi = round_bf16(x32)
+    return hi + round_bf16(x32 - hi)
 
 
 def _bits_to_float(a: np.ndarray) -> np.ndarray:
@@ -119,8 +128,12 @@ class OracleModel:
 
     # -- storage points ---------------------------------------------------
     def _store(self, x: np.ndarray) -> np.ndarray:
-        """Value as a kernel stores it: bf16 in bf16 mode, unchanged in f64."""
+        """Q/K/V as stored in the cache: bf16 in bf16 mode, unchanged in f64."""
         return round_bf16(x) if self.precision == "bf16" else x
+
+    def _operand(self, x: np.ndarray) -> np.ndarray:
+        """Matmul activation operand: the bf16 pair value in bf16 mode."""
+        return split_bf16x2(x) if self.precision == "bf16" else x
 
     def _mm(self, a: np.ndarray, w: np.ndarray) -> np.ndarray:
         """a @ w.T for a [rows][in] and a weight stored [out][in]."""
@@ -161,7 +174,7 @@ class OracleModel:
         return out
 
     def dense_ffn(self, a: np.ndarray, L) -> np.ndarray:
-        act = self._store(_silu(self._mm(a, L["w_gate"])) * self._mm(a, L["w_up"]))
+        act = self._operand(_silu(self._mm(a, L["w_gate"])) * self._mm(a, L["w_up"]))
         return self._mm(act, L["w_down"])
 
     def router(self, a: np.ndarray, L):
@@ -184,11 +197,11 @@ class OracleModel:
             ae = a[rows]
             g = self._mm(ae, L["w_gate_e"][e])
             u = self._mm(ae, L["w_up_e"][e])
-            y = self._mm(self._store(_silu(g) * u), L["w_down_e"][e])
+            y = self._mm(self._operand(_silu(g) * u), L["w_down_e"][e])
             out[rows] += wts[rows, slot][:, None] * y
         g = self._mm(a, L["w_gate_s"])
         u = self._mm(a, L["w_up_s"])
-        return out + self._mm(self._store(_silu(g) * u), L["w_down_s"])
+        return out + self._mm(self._operand(_silu(g) * u), L["w_down_s"])
 
     # -- forward ------------------------------------------------------------
     def forward(self, tokens: np.ndarray, start: int, end: int, cache: KVCache, B: int) -> np.ndarray:
@@ -204,7 +217,7 @@ class OracleModel:
         x = self.embed[tokens[start:end]].astype(np.float64)
         H, Hkv, hd = self.H, self.Hkv, self.hd
         for li, L in enumerate(self.layers):
-            a = self._store(_rmsnorm(x, L["attn_norm"], cfg.rms_eps))
+            a = self._operand(_rmsnorm(x, L["attn_norm"], cfg.rms_eps))
             qkv = self._mm(a, L["w_qkv"])
             q = qkv[:, :H * hd].reshape(-1, H, hd)
             k = qkv[:, H * hd:(H + Hkv) * hd].reshape(-1, Hkv, hd)
@@ -213,10 +226,10 @@ class OracleModel:
             cache.k[li][start:end] = self._store(self.rope(k, pos))
             cache.v[li][start:end] = self._store(v)
             o = self.attention(q, pos, cache.k[li][:end], cache.v[li][:end], B)
-            x = x + self._mm(self._store(o.reshape(len(pos), H * hd)), L["w_o"])
-            a = self._store(_rmsnorm(x, L["ffn_norm"], cfg.rms_eps))
+            x = x + self._mm(self._operand(o.reshape(len(pos), H * hd)), L["w_o"])
+            a = self._operand(_rmsnorm(x, L["ffn_norm"], cfg.rms_eps))
             x = x + (self.dense_ffn(a, L) if cfg.n_experts == 0 else self.moe_ffn(a, L))
-        return self._store(_rmsnorm(x, self.final_norm, cfg.rms_eps))
+        return self._operand(_rmsnorm(x, self.final_norm, cfg.rms_eps))
 
     def logits(self, h: np.ndarray) -> np.ndarray:
         """Scaled LM-head logits with the mask token's column suppressed."""

@@ -1,0 +1,575 @@
+// Host runtime behind the C ABI in include/bd.h: model binding, decode-state
+// allocation, and the launch sequence of one denoising step.
+//
+// One step = embedding gather of the window rows -> per layer {RMSNorm, QKV
+// GEMM, RoPE + K/V cache write, block-causal attention, O GEMM + residual,
+// RMSNorm, gate/up GEMM with SwiGLU epilogue, down GEMM + residual} -> final
+// RMSNorm of the masked rows -> fused LM-head statistics.  Then the commit
+// kernel applies the threshold rule, sweeps, admits and writes the next plan.
+// Every launch is sized for the largest window and reads the live row counts
+// from the device plan, so the host never waits inside a decode.
+#include "../../include/bd.h"
+#include "bd_internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+#include <vector>
+
+using namespace bd;
+
+static thread_local std::string g_err;
+
+static bd_status fail(bd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                      \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return fail(BD_EHIP, "%s failed: %s (%s:%d)", #expr, hipGetErrorString(e_), __FILE__, \
+                  __LINE__);                                                              \
+  } while (0)
+
+struct LayerW {
+  const float* attn_norm;
+  const void* w_qkv;
+  const void* w_o;
+  const float* ffn_norm;
+  void* w_gu;           // packed gate/up (library-owned)
+  const void* w_down;
+};
+
+struct bd_model {
+  bd_model_cfg cfg;
+  bool bf16;
+  size_t esz;
+  hipStream_t stream;
+  const void* embed;
+  std::vector<LayerW> layers;
+  const float* final_norm;
+  const void* lm_head;
+  std::vector<void*> owned;
+  double* inv_freq;
+  int32_t* err_flag;
+  // optional per-kernel-class timing with HIP events on the model's stream
+  bool prof = false;
+  std::vector<hipEvent_t> ev_pool;
+  struct Rec { int kind; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  double prof_ms[BD_PROF_KINDS] = {};
+  int prof_n[BD_PROF_KINDS] = {};
+};
+
+static hipEvent_t take_event(bd_model* m) {
+  if (!m->ev_pool.empty()) {
+    hipEvent_t e = m->ev_pool.back();
+    m->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct ProfScope {
+  bd_model* m;
+  int kind;
+  hipEvent_t a = nullptr;
+  ProfScope(bd_model* m_, int k) : m(m_), kind(k) {
+    if (m->prof && (a = take_event(m))) (void)hipEventRecord(a, m->stream);
+  }
+  ~ProfScope() {
+    if (!a) return;
+    hipEvent_t b = take_event(m);
+    if (!b) return;
+    (void)hipEventRecord(b, m->stream);
+    m->recs.push_back({kind, a, b});
+  }
+};
+
+#define LAUNCH(kind, expr)            \
+  do {                                \
+    ProfScope ps_(m, (kind));         \
+    HIPCHK(expr);                     \
+  } while (0)
+
+struct bd_state {
+  int b, P, G, B, nb;
+  float tau;
+  int maxpos, rows_step, rows_pre, rows_cap, lm_cap, win_step;
+  int32_t *tokens, *commit_step, *seq_state, *commit_flag;
+  int32_t* plan_buf[3];
+  PlanView plan[3];      // [0], [1]: step plans (ping-pong); [2]: prefill
+  int cur;
+  float* X;
+  void* A;
+  float* QKV;
+  void* Qb;
+  void* Ob;
+  void* Hact;
+  void* Alm;
+  float *pmax, *psum;
+  int32_t* parg;
+  float* conf;
+  int32_t* tok;
+  float* logits_tmp;
+  void* Kc;
+  void* Vc;
+  int steps;
+  bool pending;
+  int32_t* host_flag;    // pinned
+  long long* stats;      // device [8]
+  std::vector<void*> allocs;
+};
+
+static int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+static bd_status dev_alloc(bd_state* s, void** p, size_t bytes) {
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) return fail(BD_ENOMEM, "hipMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+  s->allocs.push_back(*p);
+  return BD_OK;
+}
+
+extern "C" const char* bd_last_error(void) { return g_err.c_str(); }
+
+namespace bd {
+void set_error(const char* msg) { g_err = msg; }
+}
+
+extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w, int32_t n_weights,
+                                   void* stream, bd_model** out) {
+  if (!cfg || !w || !out) return fail(BD_EINVAL, "NULL argument");
+  *out = nullptr;
+  const bd_model_cfg& c = *cfg;
+  if (c.n_layers < 1 || c.d_model < 1 || c.n_heads < 1 || c.n_kv_heads < 1 || c.vocab < 2)
+    return fail(BD_EINVAL, "non-positive model dimension");
+  if (c.head_dim != 64 && c.head_dim != 128) return fail(BD_EINVAL, "head_dim must be 64 or 128");
+  if (c.n_heads % c.n_kv_heads) return fail(BD_EINVAL, "n_heads must be a multiple of n_kv_heads");
+  if (c.mask_id < 0 || c.mask_id >= c.vocab) return fail(BD_EINVAL, "mask_id outside [0, vocab)");
+  if (c.dtype != BD_F32 && c.dtype != BD_BF16) return fail(BD_EINVAL, "unknown dtype");
+  if (c.n_experts != 0) return fail(BD_EUNSUPPORTED, "MoE layers are not supported by this build");
+  if (c.ffn_dim < 16 || c.ffn_dim % 16) return fail(BD_EINVAL, "ffn_dim must be a positive multiple of 16");
+  const int per_layer = 7;
+  const int need = 1 + per_layer * c.n_layers + 2;
+  if (n_weights != need) return fail(BD_EINVAL, "expected %d weight tensors, got %d", need, n_weights);
+  for (int i = 0; i < n_weights; ++i)
+    if (!w[i]) return fail(BD_EINVAL, "weight %d is NULL", i);
+  const bool bf16 = c.dtype == BD_BF16;
+  // GEMM tiling constraints (bf16: N % 128, K % 32; f32: N % 64, K % 16)
+  const int nq = bf16 ? 128 : 64, kq = bf16 ? 32 : 16;
+  const int qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+  if (qkv % nq || c.d_model % nq || c.vocab % nq || (2 * c.ffn_dim) % nq || c.d_model % kq ||
+      (c.n_heads * c.head_dim) % kq || c.ffn_dim % kq)
+    return fail(BD_EUNSUPPORTED, "dimensions do not fit the GEMM tiles (N %% %d, K %% %d)", nq, kq);
+
+  bd_model* m = new bd_model();
+  m->cfg = c;
+  m->bf16 = bf16;
+  m->esz = bf16 ? 2 : 4;
+  m->stream = (hipStream_t)stream;
+  int t = 0;
+  m->embed = w[t++];
+  m->layers.resize(c.n_layers);
+  const size_t row_bytes = (size_t)c.d_model * m->esz;
+  for (int l = 0; l < c.n_layers; ++l) {
+    LayerW& L = m->layers[l];
+    L.attn_norm = (const float*)w[t++];
+    L.w_qkv = w[t++];
+    L.w_o = w[t++];
+    L.ffn_norm = (const float*)w[t++];
+    const void* gate = w[t++];
+    const void* up = w[t++];
+    L.w_down = w[t++];
+    void* packed = nullptr;
+    hipError_t e = hipMalloc(&packed, 2 * (size_t)c.ffn_dim * row_bytes);
+    if (e != hipSuccess) {
+      bd_model_free(m);
+      return fail(BD_ENOMEM, "hipMalloc for packed gate/up failed");
+    }
+    m->owned.push_back(packed);
+    L.w_gu = packed;
+    e = launch_pack_gate_up(gate, up, packed, c.ffn_dim, row_bytes, m->stream);
+    if (e != hipSuccess) {
+      bd_model_free(m);
+      return fail(BD_EHIP, "pack gate/up: %s", hipGetErrorString(e));
+    }
+  }
+  m->final_norm = (const float*)w[t++];
+  m->lm_head = w[t++];
+  std::vector<double> inv(c.head_dim / 2);
+  for (int i = 0; i < c.head_dim / 2; ++i)
+    inv[i] = pow((double)c.rope_theta, -2.0 * i / (double)c.head_dim);
+  hipError_t e1 = hipMalloc((void**)&m->inv_freq, inv.size() * sizeof(double));
+  hipError_t e2 = hipMalloc((void**)&m->err_flag, 64);
+  if (e1 != hipSuccess || e2 != hipSuccess) {
+    bd_model_free(m);
+    return fail(BD_ENOMEM, "hipMalloc failed");
+  }
+  m->owned.push_back(m->inv_freq);
+  m->owned.push_back(m->err_flag);
+  hipError_t e = hipMemcpyAsync(m->inv_freq, inv.data(), inv.size() * sizeof(double),
+                                hipMemcpyHostToDevice, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(m->err_flag, 0, 64, m->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+  if (e != hipSuccess) {
+    bd_model_free(m);
+    return fail(BD_EHIP, "model upload: %s", hipGetErrorString(e));
+  }
+  *out = m;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_model_free(bd_model* m) {
+  if (!m) return BD_OK;
+  if (m->stream) (void)hipStreamSynchronize(m->stream);
+  else (void)hipDeviceSynchronize();
+  for (void* p : m->owned) (void)hipFree(p);
+  for (auto& r : m->recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+  for (hipEvent_t e : m->ev_pool) (void)hipEventDestroy(e);
+  delete m;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_state_free(bd_state* s) {
+  if (!s) return BD_OK;
+  (void)hipDeviceSynchronize();
+  for (void* p : s->allocs) (void)hipFree(p);
+  if (s->host_flag) (void)hipHostFree(s->host_flag);
+  delete s;
+  return BD_OK;
+}
+
+// One forward over the rows of `plan`; with `lm` the masked rows get the LM head.
+static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int rows_cap,
+                             int win_cap, bool lm) {
+  const bd_model_cfg& c = m->cfg;
+  const bool bf = m->bf16;
+  const hipStream_t st = m->stream;
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+  const int qkv = (H + 2 * Hkv) * hd;
+  const size_t layer_kv = (size_t)s->b * Hkv * s->maxpos * hd * m->esz;
+  LAUNCH(BD_PROF_EMBED, launch_embed(bf, s->tokens, s->P + s->G, m->embed, d, c.vocab, plan,
+                                     rows_cap, s->X, m->err_flag, st));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const LayerW& L = m->layers[l];
+    void* Kl = (char*)s->Kc + l * layer_kv;
+    void* Vl = (char*)s->Vc + l * layer_kv;
+    LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.attn_norm, d, c.rms_eps, plan.hdr, nullptr,
+                                        rows_cap, s->A, st));
+    LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, L.w_qkv, d, qkv, d, plan.hdr,
+                                         rows_cap, s->QKV, qkv, st));
+    LAUNCH(BD_PROF_ROPE, launch_rope_kv(bf, s->QKV, plan, rows_cap, H, Hkv, hd, m->inv_freq, s->Qb,
+                                        Kl, Vl, s->maxpos, st));
+    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, Kl, Vl, s->Ob, plan, s->b, win_cap, H, Hkv, hd,
+                                          s->maxpos, s->B, st));
+    LAUNCH(BD_PROF_GEMM_O, launch_gemm(EPI_ADD_F32, bf, s->Ob, H * hd, L.w_o, H * hd, d, H * hd,
+                                       plan.hdr, rows_cap, s->X, d, st));
+    LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
+                                        rows_cap, s->A, st));
+    LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, L.w_gu, d, 2 * F, d, plan.hdr,
+                                        rows_cap, s->Hact, F, st));
+    LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, bf, s->Hact, F, L.w_down, F, d, F, plan.hdr,
+                                          rows_cap, s->X, d, st));
+  }
+  if (lm) {
+    LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, m->final_norm, d, c.rms_eps, plan.hdr + 1,
+                                        plan.lm_row, s->lm_cap, s->Alm, st));
+    LAUNCH(BD_PROF_LM_HEAD, launch_lm_head(bf, s->Alm, d, m->lm_head, c.vocab, c.mask_id,
+                                           c.logit_scale, plan.hdr + 1, s->lm_cap, s->pmax, s->psum,
+                                           s->parg, s->conf, s->tok, st));
+  }
+  return BD_OK;
+}
+
+static bd_status check_err_flag(bd_model* m) {
+  int32_t flag = 0;
+  HIPCHK(hipMemcpyAsync(&flag, m->err_flag, sizeof flag, hipMemcpyDeviceToHost, m->stream));
+  HIPCHK(hipStreamSynchronize(m->stream));
+  if (flag) {
+    HIPCHK(hipMemsetAsync(m->err_flag, 0, sizeof flag, m->stream));
+    return fail(BD_EINVAL, "token id outside [0, vocab) in a prompt");
+  }
+  return BD_OK;
+}
+
+extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
+                                const bd_decode_cfg* cfg, bd_state** out) {
+  if (!m || !cfg || !out) return fail(BD_EINVAL, "NULL argument");
+  *out = nullptr;
+  const int B = cfg->block_size, nb = cfg->n_inflight;
+  if (b < 1 || P < 0 || G < 1 || B < 1 || nb < 1) return fail(BD_EINVAL, "need b, G, B, n_inflight >= 1 and P >= 0");
+  if (P % B || G % B) return fail(BD_EINVAL, "P and G must be multiples of the block size");
+  if (isnan(cfg->tau)) return fail(BD_EINVAL, "tau is NaN");
+  if (P > 0 && !prompt) return fail(BD_EINVAL, "NULL prompt");
+  if (b > 256) return fail(BD_EUNSUPPORTED, "at most 256 sequences per state");
+  if (nb > 8) return fail(BD_EUNSUPPORTED, "at most 8 in-flight blocks");
+  const bd_model_cfg& c = m->cfg;
+
+  bd_state* s = new bd_state();
+  s->b = b; s->P = P; s->G = G; s->B = B; s->nb = nb; s->tau = cfg->tau;
+  s->maxpos = P + G;
+  s->win_step = 2 * nb * B;
+  s->rows_step = round_up(b * s->win_step, 256);
+  s->rows_pre = round_up(b * P, 256);
+  s->rows_cap = s->rows_step > s->rows_pre ? s->rows_step : s->rows_pre;
+  s->lm_cap = round_up(b * nb * B, 256);
+  const size_t esz = m->esz;
+  const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim;
+  const int qkv = (H + 2 * Hkv) * hd;
+  const int ntiles = c.vocab / (m->bf16 ? 128 : 64);
+  bd_status r = BD_OK;
+#define ALLOC(ptr, bytes)                                      \
+  do {                                                         \
+    if ((r = dev_alloc(s, (void**)&(ptr), (bytes))) != BD_OK) { \
+      bd_state_free(s);                                        \
+      return r;                                                \
+    }                                                          \
+  } while (0)
+  ALLOC(s->tokens, (size_t)b * (P + G) * 4);
+  ALLOC(s->commit_step, (size_t)b * G * 4);
+  ALLOC(s->seq_state, (size_t)b * SS_N * 4);
+  ALLOC(s->stats, 8 * sizeof(long long));
+  ALLOC(s->commit_flag, (size_t)s->lm_cap * 4);
+  for (int i = 0; i < 3; ++i) {
+    const int rc = i < 2 ? s->rows_step : s->rows_pre;
+    ALLOC(s->plan_buf[i], plan_words(rc, s->lm_cap, b) * 4);
+    s->plan[i] = plan_view(s->plan_buf[i], rc, s->lm_cap, b);
+  }
+  ALLOC(s->X, (size_t)s->rows_cap * d * 4);
+  ALLOC(s->A, (size_t)s->rows_cap * d * 4);
+  ALLOC(s->QKV, (size_t)s->rows_cap * qkv * 4);
+  ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * esz);
+  ALLOC(s->Ob, (size_t)s->rows_cap * H * hd * 4);
+  ALLOC(s->Hact, (size_t)s->rows_cap * c.ffn_dim * 4);
+  ALLOC(s->Alm, (size_t)s->lm_cap * d * 4);
+  ALLOC(s->pmax, (size_t)ntiles * s->lm_cap * 4);
+  ALLOC(s->psum, (size_t)ntiles * s->lm_cap * 4);
+  ALLOC(s->parg, (size_t)ntiles * s->lm_cap * 4);
+  ALLOC(s->conf, (size_t)s->lm_cap * 4);
+  ALLOC(s->tok, (size_t)s->lm_cap * 4);
+  const size_t kv_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * esz;
+  ALLOC(s->Kc, kv_bytes);
+  ALLOC(s->Vc, kv_bytes);
+#undef ALLOC
+  if (hipHostMalloc((void**)&s->host_flag, 64, hipHostMallocDefault) != hipSuccess) {
+    s->host_flag = nullptr;
+    bd_state_free(s);
+    return fail(BD_ENOMEM, "hipHostMalloc failed");
+  }
+  // Row buffers are read in whole GEMM tiles: clear them once so that rows
+  // past the live count never hold NaN patterns.
+  hipError_t e = hipMemsetAsync(s->A, 0, (size_t)s->rows_cap * d * 4, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(s->Ob, 0, (size_t)s->rows_cap * H * hd * 4, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(s->Hact, 0, (size_t)s->rows_cap * c.ffn_dim * 4, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(s->Alm, 0, (size_t)s->lm_cap * d * 4, m->stream);
+  if (e != hipSuccess) {
+    bd_state_free(s);
+    return fail(BD_EHIP, "hipMemsetAsync: %s", hipGetErrorString(e));
+  }
+  InitArgs ia;
+  ia.plan = s->plan[0];
+  ia.prefill = s->plan[2];
+  ia.tokens = s->tokens;
+  ia.prompt = P > 0 ? prompt : nullptr;
+  ia.commit_step = s->commit_step;
+  ia.seq_state = s->seq_state;
+  ia.b = b; ia.P = P; ia.G = G; ia.B = B; ia.nb = nb; ia.mask_id = c.mask_id; ia.vocab = c.vocab;
+  ia.err_flag = m->err_flag;
+  ia.stats = s->stats;
+  e = launch_init_decode(ia, m->stream);
+  if (e != hipSuccess) {
+    bd_state_free(s);
+    return fail(BD_EHIP, "init kernel: %s", hipGetErrorString(e));
+  }
+  s->cur = 0;
+  if (P > 0) {
+    r = run_forward(m, s, s->plan[2], s->rows_pre, P, false);
+    if (r != BD_OK) {
+      bd_state_free(s);
+      return r;
+    }
+  }
+  *out = s;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_state_reset(bd_model* m, bd_state* s) {
+  if (!m || !s) return fail(BD_EINVAL, "NULL argument");
+  InitArgs ia;
+  ia.plan = s->plan[0];
+  ia.prefill = PlanView{};
+  ia.prefill.hdr = nullptr;
+  ia.tokens = s->tokens;
+  ia.prompt = nullptr;
+  ia.commit_step = s->commit_step;
+  ia.seq_state = s->seq_state;
+  ia.b = s->b; ia.P = s->P; ia.G = s->G; ia.B = s->B; ia.nb = s->nb;
+  ia.mask_id = m->cfg.mask_id; ia.vocab = m->cfg.vocab; ia.err_flag = m->err_flag;
+  ia.stats = s->stats;
+  HIPCHK(launch_init_decode(ia, m->stream));
+  s->cur = 0;
+  s->steps = 0;
+  s->pending = false;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_state_steps(const bd_state* s, int32_t* out) {
+  if (!s || !out) return fail(BD_EINVAL, "NULL argument");
+  *out = s->steps;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_denoise_step(bd_model* m, bd_state* s, float* conf_dev, int32_t* tok_dev,
+                                     float* logits_dev) {
+  if (!m || !s) return fail(BD_EINVAL, "NULL argument");
+  if (s->pending) return fail(BD_ESTATE, "previous step not committed");
+  const PlanView& plan = s->plan[s->cur];
+  bd_status r = run_forward(m, s, plan, s->rows_step, s->win_step, true);
+  if (r != BD_OK) return r;
+  const bd_model_cfg& c = m->cfg;
+  if (conf_dev || tok_dev)
+    HIPCHK(launch_scatter_stats(s->conf, s->tok, plan, s->P, s->G, conf_dev, tok_dev, s->lm_cap,
+                                m->stream));
+  if (logits_dev) {
+    if (!s->logits_tmp) {
+      if ((r = dev_alloc(s, (void**)&s->logits_tmp, (size_t)s->lm_cap * c.vocab * 4)) != BD_OK) return r;
+    }
+    HIPCHK(launch_lm_logits(m->bf16, s->Alm, c.d_model, m->lm_head, c.vocab, c.mask_id, c.logit_scale,
+                            plan.hdr + 1, s->lm_cap, s->logits_tmp, m->stream));
+    HIPCHK(launch_scatter_logits(s->logits_tmp, plan, c.vocab, s->P, s->G, logits_dev, s->lm_cap,
+                                 m->stream));
+  }
+  s->pending = true;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_commit(bd_model* m, bd_state* s, int32_t* all_done_host) {
+  if (!m || !s) return fail(BD_EINVAL, "NULL argument");
+  if (!s->pending) return fail(BD_ESTATE, "no denoising step to commit");
+  CommitArgs a;
+  a.in = s->plan[s->cur];
+  a.out = s->plan[s->cur ^ 1];
+  a.conf = s->conf;
+  a.tok = s->tok;
+  a.tokens = s->tokens;
+  a.tok_stride = s->P + s->G;
+  a.commit_step = s->commit_step;
+  a.seq_state = s->seq_state;
+  a.commit_flag = s->commit_flag;
+  a.b = s->b; a.P = s->P; a.G = s->G; a.B = s->B; a.nb = s->nb;
+  a.mask_id = m->cfg.mask_id;
+  a.step = s->steps;
+  a.tau = s->tau;
+  a.stats = s->stats;
+  LAUNCH(BD_PROF_COMMIT, launch_commit(a, m->stream));
+  s->cur ^= 1;
+  s->steps += 1;
+  s->pending = false;
+  if (all_done_host) {
+    HIPCHK(hipMemcpyAsync(s->host_flag, s->plan[s->cur].hdr + 2, 4, hipMemcpyDeviceToHost, m->stream));
+    HIPCHK(hipStreamSynchronize(m->stream));
+    *all_done_host = s->host_flag[0];
+    bd_status r = check_err_flag(m);
+    if (r != BD_OK) return r;
+  }
+  return BD_OK;
+}
+
+__global__ void k_read_trace(const int32_t* __restrict__ tokens, const int32_t* __restrict__ cs,
+                             const int32_t* __restrict__ ss, int b, int P, int G,
+                             int32_t* __restrict__ t_out, int32_t* __restrict__ c_out,
+                             int32_t* __restrict__ f_out) {
+  const int s = blockIdx.x;
+  for (int j = threadIdx.x; j < G; j += blockDim.x) {
+    if (t_out) t_out[(size_t)s * G + j] = tokens[(size_t)s * (P + G) + P + j];
+    if (c_out) c_out[(size_t)s * G + j] = cs[(size_t)s * G + j];
+  }
+  if (f_out && threadIdx.x == 0) f_out[s] = ss[s * SS_N + SS_FORWARDS];
+}
+
+extern "C" bd_status bd_state_read(bd_model* m, bd_state* s, int32_t* tokens_dev,
+                                   int32_t* commit_step_dev, int32_t* forwards_dev) {
+  if (!m || !s) return fail(BD_EINVAL, "NULL argument");
+  k_read_trace<<<s->b, 256, 0, m->stream>>>(s->tokens, s->commit_step, s->seq_state, s->b, s->P, s->G,
+                                            tokens_dev, commit_step_dev, forwards_dev);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(m->stream));
+  return check_err_flag(m);
+}
+
+extern "C" bd_status bd_decode(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
+                               const bd_decode_cfg* cfg, int32_t* tokens_dev, int32_t* commit_step_dev,
+                               int32_t* forwards_dev) {
+  bd_state* s = nullptr;
+  bd_status r = bd_prefill(m, prompt, b, P, G, cfg, &s);
+  if (r != BD_OK) return r;
+  // Each step commits at least one token of every unfinished sequence, so G
+  // steps always suffice; the host checks the device flag every few steps
+  // (steps after completion are empty launches).
+  const int check = 4;
+  int32_t done = 0;
+  while (!done) {
+    for (int k = 0; k < check && r == BD_OK; ++k) {
+      r = bd_denoise_step(m, s, nullptr, nullptr, nullptr);
+      if (r == BD_OK) r = bd_commit(m, s, (k == check - 1) ? &done : nullptr);
+    }
+    if (r != BD_OK) break;
+    if (!done && s->steps > G + check) {
+      r = fail(BD_ESTATE, "decode did not finish within %d steps", s->steps);
+      break;
+    }
+  }
+  if (r == BD_OK) r = bd_state_read(m, s, tokens_dev, commit_step_dev, forwards_dev);
+  bd_state_free(s);
+  return r;
+}
+
+extern "C" bd_status bd_state_stats(bd_model* m, bd_state* s, int64_t* out, int32_t n) {
+  if (!m || !s || !out || n < 1 || n > 8) return fail(BD_EINVAL, "bad arguments");
+  long long tmp[8];
+  HIPCHK(hipMemcpyAsync(tmp, s->stats, sizeof tmp, hipMemcpyDeviceToHost, m->stream));
+  HIPCHK(hipStreamSynchronize(m->stream));
+  for (int i = 0; i < n; ++i) out[i] = (int64_t)tmp[i];
+  return BD_OK;
+}
+
+extern "C" bd_status bd_profile(bd_model* m, int32_t enable) {
+  if (!m) return fail(BD_EINVAL, "NULL model");
+  HIPCHK(hipStreamSynchronize(m->stream));
+  for (auto& r : m->recs) { m->ev_pool.push_back(r.a); m->ev_pool.push_back(r.b); }
+  m->recs.clear();
+  for (int k = 0; k < BD_PROF_KINDS; ++k) { m->prof_ms[k] = 0.0; m->prof_n[k] = 0; }
+  m->prof = enable != 0;
+  return BD_OK;
+}
+
+extern "C" bd_status bd_profile_read(bd_model* m, double* ms_out, int32_t* count_out) {
+  if (!m) return fail(BD_EINVAL, "NULL model");
+  HIPCHK(hipStreamSynchronize(m->stream));
+  for (auto& r : m->recs) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, r.a, r.b));
+    m->prof_ms[r.kind] += ms;
+    m->prof_n[r.kind] += 1;
+    m->ev_pool.push_back(r.a);
+    m->ev_pool.push_back(r.b);
+  }
+  m->recs.clear();
+  for (int k = 0; k < BD_PROF_KINDS; ++k) {
+    if (ms_out) ms_out[k] = m->prof_ms[k];
+    if (count_out) count_out[k] = m->prof_n[k];
+  }
+  return BD_OK;
+}

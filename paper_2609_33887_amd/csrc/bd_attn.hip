@@ -1,0 +1,250 @@
+// Block-causal attention over the KV cache (paper §2.1): a query at absolute
+// position p attends to every key j with j / B <= p / B, i.e. the cached
+// prefix, every earlier block and its own block (bidirectionally).  Window
+// K/V have already been written into the cache at their absolute positions,
+// so one key range [0, end of the query's block) covers prefix and window.
+//
+// bf16 kernel: one workgroup = 64 query rows of one head (4 wave64s x 16
+// queries).  Key tiles of 64 positions stream from HBM through LDS with
+// 16-byte coalesced loads (K row-major, V transposed), and the wave computes
+// S^T = K Q^T and O^T += V^T P^T with MFMA 16x16x32 bf16 (P^T as a hi/lo
+// bf16 pair, the fp32 output unrounded), so each lane owns
+// one query column: the online-softmax state and the O rescale stay in the
+// lane, and P^T is fed to the second MFMA straight from the score registers
+// (the two products use the same permutation of the key index).  The block
+// mask is applied in registers, only on tiles that reach the query's block.
+#include "bd_internal.h"
+
+#include <math.h>
+
+namespace bd {
+
+__device__ __forceinline__ float bf2f_a(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ bf16_t f2bf_a(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+constexpr int AQ = 64;    // query rows per workgroup
+constexpr int AK = 64;    // keys per tile
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
+                                                   const bf16_t* __restrict__ Kc,
+                                                   const bf16_t* __restrict__ Vc,
+                                                   float* __restrict__ O,
+                                                   const int32_t* __restrict__ seq_row_start,
+                                                   const int32_t* __restrict__ seq_win_len,
+                                                   const int32_t* __restrict__ seq_win_start, int H,
+                                                   int Hkv, int maxpos, int B, float scale_log2) {
+  constexpr int KP = HD + 8;        // padded K row (elements)
+  constexpr int VP = AK + 8;        // padded transposed-V row
+  __shared__ __attribute__((aligned(16))) bf16_t sK[AK * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t sVt[HD * VP];
+
+  const int s = blockIdx.z, h = blockIdx.y, qt = blockIdx.x;
+  const int W = seq_win_len[s];
+  if (qt * AQ >= W) return;
+  const int row0 = seq_row_start[s] + qt * AQ;
+  const int nrows = min(AQ, W - qt * AQ);
+  const int pos0 = seq_win_start[s] + qt * AQ;
+  const int kend = ((pos0 + nrows - 1) / B + 1) * B;        // keys [0, kend)
+  const int kv = h / (H / Hkv);
+  const size_t kvbase = ((size_t)s * Hkv + kv) * (size_t)maxpos * HD;
+  const bf16_t* Kp = Kc + kvbase;
+  const bf16_t* Vp = Vc + kvbase;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int q = wave * 16 + c;                                // query row in tile
+  const bool qvalid = q < nrows;
+  const int qpos = pos0 + q;
+  const int qend = ((qpos / B) + 1) * B;                      // this query's key bound
+
+  // Q^T fragments (B operand of S^T = K Q^T): dims [32 kc + 8 g, +8) of query c.
+  bf16x8 qf[HD / 32];
+#pragma unroll
+  for (int kc = 0; kc < HD / 32; ++kc) {
+    if (qvalid)
+      qf[kc] = *(const bf16x8*)(Q + ((size_t)(row0 + q) * H + h) * HD + kc * 32 + g * 8);
+    else
+      qf[kc] = bf16x8{};
+  }
+  floatx4 oacc[HD / 16];
+#pragma unroll
+  for (int t = 0; t < HD / 16; ++t) oacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_part = 0.f;
+
+  const int ntiles = (kend + AK - 1) / AK;
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int k0 = kt * AK;
+    // stage K (row-major) and V (transposed) tiles; keys >= kend are zero
+    constexpr int CH = AK * HD / 8;                            // 16-byte chunks per tile
+#pragma unroll
+    for (int it = 0; it < CH / 256; ++it) {
+      const int ci = tid + 256 * it;
+      const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
+      uint4 kvv = make_uint4(0, 0, 0, 0), vvv = make_uint4(0, 0, 0, 0);
+      if (k0 + key < kend) {
+        kvv = *(const uint4*)(Kp + (size_t)(k0 + key) * HD + dc);
+        vvv = *(const uint4*)(Vp + (size_t)(k0 + key) * HD + dc);
+      }
+      *(uint4*)(sK + key * KP + dc) = kvv;
+      const bf16_t* vv = (const bf16_t*)&vvv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sVt[(dc + e) * VP + key] = vv[e];
+    }
+    __syncthreads();
+
+    // S^T sub-tiles: keys st*16 + 4g + r, query c
+    float sv[4][4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      floatx4 a = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < HD / 32; ++kc) {
+        const bf16x8 kf = *(const bf16x8*)(sK + (st * 16 + c) * KP + kc * 32 + g * 8);
+        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], a, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sv[st][r] = a[r];
+    }
+    // In this lane, score (st, r) belongs to key k0 + st*16 + 4g + r of query c.
+    const bool need_mask = (k0 + AK > qend) || !qvalid;
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = sv[st][r] * scale_log2;
+        if (need_mask) {
+          const int key = k0 + st * 16 + 4 * g + r;
+          if (!qvalid || key >= qend) x = -INFINITY;
+        }
+        sv[st][r] = x;
+        tmax = fmaxf(tmax, x);
+      }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float m_new = fmaxf(m_run, tmax);
+    const float m_ref = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = exp2f(m_run - m_ref);
+    m_run = m_new;
+    l_part *= alpha;
+#pragma unroll
+    for (int t = 0; t < HD / 16; ++t) oacc[t] *= alpha;
+    // P^T as a hi/lo bf16 pair (p = hi + lo to 16 significant bits)
+    bf16x8 ph[2], pl[2];
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = exp2f(sv[st][r] - m_ref);
+        l_part += p;
+        const bf16_t hb = f2bf_a(p);
+        const bf16_t lb = f2bf_a(p - bf2f_a(hb));
+        ph[st >> 1][(st & 1) * 4 + r] = __builtin_bit_cast(__bf16, hb);
+        pl[st >> 1][(st & 1) * 4 + r] = __builtin_bit_cast(__bf16, lb);
+      }
+    // O^T += V^T P^T over 2 chunks of 32 keys; k-slot 8g+r <-> key 32kc+4g+r,
+    // k-slot 8g+4+r <-> key 32kc+16+4g+r (same permutation as the scores).
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+#pragma unroll
+      for (int t = 0; t < HD / 16; ++t) {
+        const bf16_t* vrow = sVt + (t * 16 + c) * VP + kc * 32 + 4 * g;
+        const bf16x4 lo = *(const bf16x4*)(vrow);
+        const bf16x4 hi = *(const bf16x4*)(vrow + 16);
+        bf16x8 vf;
+        vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
+        vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[kc], oacc[t], 0, 0, 0);
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[kc], oacc[t], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  float l = l_part;
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  if (qvalid) {
+    const float inv = 1.0f / l;
+    float* orow = O + (size_t)(row0 + q) * H * HD + h * HD;
+#pragma unroll
+    for (int t = 0; t < HD / 16; ++t) {
+      // O^T tile t: lane holds dims t*16 + 4g + r of query c
+      *(float4*)(orow + t * 16 + 4 * g) =
+          make_float4(oacc[t][0] * inv, oacc[t][1] * inv, oacc[t][2] * inv, oacc[t][3] * inv);
+    }
+  }
+}
+
+// fp32 reference-precision kernel for small fp32 models: one wave64 per
+// (query row, head); each lane owns head_dim/64 output dims and keys are
+// scanned with an online softmax.
+__global__ __launch_bounds__(256) void k_attn_f32(const float* __restrict__ Q,
+                                                  const float* __restrict__ Kc,
+                                                  const float* __restrict__ Vc,
+                                                  float* __restrict__ O,
+                                                  const int32_t* __restrict__ row_seq,
+                                                  const int32_t* __restrict__ row_pos,
+                                                  const int32_t* __restrict__ Mp, int H, int Hkv,
+                                                  int hd, int maxpos, int B, float scale) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int item = blockIdx.x * 4 + wave;
+  const int r = item / H, h = item % H;
+  if (r >= *Mp) return;
+  const int s = row_seq[r], pos = row_pos[r];
+  const int kend = (pos / B + 1) * B;
+  const int kv = h / (H / Hkv);
+  const float* Kp = Kc + ((size_t)s * Hkv + kv) * (size_t)maxpos * hd;
+  const float* Vp = Vc + ((size_t)s * Hkv + kv) * (size_t)maxpos * hd;
+  const float* q = Q + ((size_t)r * H + h) * hd;
+  const int per = hd / 64;   // 1 or 2
+  float qv[2] = {0.f, 0.f}, acc[2] = {0.f, 0.f};
+  for (int e = 0; e < per; ++e) qv[e] = q[lane * per + e];
+  float m = -INFINITY, l = 0.f;
+  for (int j = 0; j < kend; ++j) {
+    float part = 0.f;
+    for (int e = 0; e < per; ++e) part += qv[e] * Kp[(size_t)j * hd + lane * per + e];
+    for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
+    const float sc = part * scale;
+    const float mn = fmaxf(m, sc);
+    const float a = expf(m - mn), p = expf(sc - mn);
+    l = l * a + p;
+    for (int e = 0; e < per; ++e) acc[e] = acc[e] * a + p * Vp[(size_t)j * hd + lane * per + e];
+    m = mn;
+  }
+  float* o = O + (size_t)r * H * hd + h * hd;
+  for (int e = 0; e < per; ++e) o[lane * per + e] = acc[e] / l;
+}
+
+hipError_t launch_attention(bool is_bf16, const void* Q, const void* Kc, const void* Vc, void* O,
+                            PlanView plan, int b, int win_cap, int H, int Hkv, int hd, int maxpos,
+                            int B, hipStream_t st) {
+  if (is_bf16) {
+    const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
+    dim3 grid((win_cap + AQ - 1) / AQ, H, b);
+    if (hd == 128)
+      k_attn_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)Q, (const bf16_t*)Kc, (const bf16_t*)Vc,
+                                             (float*)O, plan.seq_row_start, plan.seq_win_len,
+                                             plan.seq_win_start, H, Hkv, maxpos, B, scale_log2);
+    else if (hd == 64)
+      k_attn_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)Q, (const bf16_t*)Kc, (const bf16_t*)Vc,
+                                            (float*)O, plan.seq_row_start, plan.seq_win_len,
+                                            plan.seq_win_start, H, Hkv, maxpos, B, scale_log2);
+    else
+      return hipErrorInvalidValue;
+  } else {
+    if (hd != 64 && hd != 128) return hipErrorInvalidValue;
+    const int rows_cap = win_cap * b;
+    const int items = rows_cap * H;
+    k_attn_f32<<<(items + 3) / 4, 256, 0, st>>>((const float*)Q, (const float*)Kc, (const float*)Vc,
+                                                (float*)O, plan.row_seq, plan.row_pos, plan.hdr, H,
+                                                Hkv, hd, maxpos, B, (float)(1.0 / sqrt((double)hd)));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace bd

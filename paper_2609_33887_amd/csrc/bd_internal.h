@@ -1,0 +1,136 @@
+// Internal declarations shared by the HIP sources of the block-diffusion
+// library (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bd {
+
+typedef uint16_t bf16_t;   // bfloat16 bit pattern in memory
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Per-sequence decode descriptor, int32 fields of seq_state[b][SS_N].
+enum {
+  SS_CACHE_LEN = 0,   // positions [0, cache_len) hold K/V from clean tokens
+  SS_N_PEND = 1,      // committed blocks awaiting their cache write
+  SS_FIRST_ACT = 2,   // generation-block index of the first active block
+  SS_N_ACT = 3,       // active blocks
+  SS_NEXT_BLK = 4,    // first block not yet admitted
+  SS_DONE = 5,
+  SS_FORWARDS = 6,
+  SS_N = 8
+};
+
+// Step plan: which rows the next forward runs and which get an LM head.
+// Layout inside one int32 buffer (see plan_* helpers).
+struct PlanView {
+  int32_t* hdr;          // [0] = M rows, [1] = M_lm rows, [2] = all_done
+  int32_t* row_seq;      // [rows_cap]
+  int32_t* row_pos;      // [rows_cap] absolute position of the row
+  int32_t* lm_row;       // [lm_cap]   index into rows, ascending
+  int32_t* seq_row_start;  // [b]
+  int32_t* seq_win_len;    // [b]
+  int32_t* seq_win_start;  // [b] absolute position of the first window row
+  int32_t* seq_lm_start;   // [b]
+  int32_t* seq_lm_cnt;     // [b]
+};
+
+inline size_t plan_words(int rows_cap, int lm_cap, int b) {
+  return 16 + 2 * (size_t)rows_cap + (size_t)lm_cap + 5 * (size_t)b;
+}
+
+inline PlanView plan_view(int32_t* base, int rows_cap, int lm_cap, int b) {
+  PlanView p;
+  p.hdr = base;
+  p.row_seq = base + 16;
+  p.row_pos = p.row_seq + rows_cap;
+  p.lm_row = p.row_pos + rows_cap;
+  p.seq_row_start = p.lm_row + lm_cap;
+  p.seq_win_len = p.seq_row_start + b;
+  p.seq_win_start = p.seq_win_len + b;
+  p.seq_lm_start = p.seq_win_start + b;
+  p.seq_lm_cnt = p.seq_lm_start + b;
+  return p;
+}
+
+// GEMM epilogues.
+enum { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
+
+// ---- launchers (defined in the .hip files) ---------------------------------
+// C[M][N] (+)= A[M][K] . W[N][K]^T with M read from *M_dev; grid covers rows_cap.
+// A is fp32 for every model; W is bf16 (is_bf16) or fp32.  out is fp32:
+//   EPI_STORE_F32 / EPI_ADD_F32: [M][ldo]
+//   EPI_SWIGLU: silu(gate) * up [M][ldo], W packed gate/up in 16-row groups
+hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, const void* W, int ldw, int N,
+                       int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
+                       hipStream_t st);
+
+// LM head: per-row softmax statistics over the vocabulary of
+// z = scale * (A . W^T), mask column suppressed.  Writes per-(tile,row)
+// partials, then merges them into conf/tok.
+hipError_t launch_lm_head(bool is_bf16, const void* A, int d, const void* W, int V, int mask_id,
+                          float scale, const int32_t* M_dev, int rows_cap, float* part_max,
+                          float* part_sum, int32_t* part_arg, float* conf, int32_t* tok,
+                          hipStream_t st);
+// Debug: full logits [rows][V] for the LM rows (scaled, mask column = -inf).
+hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, const void* W, int V, int mask_id,
+                            float scale, const int32_t* M_dev, int rows_cap, float* logits,
+                            hipStream_t st);
+
+hipError_t launch_attention(bool is_bf16, const void* Q, const void* Kc, const void* Vc, void* O,
+                            PlanView plan, int b, int win_cap, int H, int Hkv, int hd, int maxpos,
+                            int B, hipStream_t st);
+
+hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
+                        int vocab, PlanView plan, int rows_cap, float* X, int32_t* err_flag,
+                        hipStream_t st);
+hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
+                          const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
+                          hipStream_t st);
+hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
+                          int Hkv, int hd, const double* inv_freq, void* Q, void* Kc, void* Vc,
+                          int maxpos, hipStream_t st);
+
+struct CommitArgs {
+  PlanView in, out;
+  const float* conf;        // [lm rows of `in`]
+  const int32_t* tok;
+  int32_t* tokens;          // [b][tok_stride]
+  int tok_stride;           // P + G
+  int32_t* commit_step;     // [b][G]
+  int32_t* seq_state;       // [b][SS_N]
+  int32_t* commit_flag;     // scratch [lm_cap]
+  long long* stats;         // [8] work counters of the executed steps
+  int b, P, G, B, nb, mask_id, step;
+  float tau;
+};
+hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
+
+struct InitArgs {
+  PlanView plan;            // step plan to build
+  PlanView prefill;         // optional prefill plan to build (hdr NULL = skip)
+  int32_t* tokens;          // [b][P + G]
+  const int32_t* prompt;    // optional [b][P]: copied into tokens
+  int32_t* commit_step;
+  int32_t* seq_state;
+  int b, P, G, B, nb, mask_id, vocab;
+  int32_t* err_flag;
+  long long* stats;         // [8], cleared
+};
+hipError_t launch_init_decode(const InitArgs& a, hipStream_t st);
+
+// Debug scatter of per-LM-row conf/tok to [b][G].
+hipError_t launch_scatter_stats(const float* conf, const int32_t* tok, PlanView plan, int P, int G,
+                                float* dconf, int32_t* dtok, int lm_cap, hipStream_t st);
+// Interleave gate/up projections in groups of 16 rows (SwiGLU epilogue layout).
+hipError_t launch_pack_gate_up(const void* gate, const void* up, void* out, int F, size_t row_bytes,
+                               hipStream_t st);
+
+// Debug scatter of logits rows to [b][G][V].
+hipError_t launch_scatter_logits(const float* logits, PlanView plan, int V, int P, int G,
+                                 float* out, int lm_cap, hipStream_t st);
+
+}  // namespace bd

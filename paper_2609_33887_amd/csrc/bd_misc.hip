@@ -1,0 +1,452 @@
+// Row-wise kernels of the denoising step (embedding gather, RMSNorm, RoPE with
+// the K/V cache write) and the decode-state kernels (commit/compaction and
+// state initialisation).
+#include "bd_internal.h"
+
+#include <math.h>
+
+namespace bd {
+
+__device__ __forceinline__ float bf2f_m(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ bf16_t f2bf_m(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// ------------------------------------------------------------------ embedding
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ tokens, int tok_stride,
+                                               const void* __restrict__ E, int d, int vocab,
+                                               const int32_t* __restrict__ hdr,
+                                               const int32_t* __restrict__ row_seq,
+                                               const int32_t* __restrict__ row_pos,
+                                               float* __restrict__ X, int32_t* __restrict__ err) {
+  const int r = blockIdx.x;
+  if (r >= hdr[0]) return;
+  int t = tokens[(size_t)row_seq[r] * tok_stride + row_pos[r]];
+  if (t < 0 || t >= vocab) {
+    if (threadIdx.x == 0) atomicOr(err, 1);
+    t = 0;
+  }
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    float v;
+    if constexpr (BF16) v = bf2f_m(((const bf16_t*)E)[(size_t)t * d + c]);
+    else v = ((const float*)E)[(size_t)t * d + c];
+    X[(size_t)r * d + c] = v;
+  }
+}
+
+hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
+                        int vocab, PlanView plan, int rows_cap, float* X, int32_t* err_flag,
+                        hipStream_t st) {
+  if (is_bf16)
+    k_embed<true><<<rows_cap, 256, 0, st>>>(tokens, tok_stride, E, d, vocab, plan.hdr, plan.row_seq,
+                                            plan.row_pos, X, err_flag);
+  else
+    k_embed<false><<<rows_cap, 256, 0, st>>>(tokens, tok_stride, E, d, vocab, plan.hdr, plan.row_seq,
+                                             plan.row_pos, X, err_flag);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RMSNorm
+// One wave per row: y = x / sqrt(mean(x^2) + eps) * g in fp32 (the GEMMs take
+// fp32 activations).  `gather` (optional) picks the source row of each row.
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X,
+                                                 const float* __restrict__ g, int d, float eps,
+                                                 const int32_t* __restrict__ Mp,
+                                                 const int32_t* __restrict__ gather,
+                                                 float* __restrict__ out) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + wave;
+  if (row >= *Mp) return;
+  const int src = gather ? gather[row] : row;
+  const float* x = X + (size_t)src * d;
+  float ss = 0.f;
+  for (int c = lane; c < d; c += 64) ss += x[c] * x[c];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int c = lane; c < d; c += 64) out[(size_t)row * d + c] = x[c] * inv * g[c];
+}
+
+hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
+                          const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
+                          hipStream_t st) {
+  (void)is_bf16;
+  k_rmsnorm<<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, (float*)out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RoPE + KV
+// Rotate-half RoPE of q and k at the row's absolute position (angle in fp64,
+// rotation in fp64, rounded once to the storage type); q -> Q[row][head][hd],
+// k and v -> the layer's cache slot [seq][kv head][pos][hd].
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ QKV,
+                                                 const int32_t* __restrict__ hdr,
+                                                 const int32_t* __restrict__ row_seq,
+                                                 const int32_t* __restrict__ row_pos, int H, int Hkv,
+                                                 int hd, const double* __restrict__ inv_freq,
+                                                 void* __restrict__ Q, void* __restrict__ Kc,
+                                                 void* __restrict__ Vc, int maxpos) {
+  const int r = blockIdx.x;
+  if (r >= hdr[0]) return;
+  const int s = row_seq[r], pos = row_pos[r];
+  const int half = hd / 2, qkv = (H + 2 * Hkv) * hd;
+  const float* src = QKV + (size_t)r * qkv;
+  for (int idx = threadIdx.x; idx < (H + Hkv) * half; idx += blockDim.x) {
+    const int head = idx / half, i = idx % half;
+    double sn, cs;
+    sincos((double)pos * inv_freq[i], &sn, &cs);
+    const double x1 = src[head * hd + i], x2 = src[head * hd + i + half];
+    const float y1 = (float)(x1 * cs - x2 * sn), y2 = (float)(x2 * cs + x1 * sn);
+    size_t o;
+    void* dst;
+    if (head < H) {
+      o = ((size_t)r * H + head) * hd;
+      dst = Q;
+    } else {
+      o = (((size_t)s * Hkv + (head - H)) * maxpos + pos) * hd;
+      dst = Kc;
+    }
+    if constexpr (BF16) {
+      ((bf16_t*)dst)[o + i] = f2bf_m(y1);
+      ((bf16_t*)dst)[o + i + half] = f2bf_m(y2);
+    } else {
+      ((float*)dst)[o + i] = y1;
+      ((float*)dst)[o + i + half] = y2;
+    }
+  }
+  for (int idx = threadIdx.x; idx < Hkv * hd; idx += blockDim.x) {
+    const int kh = idx / hd, e = idx % hd;
+    const size_t o = (((size_t)s * Hkv + kh) * maxpos + pos) * hd + e;
+    const float v = src[(H + Hkv) * hd + idx];
+    if constexpr (BF16) ((bf16_t*)Vc)[o] = f2bf_m(v);
+    else ((float*)Vc)[o] = v;
+  }
+}
+
+hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
+                          int Hkv, int hd, const double* inv_freq, void* Q, void* Kc, void* Vc,
+                          int maxpos, hipStream_t st) {
+  if (is_bf16)
+    k_rope_kv<true><<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd,
+                                              inv_freq, Q, Kc, Vc, maxpos);
+  else
+    k_rope_kv<false><<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd,
+                                               inv_freq, Q, Kc, Vc, maxpos);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ commit
+constexpr int MAXB = 256;     // sequences per state
+constexpr int MAXNB = 8;      // in-flight blocks per sequence
+
+__device__ __forceinline__ int wave_popc(bool p) { return __popcll(__ballot(p)); }
+
+// Single workgroup; wave w owns sequences w, w + 16, ...
+//  phase 1: commit rule, token/commit-step writes, per-block resolution counts,
+//           cache write of the pending blocks, in-order sweep, admission;
+//  phase 2: prefix sums of the next window sizes and masked-row counts;
+//  phase 3: the next step plan (rows = [pending blocks][active blocks],
+//           masked rows ascending).
+__global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
+  __shared__ int s_win[MAXB], s_lm[MAXB], s_rs[MAXB], s_ls[MAXB];
+  __shared__ int s_cl[MAXB], s_fa[MAXB], s_sw[MAXB], s_nb0[MAXB], s_adm[MAXB], s_lmn[MAXB], s_lm0[MAXB];
+  __shared__ long long s_pairs[MAXB], s_keys[MAXB];
+  __shared__ int s_ncommit[MAXB];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  const int P = a.P, G = a.G, B = a.B;
+
+  for (int s = wave; s < a.b; s += nw) {
+    int* ss = a.seq_state + s * SS_N;
+    const int done = ss[SS_DONE];
+    const int lm0 = a.in.seq_lm_start[s];
+    const int lmn = done ? 0 : a.in.seq_lm_cnt[s];
+    int cache_len = ss[SS_CACHE_LEN], n_pend = ss[SS_N_PEND], first_act = ss[SS_FIRST_ACT];
+    int n_act = ss[SS_N_ACT], next_blk = ss[SS_NEXT_BLK];
+    if (done) {
+      if (lane == 0) {
+        s_win[s] = 0; s_lm[s] = 0; s_cl[s] = cache_len; s_fa[s] = first_act; s_sw[s] = 0;
+        s_nb0[s] = next_blk; s_adm[s] = 0; s_lmn[s] = 0; s_lm0[s] = lm0;
+        s_pairs[s] = 0; s_keys[s] = 0; s_ncommit[s] = 0;
+      }
+      continue;
+    }
+    // work of the forward just executed: visible query-key pairs (per head)
+    // and keys streamed (prefix + window, per kv head)
+    if (lane == 0) {
+      const long long start = a.in.seq_win_start[s], nbw = a.in.seq_win_len[s] / B;
+      s_pairs[s] = (long long)B * (nbw * start + (long long)B * nbw * (nbw + 1) / 2);
+      s_keys[s] = start + (long long)a.in.seq_win_len[s];
+    }
+    // pass 1: does any position clear tau, and the most confident position
+    bool any = false;
+    float best = -INFINITY;
+    int bestpos = 0x7fffffff;
+    for (int base = 0; base < lmn; base += 64) {
+      const int i = base + lane;
+      if (i < lmn) {
+        const float cf = a.conf[lm0 + i];
+        const int pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
+        any |= (cf >= a.tau);
+        if (cf > best || (cf == best && pos < bestpos)) { best = cf; bestpos = pos; }
+      }
+    }
+    any = __ballot(any) != 0;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float ob = __shfl_xor(best, off);
+      const int op = __shfl_xor(bestpos, off);
+      if (ob > best || (ob == best && op < bestpos)) { best = ob; bestpos = op; }
+    }
+    // pass 2: commit, and count masked / committed positions per active block
+    int blk_masked[MAXNB], blk_commit[MAXNB];
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k) { blk_masked[k] = 0; blk_commit[k] = 0; }
+    for (int base = 0; base < lmn; base += 64) {
+      const int i = base + lane;
+      const bool valid = i < lmn;
+      bool c = false;
+      int kb = -1;
+      if (valid) {
+        const float cf = a.conf[lm0 + i];
+        const int pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
+        c = any ? (cf >= a.tau) : (pos == bestpos);
+        kb = (pos - P) / B - first_act;
+        if (c) {
+          a.tokens[(size_t)s * a.tok_stride + pos] = a.tok[lm0 + i];
+          a.commit_step[(size_t)s * G + pos - P] = a.step;
+        }
+        a.commit_flag[lm0 + i] = c ? 1 : 0;
+      }
+#pragma unroll
+      for (int k = 0; k < MAXNB; ++k) {
+        blk_masked[k] += wave_popc(valid && kb == k);
+        blk_commit[k] += wave_popc(valid && kb == k && c);
+      }
+    }
+    int ncommit = 0;
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k) ncommit += blk_commit[k];
+    // the blocks that rode along as clean rows now hold their K/V
+    cache_len += n_pend * B;
+    // in-order sweep: commit a chain of complete blocks from the oldest
+    int sw = 0;
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k)
+      if (sw == k && k < n_act && blk_masked[k] == blk_commit[k]) sw = k + 1;
+    int left = 0;
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k)
+      if (k >= sw && k < n_act) left += blk_masked[k] - blk_commit[k];
+    const int first_act_old = first_act, next_blk_old = next_blk;
+    first_act += sw;
+    n_act -= sw;
+    const int nblk = G / B;
+    int adm = 0;
+    while (n_act < a.nb && next_blk < nblk) { ++n_act; ++next_blk; ++adm; }
+    const int now_done = (n_act == 0);
+    if (lane == 0) {
+      ss[SS_CACHE_LEN] = cache_len;
+      ss[SS_N_PEND] = sw;
+      ss[SS_FIRST_ACT] = first_act;
+      ss[SS_N_ACT] = n_act;
+      ss[SS_NEXT_BLK] = next_blk;
+      ss[SS_DONE] = now_done;
+      ss[SS_FORWARDS] += 1;
+      s_win[s] = now_done ? 0 : (sw + n_act) * B;
+      s_lm[s] = now_done ? 0 : left + adm * B;
+      s_cl[s] = cache_len; s_fa[s] = first_act_old; s_sw[s] = sw; s_nb0[s] = next_blk_old;
+      s_adm[s] = adm; s_lmn[s] = now_done ? 0 : lmn; s_lm0[s] = lm0;
+      s_ncommit[s] = ncommit;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int r = 0, l = 0;
+    for (int s = 0; s < a.b; ++s) {
+      s_rs[s] = r; s_ls[s] = l;
+      r += s_win[s]; l += s_lm[s];
+    }
+    a.out.hdr[0] = r;
+    a.out.hdr[1] = l;
+    a.out.hdr[2] = (r == 0) ? 1 : 0;
+    long long pairs = 0, keys = 0, nc = 0;
+    for (int s = 0; s < a.b; ++s) { pairs += s_pairs[s]; keys += s_keys[s]; nc += s_ncommit[s]; }
+    const int m_in = a.in.hdr[0];
+    a.stats[0] += (m_in > 0);
+    a.stats[1] += m_in;
+    a.stats[2] += a.in.hdr[1];
+    a.stats[3] += pairs;
+    a.stats[4] += keys;
+    a.stats[5] += nc;
+  }
+  __syncthreads();
+  for (int s = wave; s < a.b; s += nw) {
+    const int rs = s_rs[s], W = s_win[s], cl = s_cl[s], ls = s_ls[s];
+    if (lane == 0) {
+      a.out.seq_row_start[s] = rs; a.out.seq_win_len[s] = W; a.out.seq_win_start[s] = cl;
+      a.out.seq_lm_start[s] = ls; a.out.seq_lm_cnt[s] = s_lm[s];
+    }
+    for (int e = lane; e < W; e += 64) {
+      a.out.row_seq[rs + e] = s;
+      a.out.row_pos[rs + e] = cl + e;
+    }
+    const int lmn = s_lmn[s], lm0 = s_lm0[s], fa = s_fa[s], sw = s_sw[s];
+    int w = 0;
+    for (int base = 0; base < lmn; base += 64) {
+      const int i = base + lane;
+      bool keep = false;
+      int pos = 0;
+      if (i < lmn) {
+        pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
+        keep = !a.commit_flag[lm0 + i] && ((pos - P) / B - fa) >= sw;
+      }
+      const unsigned long long m = __ballot(keep);
+      const int pre = __popcll(m & ((1ull << lane) - 1ull));
+      if (keep) a.out.lm_row[ls + w + pre] = rs + (pos - cl);
+      w += __popcll(m);
+    }
+    const int adm = s_adm[s], p0 = P + s_nb0[s] * B;
+    for (int e = lane; e < adm * B; e += 64) a.out.lm_row[ls + w + e] = rs + (p0 + e - cl);
+  }
+}
+
+hipError_t launch_commit(const CommitArgs& a, hipStream_t st) {
+  if (a.b > MAXB || a.nb > MAXNB) return hipErrorInvalidValue;
+  k_commit<<<1, 1024, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ init
+__global__ __launch_bounds__(1024) void k_init_decode(InitArgs a) {
+  __shared__ int s_win[MAXB], s_rs[MAXB];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  const int stride = a.P + a.G, nblk = a.G / a.B;
+  const int nact = min(a.nb, nblk);
+  for (int s = wave; s < a.b; s += nw) {
+    int32_t* t = a.tokens + (size_t)s * stride;
+    if (a.prompt) {
+      for (int j = lane; j < a.P; j += 64) {
+        const int v = a.prompt[(size_t)s * a.P + j];
+        if (v < 0 || v >= a.vocab) atomicOr(a.err_flag, 1);
+        t[j] = v;
+      }
+    }
+    for (int j = lane; j < a.G; j += 64) {
+      t[a.P + j] = a.mask_id;
+      a.commit_step[(size_t)s * a.G + j] = -1;
+    }
+    if (lane == 0) {
+      int32_t* ss = a.seq_state + s * SS_N;
+      ss[SS_CACHE_LEN] = a.P; ss[SS_N_PEND] = 0; ss[SS_FIRST_ACT] = 0; ss[SS_N_ACT] = nact;
+      ss[SS_NEXT_BLK] = nact; ss[SS_DONE] = 0; ss[SS_FORWARDS] = 0; ss[7] = 0;
+      s_win[s] = nact * a.B;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int r = 0;
+    for (int s = 0; s < a.b; ++s) { s_rs[s] = r; r += s_win[s]; }
+    a.plan.hdr[0] = r; a.plan.hdr[1] = r; a.plan.hdr[2] = (r == 0);
+    for (int k = 0; k < 8; ++k) a.stats[k] = 0;
+    if (a.prefill.hdr) {
+      a.prefill.hdr[0] = a.b * a.P; a.prefill.hdr[1] = 0; a.prefill.hdr[2] = 0;
+    }
+  }
+  __syncthreads();
+  for (int s = wave; s < a.b; s += nw) {
+    const int rs = s_rs[s], W = s_win[s];
+    if (lane == 0) {
+      a.plan.seq_row_start[s] = rs; a.plan.seq_win_len[s] = W; a.plan.seq_win_start[s] = a.P;
+      a.plan.seq_lm_start[s] = rs; a.plan.seq_lm_cnt[s] = W;
+      if (a.prefill.hdr) {
+        a.prefill.seq_row_start[s] = s * a.P; a.prefill.seq_win_len[s] = a.P;
+        a.prefill.seq_win_start[s] = 0; a.prefill.seq_lm_start[s] = 0; a.prefill.seq_lm_cnt[s] = 0;
+      }
+    }
+    for (int e = lane; e < W; e += 64) {
+      a.plan.row_seq[rs + e] = s;
+      a.plan.row_pos[rs + e] = a.P + e;
+      a.plan.lm_row[rs + e] = rs + e;
+    }
+    if (a.prefill.hdr) {
+      for (int j = lane; j < a.P; j += 64) {
+        a.prefill.row_seq[s * a.P + j] = s;
+        a.prefill.row_pos[s * a.P + j] = j;
+      }
+    }
+  }
+}
+
+hipError_t launch_init_decode(const InitArgs& a, hipStream_t st) {
+  if (a.b > MAXB) return hipErrorInvalidValue;
+  k_init_decode<<<1, 1024, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ debug
+__global__ void k_scatter_logits(const float* __restrict__ logits, const int32_t* __restrict__ hdr,
+                                 const int32_t* __restrict__ lm_row,
+                                 const int32_t* __restrict__ row_seq,
+                                 const int32_t* __restrict__ row_pos, int V, int P, int G,
+                                 float* __restrict__ out) {
+  const int i = blockIdx.y;
+  if (i >= hdr[1]) return;
+  const int r = lm_row[i];
+  const size_t o = ((size_t)row_seq[r] * G + (row_pos[r] - P)) * V;
+  for (int n = blockIdx.x * blockDim.x + threadIdx.x; n < V; n += gridDim.x * blockDim.x)
+    out[o + n] = logits[(size_t)i * V + n];
+}
+
+hipError_t launch_scatter_logits(const float* logits, PlanView plan, int V, int P, int G,
+                                 float* out, int lm_cap, hipStream_t st) {
+  k_scatter_logits<<<dim3((V + 2047) / 2048, lm_cap), 256, 0, st>>>(logits, plan.hdr, plan.lm_row,
+                                                                     plan.row_seq, plan.row_pos, V,
+                                                                     P, G, out);
+  return hipGetLastError();
+}
+
+__global__ void k_scatter_stats(const float* __restrict__ conf, const int32_t* __restrict__ tok,
+                                const int32_t* __restrict__ hdr, const int32_t* __restrict__ lm_row,
+                                const int32_t* __restrict__ row_seq,
+                                const int32_t* __restrict__ row_pos, int P, int G,
+                                float* __restrict__ dconf, int32_t* __restrict__ dtok) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= hdr[1]) return;
+  const int r = lm_row[i];
+  const size_t o = (size_t)row_seq[r] * G + (row_pos[r] - P);
+  if (dconf) dconf[o] = conf[i];
+  if (dtok) dtok[o] = tok[i];
+}
+
+hipError_t launch_scatter_stats(const float* conf, const int32_t* tok, PlanView plan, int P, int G,
+                                float* dconf, int32_t* dtok, int lm_cap, hipStream_t st) {
+  k_scatter_stats<<<(lm_cap + 255) / 256, 256, 0, st>>>(conf, tok, plan.hdr, plan.lm_row, plan.row_seq,
+                                                        plan.row_pos, P, G, dconf, dtok);
+  return hipGetLastError();
+}
+
+// Pack gate and up projections into groups of 16 rows: packed rows
+// [32q, 32q + 16) = gate rows [16q, 16q + 16), [32q + 16, 32q + 32) = up rows.
+__global__ void k_pack_gate_up(const uint8_t* __restrict__ gate, const uint8_t* __restrict__ up,
+                               uint8_t* __restrict__ out, size_t row_bytes) {
+  const int pr = blockIdx.x;
+  const int q = pr >> 5, w = pr & 31;
+  const uint8_t* src = (w < 16 ? gate : up) + (size_t)(q * 16 + (w & 15)) * row_bytes;
+  uint8_t* dst = out + (size_t)pr * row_bytes;
+  for (size_t c = threadIdx.x * 4; c < row_bytes; c += blockDim.x * 4)
+    *(uint32_t*)(dst + c) = *(const uint32_t*)(src + c);
+}
+
+hipError_t launch_pack_gate_up(const void* gate, const void* up, void* out, int F, size_t row_bytes,
+                               hipStream_t st) {
+  if (F % 16 || row_bytes % 4) return hipErrorInvalidValue;
+  k_pack_gate_up<<<2 * F, 256, 0, st>>>((const uint8_t*)gate, (const uint8_t*)up, (uint8_t*)out,
+                                        row_bytes);
+  return hipGetLastError();
+}
+
+}  // namespace bd

@@ -1,0 +1,138 @@
+"""Step-by-step GPU trace capture and lockstep comparison with the oracle.
+
+The GPU decodes the whole batch through the C ABI, one bd_denoise_step +
+bd_commit at a time, and records for every step the confidence and argmax of
+each masked position (and, optionally, its logits).  The oracle then decodes
+chosen sequences on the CPU; at every step it compares its statistics with the
+GPU's and its own commit decision with the GPU's.  A differing decision is
+excused only when the oracle's numbers make it a near-tie:
+
+  T1  |conf - tau| <= 1e-3 at a position committed by one side only;
+  T2  the two most probable tokens are within 1e-3 of probability;
+  T3  the forced single commit where the two best confidences are within 1e-3.
+
+After an excused difference the oracle adopts the GPU's decision, so that the
+rest of the trace stays comparable.  Any other difference is a failure.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+NEAR = 1e-3
+
+
+@dataclass
+class GpuTrace:
+    steps: list                      # per step: dict seq -> (positions, conf, tok, logits or None)
+    tokens: np.ndarray               # [b][G]
+    commit_step: np.ndarray          # [b][G]
+    forwards: np.ndarray             # [b]
+
+
+def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=None):
+    import torch
+    from paper_2609_33887_amd import bd
+    st = bd.State(model, prompts, G, tau, nb, B)
+    b = st.b
+    dev = model.device
+    V = model.w.vocab
+    conf = torch.empty((b, G), dtype=torch.float32, device=dev)
+    tok = torch.empty((b, G), dtype=torch.int32, device=dev)
+    logits = torch.empty((b, G, V), dtype=torch.float32, device=dev) if logits_for else None
+    steps = []
+    limit = max_steps or (G + 2)
+    for s in range(limit):
+        conf.fill_(-1.0)
+        tok.fill_(-1)
+        st.step(conf, tok, logits)
+        done = st.commit(want_done=True)
+        c = conf.cpu().numpy()
+        t = tok.cpu().numpy()
+        rec = {}
+        for i in range(b):
+            pos = np.nonzero(c[i] >= 0)[0]
+            if pos.size:
+                lg = None
+                if i in logits_for:
+                    lg = logits[i, torch.as_tensor(pos, device=dev)].cpu().numpy()
+                rec[i] = (pos, c[i, pos], t[i, pos], lg)
+        steps.append(rec)
+        if done:
+            break
+    tokens, cstep, fwd = st.read()
+    st.close()
+    return GpuTrace(steps, tokens, cstep, fwd)
+
+
+@dataclass
+class Report:
+    max_conf_diff: float = 0.0
+    max_logit_diff: float = 0.0
+    t1: int = 0
+    t2: int = 0
+    t3: int = 0
+    positions: int = 0
+    failures: list = field(default_factory=list)
+
+
+def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, conf_tol, logit_tol):
+    """Replay the chosen sequences in the oracle against ``trace``."""
+    from oracle.decode import SeqDecoder
+    rep = Report()
+    tau32 = float(np.float32(tau))
+    for i in seq_ids:
+        d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau)
+        d.prefill()
+        P = d.P
+        step = 0
+        while not d.done:
+            if step >= len(trace.steps) or i not in trace.steps[step]:
+                rep.failures.append((i, step, "GPU finished this sequence earlier than the oracle"))
+                break
+            gpos, gconf, gtok, glog = trace.steps[step][i]
+            masked, conf, tok, p2, z = d.forward_step(with_logits=True)
+            if not np.array_equal(masked - P, gpos):
+                rep.failures.append((i, step, "masked position sets differ"))
+                break
+            rep.positions += len(masked)
+            rep.max_conf_diff = max(rep.max_conf_diff, float(np.max(np.abs(conf - gconf))))
+            if glog is not None:
+                fin = np.isfinite(z)
+                if not np.array_equal(fin, np.isfinite(glog)):
+                    rep.failures.append((i, step, "suppressed logit columns differ"))
+                rep.max_logit_diff = max(rep.max_logit_diff, float(np.max(np.abs(z[fin] - glog[fin]))))
+            if np.any(np.abs(conf - gconf) > conf_tol):
+                rep.failures.append((i, step, f"confidence differs by {np.max(np.abs(conf - gconf)):.3g}"))
+            # decisions
+            own = np.zeros(len(masked), dtype=bool)
+            own_sel = conf >= tau32
+            if own_sel.any():
+                own = own_sel
+            else:
+                own[int(np.argmax(conf))] = True
+            gsel = trace.commit_step[i, masked - P] == step
+            for k in np.nonzero(own != gsel)[0]:
+                if abs(conf[k] - tau32) <= NEAR:
+                    rep.t1 += 1
+                elif not own_sel.any() and len(conf) > 1 and \
+                        np.sort(conf)[-1] - np.sort(conf)[-2] <= NEAR:
+                    rep.t3 += 1
+                else:
+                    rep.failures.append((i, step, f"commit decision differs at position {masked[k] - P} "
+                                                  f"(oracle conf {conf[k]:.6f}, GPU conf {gconf[k]:.6f})"))
+            both = own & gsel
+            gtoks = trace.tokens[i, masked - P]
+            for k in np.nonzero(both & (tok != gtoks))[0]:
+                if conf[k] - p2[k] <= NEAR:
+                    rep.t2 += 1
+                else:
+                    rep.failures.append((i, step, f"token differs at position {masked[k] - P}"))
+            d.apply(masked[gsel], gtoks[gsel], step)
+            step += 1
+        if d.done and d.forwards != trace.forwards[i]:
+            rep.failures.append((i, step, f"forwards {d.forwards} vs GPU {trace.forwards[i]}"))
+        if d.done and not np.array_equal(d.tokens[P:], trace.tokens[i]):
+            rep.failures.append((i, step, "final tokens differ"))
+    return rep

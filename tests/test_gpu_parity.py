@@ -1,0 +1,188 @@
+"""GPU parity of the HIP path against the oracle, through the C ABI.
+
+Tolerances (stated numerically): bf16 models -- logits max-abs <= 3e-2,
+confidence <= 5e-3; fp32 models -- confidence <= 1e-4, logits <= 1e-3.
+Committed tokens, commit steps and forwards must be identical except at
+near-ties in the oracle's own numbers (|conf - tau| <= 1e-3, top-1/top-2
+probability gap <= 1e-3, or best-two confidences within 1e-3 for a forced
+commit), which are counted and printed.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+from bd_synth import workload, make_weights, make_prompts, Workload   # noqa: E402
+
+TOL = {"bf16": (5e-3, 3e-2), "f32": (1e-4, 1e-3)}
+
+
+def small(name, **kw):
+    base = dict(name=name, seed=90, n_layers=2, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64,
+                ffn_dim=512, vocab=1024, dtype="bf16", batch=3, prompt_len=64, block_size=16,
+                n_inflight=2, gen_len=64, taus=(0.9,))
+    base.update(kw)
+    return Workload(**base)
+
+
+SMALL = {
+    "mha64": small("mha64"),
+    "gqa128_ragged": small("gqa128_ragged", seed=91, n_heads=4, n_kv_heads=2, head_dim=128, vocab=2048,
+                           batch=2, prompt_len=96, block_size=32, n_inflight=3, gen_len=128),
+    "f32_gqa": small("f32_gqa", seed=92, dtype="f32", n_heads=4, n_kv_heads=1, vocab=1024, batch=2,
+                     prompt_len=8, block_size=8, n_inflight=2, gen_len=48),
+    "block1": small("block1", seed=93, batch=2, prompt_len=5, block_size=1, n_inflight=1, gen_len=12,
+                    dtype="f32"),
+}
+
+_models = {}
+
+
+def get_model(w):
+    from paper_2609_33887_amd import bd
+    key = (w.name, w.seed)
+    if key not in _models:
+        _models[key] = (bd.Model(w, make_weights(w)), make_weights(w))
+    return _models[key]
+
+
+def run_parity(w, tau, seq_ids=None, logits=True, max_seqs=None):
+    from oracle.model import OracleModel
+    from tests.gpu_harness import capture_gpu_trace, lockstep
+    _need_gpu()
+    _say(f"[parity] {w.name} tau={tau} b={w.batch} P={w.prompt_len} G={w.gen_len} B={w.block_size} "
+         f"nb={w.n_inflight}")
+    model, ws = get_model(w)
+    prompts = make_prompts(w)
+    ids = list(range(w.batch)) if seq_ids is None else list(seq_ids)
+    tr = capture_gpu_trace(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size,
+                           logits_for=set(ids) if logits else ())
+    om = OracleModel(w, ws, "f64" if w.dtype == "f32" else "bf16")
+    rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, w.n_inflight, w.block_size, *TOL[w.dtype])
+    ctol, ltol = TOL[w.dtype]
+    _say(f"  positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} max|dlogit|={rep.max_logit_diff:.3g} "
+         f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
+    assert not rep.failures, rep.failures[:5]
+    assert rep.max_conf_diff <= ctol
+    assert rep.max_logit_diff <= ltol
+    return tr, rep
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
+def test_small_models(name, tau):
+    run_parity(SMALL[name], tau)
+
+
+@pytest.mark.parametrize("tau", [0.0, 2.0])
+def test_degenerate_thresholds(tau):
+    """tau = 0 resolves every admitted block in one step; tau > 1 commits
+    exactly one token per step (forwards = G)."""
+    w = SMALL["mha64"]
+    tr, rep = run_parity(w, tau, logits=False)
+    nblk = w.gen_len // w.block_size
+    if tau == 0.0:
+        assert (tr.forwards == -(-nblk // w.n_inflight)).all()
+    else:
+        assert (tr.forwards == w.gen_len).all()
+
+
+def test_config0_tiny_f32():
+    w = workload(0)
+    for tau in w.taus:
+        run_parity(w, tau)
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
+def test_config1_dense_bf16_full_size(tau):
+    """Full-size dense bf16 model (12 layers, d 1024, vocab 32768, batch 16,
+    prompts 512, 256 generated tokens); the oracle replays 2 of the 16
+    sequences (sequences are independent, so the subset is exact)."""
+    w = workload(1)
+    run_parity(w, tau, seq_ids=[0, 11], logits=True)
+
+
+def test_decode_entry_point_matches_stepwise_and_is_deterministic():
+    from paper_2609_33887_amd import bd
+    from tests.gpu_harness import capture_gpu_trace
+    _need_gpu()
+    w = SMALL["gqa128_ragged"]
+    model, _ = get_model(w)
+    prompts = make_prompts(w)
+    t1, c1, f1 = bd.decode(model, prompts, w.gen_len, 0.8, w.n_inflight, w.block_size)
+    t2, c2, f2 = bd.decode(model, prompts, w.gen_len, 0.8, w.n_inflight, w.block_size)
+    tr = capture_gpu_trace(model, prompts, w.gen_len, 0.8, w.n_inflight, w.block_size)
+    np.testing.assert_array_equal(t1, t2)
+    np.testing.assert_array_equal(c1, c2)
+    np.testing.assert_array_equal(t1, tr.tokens)
+    np.testing.assert_array_equal(c1, tr.commit_step)
+    np.testing.assert_array_equal(f1, tr.forwards)
+
+
+def test_state_reset_replays_the_same_trace():
+    from paper_2609_33887_amd import bd
+    _need_gpu()
+    w = SMALL["mha64"]
+    model, _ = get_model(w)
+    st = bd.State(model, make_prompts(w), w.gen_len, 0.9, w.n_inflight, w.block_size)
+    outs = []
+    for _ in range(2):
+        done = False
+        while not done:
+            st.step()
+            done = st.commit(want_done=True)
+        outs.append(st.read())
+        st.reset()
+    st.close()
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_error_paths():
+    from paper_2609_33887_amd import bd
+    _need_gpu()
+    w = SMALL["mha64"]
+    model, _ = get_model(w)
+    pr = make_prompts(w)
+    with pytest.raises(bd.BDError) as e:
+        bd.State(model, pr, 60, 0.9, 2, 16)               # G not a multiple of B
+    assert e.value.status == bd.BD_EINVAL
+    with pytest.raises(bd.BDError) as e:
+        bd.State(model, pr[:, :60], 64, 0.9, 2, 16)       # P not a multiple of B
+    assert e.value.status == bd.BD_EINVAL
+    with pytest.raises(bd.BDError) as e:
+        bd.State(model, pr, 64, float("nan"), 2, 16)
+    assert e.value.status == bd.BD_EINVAL
+    st = bd.State(model, pr, 64, 0.9, 2, 16)
+    with pytest.raises(bd.BDError) as e:
+        st.commit()                                        # nothing to commit
+    assert e.value.status == bd.BD_ESTATE
+    st.step()
+    with pytest.raises(bd.BDError) as e:
+        st.step()                                          # previous step not committed
+    assert e.value.status == bd.BD_ESTATE
+    st.commit()
+    st.close()
+    bad = pr.copy()
+    bad[1, 3] = w.vocab + 5
+    st = bd.State(model, bad, 64, 0.9, 2, 16)
+    st.step()
+    with pytest.raises(bd.BDError) as e:
+        st.commit(want_done=True)
+    assert e.value.status == bd.BD_EINVAL
+    st.close()

@@ -26,6 +26,21 @@ def test_round_bf16_matches_torch():
     assert round_bf16(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
 
 
+def test_split_bf16x2_carries_16_bits():
+    """hi + lo represents fp32(x) to 16 significant bits; both halves are
+    bf16 values; values that are already bf16 have lo = 0."""
+    from oracle.model import split_bf16x2
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal(50000) * 10.0 ** rng.integers(-4, 4, 50000)
+    x32 = x.astype(np.float32).astype(np.float64)
+    y = split_bf16x2(x)
+    assert np.all(np.abs(y - x32) <= np.abs(x32) * 2.0 ** -16)
+    hi = round_bf16(x32)
+    np.testing.assert_array_equal(round_bf16(y - hi), y - hi)
+    b = round_bf16(x)
+    np.testing.assert_array_equal(split_bf16x2(b), b)
+
+
 def _model(cfg=None, seed=0, precision="f64", std=0.3):
     cfg = cfg or TinyCfg()
     return cfg, tiny_weights(cfg, seed, std), OracleModel(cfg, tiny_weights(cfg, seed, std), precision)
@@ -184,7 +199,9 @@ def test_cached_step_equals_full_recompute(precision):
         fresh = m.kv_cache(P + G)
         full = m.forward(d.tokens, 0, e, fresh, B)[s:]
         cached = m.forward(d.tokens, s, e, d.cache, B)
-        tol = 1e-12 if precision == "f64" else 1e-6
+        # bf16 mode: BLAS may accumulate the two row sets in different orders
+        # before Q/K/V are rounded, so agreement is at the rounding level there
+        tol = 1e-12 if precision == "f64" else 2e-3
         np.testing.assert_allclose(cached, full, atol=tol, rtol=0)
         checked += 1
         d.step(step)
@@ -263,6 +280,7 @@ def test_bf16_mode_differs_only_at_storage_points(monkeypatch):
     a = OracleModel(cfg, ws, "f64")
     za = a.logits(a.forward(toks, 0, 8, a.kv_cache(8), 4))
     monkeypatch.setattr(om, "round_bf16", lambda x: np.asarray(x, dtype=np.float64))
+    monkeypatch.setattr(om, "split_bf16x2", lambda x: np.asarray(x, dtype=np.float64))
     b = OracleModel(cfg, ws, "bf16")
     zb = b.logits(b.forward(toks, 0, 8, b.kv_cache(8), 4))
     np.testing.assert_allclose(zb, za, atol=2e-4)
