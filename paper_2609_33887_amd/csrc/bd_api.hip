@@ -123,6 +123,13 @@ struct bd_state {
   float* conf;
   int32_t* tok;
   float* logits_tmp;
+  float* gemm_ws;
+  size_t gemm_ws_floats;
+  // bf16 models: plane offsets (elements) of the lo halves of A, Ob, Hact, Alm
+  size_t pl_A, pl_O, pl_H, pl_lm;
+  int attn_splits;
+  float* attn_ws_o;
+  float* attn_ws_ml;
   void* Kc;
   void* Vc;
   int steps;
@@ -167,8 +174,8 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
   for (int i = 0; i < n_weights; ++i)
     if (!w[i]) return fail(BD_EINVAL, "weight %d is NULL", i);
   const bool bf16 = c.dtype == BD_BF16;
-  // GEMM tiling constraints (bf16: N % 128, K % 32; f32: N % 64, K % 16)
-  const int nq = bf16 ? 128 : 64, kq = bf16 ? 32 : 16;
+  // GEMM tiling constraints (bf16: N % 128, K % 64; f32: N % 64, K % 16)
+  const int nq = bf16 ? 128 : 64, kq = bf16 ? 64 : 16;
   const int qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
   if (qkv % nq || c.d_model % nq || c.vocab % nq || (2 * c.ffn_dim) % nq || c.d_model % kq ||
       (c.n_heads * c.head_dim) % kq || c.ffn_dim % kq)
@@ -260,6 +267,7 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int qkv = (H + 2 * Hkv) * hd;
   const size_t layer_kv = (size_t)s->b * Hkv * s->maxpos * hd * m->esz;
+  const int kv_splits = (bf && lm) ? s->attn_splits : 1;
   LAUNCH(BD_PROF_EMBED, launch_embed(bf, s->tokens, s->P + s->G, m->embed, d, c.vocab, plan,
                                      rows_cap, s->X, m->err_flag, st));
   for (int l = 0; l < c.n_layers; ++l) {
@@ -267,26 +275,31 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
     void* Kl = (char*)s->Kc + l * layer_kv;
     void* Vl = (char*)s->Vc + l * layer_kv;
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.attn_norm, d, c.rms_eps, plan.hdr, nullptr,
-                                        rows_cap, s->A, st));
-    LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, L.w_qkv, d, qkv, d, plan.hdr,
-                                         rows_cap, s->QKV, qkv, st));
+                                        rows_cap, s->A, s->pl_A, st));
+    LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, s->pl_A, L.w_qkv, d, qkv, d,
+                                         plan.hdr, rows_cap, s->QKV, qkv, 0, s->gemm_ws,
+                                         s->gemm_ws_floats, st));
     LAUNCH(BD_PROF_ROPE, launch_rope_kv(bf, s->QKV, plan, rows_cap, H, Hkv, hd, m->inv_freq, s->Qb,
                                         Kl, Vl, s->maxpos, st));
-    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, Kl, Vl, s->Ob, plan, s->b, win_cap, H, Hkv, hd,
-                                          s->maxpos, s->B, st));
-    LAUNCH(BD_PROF_GEMM_O, launch_gemm(EPI_ADD_F32, bf, s->Ob, H * hd, L.w_o, H * hd, d, H * hd,
-                                       plan.hdr, rows_cap, s->X, d, st));
+    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, Kl, Vl, s->Ob, s->pl_O, plan, s->b, win_cap, H, Hkv, hd,
+                                          s->maxpos, s->B, kv_splits, s->attn_ws_o, s->attn_ws_ml,
+                                          rows_cap, st));
+    LAUNCH(BD_PROF_GEMM_O, launch_gemm(EPI_ADD_F32, bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d,
+                                       H * hd, plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
+                                       s->gemm_ws_floats, st));
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
-                                        rows_cap, s->A, st));
-    LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, L.w_gu, d, 2 * F, d, plan.hdr,
-                                        rows_cap, s->Hact, F, st));
-    LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, bf, s->Hact, F, L.w_down, F, d, F, plan.hdr,
-                                          rows_cap, s->X, d, st));
+                                        rows_cap, s->A, s->pl_A, st));
+    LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, s->pl_A, L.w_gu, d, 2 * F, d,
+                                        plan.hdr, rows_cap, s->Hact, F, s->pl_H, s->gemm_ws,
+                                        s->gemm_ws_floats, st));
+    LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
+                                          plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
+                                          s->gemm_ws_floats, st));
   }
   if (lm) {
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, m->final_norm, d, c.rms_eps, plan.hdr + 1,
-                                        plan.lm_row, s->lm_cap, s->Alm, st));
-    LAUNCH(BD_PROF_LM_HEAD, launch_lm_head(bf, s->Alm, d, m->lm_head, c.vocab, c.mask_id,
+                                        plan.lm_row, s->lm_cap, s->Alm, s->pl_lm, st));
+    LAUNCH(BD_PROF_LM_HEAD, launch_lm_head(bf, s->Alm, d, s->pl_lm, m->lm_head, c.vocab, c.mask_id,
                                            c.logit_scale, plan.hdr + 1, s->lm_cap, s->pmax, s->psum,
                                            s->parg, s->conf, s->tok, st));
   }
@@ -348,7 +361,14 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
     s->plan[i] = plan_view(s->plan_buf[i], rc, s->lm_cap, b);
   }
   ALLOC(s->X, (size_t)s->rows_cap * d * 4);
+  // activation operands: fp32, or two bf16 planes (same bytes) for bf16 models
   ALLOC(s->A, (size_t)s->rows_cap * d * 4);
+  if (m->bf16) {
+    s->pl_A = (size_t)s->rows_cap * d;
+    s->pl_O = (size_t)s->rows_cap * H * hd;
+    s->pl_H = (size_t)s->rows_cap * c.ffn_dim;
+    s->pl_lm = (size_t)s->lm_cap * d;
+  }
   ALLOC(s->QKV, (size_t)s->rows_cap * qkv * 4);
   ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * esz);
   ALLOC(s->Ob, (size_t)s->rows_cap * H * hd * 4);
@@ -362,6 +382,24 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   const size_t kv_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * esz;
   ALLOC(s->Kc, kv_bytes);
   ALLOC(s->Vc, kv_bytes);
+  {
+    // split-K workspace: the largest need of the projections at either row capacity
+    const int shapes[4][2] = {{qkv, d}, {d, H * hd}, {2 * c.ffn_dim, d}, {d, c.ffn_dim}};
+    size_t need = 0;
+    for (int rc : {s->rows_step, s->rows_pre})
+      for (auto& sh : shapes) {
+        const GemmPlan gp = plan_gemm(m->bf16, sh[0], sh[1], rc);
+        const size_t f = gemm_workspace_floats(gp, sh[0], rc);
+        if (f > need) need = f;
+      }
+    s->gemm_ws_floats = need;
+    if (need) ALLOC(s->gemm_ws, need * sizeof(float));
+  }
+  s->attn_splits = m->bf16 ? attention_splits(b, s->win_step, H, s->maxpos) : 1;
+  if (s->attn_splits > 1) {
+    ALLOC(s->attn_ws_o, (size_t)s->attn_splits * s->rows_step * H * hd * 4);
+    ALLOC(s->attn_ws_ml, (size_t)s->attn_splits * s->rows_step * H * 2 * 4);
+  }
 #undef ALLOC
   if (hipHostMalloc((void**)&s->host_flag, 64, hipHostMallocDefault) != hipSuccess) {
     s->host_flag = nullptr;
@@ -446,7 +484,7 @@ extern "C" bd_status bd_denoise_step(bd_model* m, bd_state* s, float* conf_dev, 
     if (!s->logits_tmp) {
       if ((r = dev_alloc(s, (void**)&s->logits_tmp, (size_t)s->lm_cap * c.vocab * 4)) != BD_OK) return r;
     }
-    HIPCHK(launch_lm_logits(m->bf16, s->Alm, c.d_model, m->lm_head, c.vocab, c.mask_id, c.logit_scale,
+    HIPCHK(launch_lm_logits(m->bf16, s->Alm, c.d_model, s->pl_lm, m->lm_head, c.vocab, c.mask_id, c.logit_scale,
                             plan.hdr + 1, s->lm_cap, s->logits_tmp, m->stream));
     HIPCHK(launch_scatter_logits(s->logits_tmp, plan, c.vocab, s->P, s->G, logits_dev, s->lm_cap,
                                  m->stream));

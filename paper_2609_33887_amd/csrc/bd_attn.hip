@@ -8,7 +8,8 @@
 // queries).  Key tiles of 64 positions stream from HBM through LDS with
 // 16-byte coalesced loads (K row-major, V transposed), and the wave computes
 // S^T = K Q^T and O^T += V^T P^T with MFMA 16x16x32 bf16 (P^T as a hi/lo
-// bf16 pair, the fp32 output unrounded), so each lane owns
+// bf16 pair; the output leaves as the hi/lo pair of the next matmul operand),
+// so each lane owns
 // one query column: the online-softmax state and the O rescale stay in the
 // lane, and P^T is fed to the second MFMA straight from the score registers
 // (the two products use the same permutation of the key index).  The block
@@ -33,23 +34,32 @@ template <int HD>
 __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
                                                    const bf16_t* __restrict__ Kc,
                                                    const bf16_t* __restrict__ Vc,
-                                                   float* __restrict__ O,
+                                                   bf16_t* __restrict__ O, size_t o_plane,
                                                    const int32_t* __restrict__ seq_row_start,
                                                    const int32_t* __restrict__ seq_win_len,
                                                    const int32_t* __restrict__ seq_win_start, int H,
-                                                   int Hkv, int maxpos, int B, float scale_log2) {
+                                                   int Hkv, int maxpos, int B, float scale_log2,
+                                                   int kv_splits, float* __restrict__ ws_o,
+                                                   float* __restrict__ ws_ml, int rows_cap) {
   constexpr int KP = HD + 8;        // padded K row (elements)
   constexpr int VP = AK + 8;        // padded transposed-V row
+  constexpr int CH = AK * HD / 8;   // 16-byte chunks per K (or V) tile
+  constexpr int NCH = CH / 256;     // chunks per thread
   __shared__ __attribute__((aligned(16))) bf16_t sK[AK * KP];
   __shared__ __attribute__((aligned(16))) bf16_t sVt[HD * VP];
 
-  const int s = blockIdx.z, h = blockIdx.y, qt = blockIdx.x;
+  const int s = blockIdx.z / kv_splits, split = blockIdx.z % kv_splits;
+  const int h = blockIdx.y, qt = blockIdx.x;
   const int W = seq_win_len[s];
   if (qt * AQ >= W) return;
   const int row0 = seq_row_start[s] + qt * AQ;
   const int nrows = min(AQ, W - qt * AQ);
   const int pos0 = seq_win_start[s] + qt * AQ;
   const int kend = ((pos0 + nrows - 1) / B + 1) * B;        // keys [0, kend)
+  // this split's key tiles: a contiguous, tile-aligned share of [0, kend)
+  const int ntiles_all = (kend + AK - 1) / AK;
+  const int per = (ntiles_all + kv_splits - 1) / kv_splits;
+  const int t_lo = split * per, t_hi = min(ntiles_all, t_lo + per);
   const int kv = h / (H / Hkv);
   const size_t kvbase = ((size_t)s * Hkv + kv) * (size_t)maxpos * HD;
   const bf16_t* Kp = Kc + kvbase;
@@ -76,26 +86,36 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
   for (int t = 0; t < HD / 16; ++t) oacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
-  const int ntiles = (kend + AK - 1) / AK;
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int k0 = kt * AK;
-    // stage K (row-major) and V (transposed) tiles; keys >= kend are zero
-    constexpr int CH = AK * HD / 8;                            // 16-byte chunks per tile
+  // register prefetch of the next K/V tile overlaps the loads with the MFMAs
+  u32x4 pk[NCH], pv[NCH];
+  auto fetch = [&](int k0) {
 #pragma unroll
-    for (int it = 0; it < CH / 256; ++it) {
+    for (int it = 0; it < NCH; ++it) {
       const int ci = tid + 256 * it;
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
-      uint4 kvv = make_uint4(0, 0, 0, 0), vvv = make_uint4(0, 0, 0, 0);
+      pk[it] = u32x4{0u, 0u, 0u, 0u};
+      pv[it] = u32x4{0u, 0u, 0u, 0u};
       if (k0 + key < kend) {
-        kvv = *(const uint4*)(Kp + (size_t)(k0 + key) * HD + dc);
-        vvv = *(const uint4*)(Vp + (size_t)(k0 + key) * HD + dc);
+        pk[it] = *(const u32x4*)(Kp + (size_t)(k0 + key) * HD + dc);
+        pv[it] = *(const u32x4*)(Vp + (size_t)(k0 + key) * HD + dc);
       }
-      *(uint4*)(sK + key * KP + dc) = kvv;
-      const bf16_t* vv = (const bf16_t*)&vvv;
+    }
+  };
+  if (t_lo < t_hi) fetch(t_lo * AK);
+  for (int kt = t_lo; kt < t_hi; ++kt) {
+    const int k0 = kt * AK;
+    // stage K (row-major) and V (transposed); keys >= kend are zero
+#pragma unroll
+    for (int it = 0; it < NCH; ++it) {
+      const int ci = tid + 256 * it;
+      const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
+      *(u32x4*)(sK + key * KP + dc) = pk[it];
+      const bf16_t* vv = (const bf16_t*)&pv[it];
 #pragma unroll
       for (int e = 0; e < 8; ++e) sVt[(dc + e) * VP + key] = vv[e];
     }
     __syncthreads();
+    if (kt + 1 < t_hi) fetch(k0 + AK);
 
     // S^T sub-tiles: keys st*16 + 4g + r, query c
     float sv[4][4];
@@ -168,15 +188,69 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
   float l = l_part;
   l += __shfl_xor(l, 16);
   l += __shfl_xor(l, 32);
-  if (qvalid) {
+  if (!qvalid) return;
+  if (kv_splits == 1) {
     const float inv = 1.0f / l;
-    float* orow = O + (size_t)(row0 + q) * H * HD + h * HD;
+    bf16_t* orow = O + (size_t)(row0 + q) * H * HD + h * HD;
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t) {
-      // O^T tile t: lane holds dims t*16 + 4g + r of query c
-      *(float4*)(orow + t * 16 + 4 * g) =
-          make_float4(oacc[t][0] * inv, oacc[t][1] * inv, oacc[t][2] * inv, oacc[t][3] * inv);
+      // O^T tile t: lane holds dims t*16 + 4g + r of query c; stored as the
+      // bf16 pair (hi, lo) of the O-projection operand
+      bf16_t hb[4], lb[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float y = oacc[t][r] * inv;
+        hb[r] = f2bf_a(y);
+        lb[r] = f2bf_a(y - bf2f_a(hb[r]));
+      }
+      *(uint2*)(orow + t * 16 + 4 * g) =
+          make_uint2((uint32_t)hb[0] | ((uint32_t)hb[1] << 16), (uint32_t)hb[2] | ((uint32_t)hb[3] << 16));
+      *(uint2*)(orow + o_plane + t * 16 + 4 * g) =
+          make_uint2((uint32_t)lb[0] | ((uint32_t)lb[1] << 16), (uint32_t)lb[2] | ((uint32_t)lb[3] << 16));
     }
+  } else {
+    // unnormalised partial of this key split, merged by k_attn_merge
+    const size_t base = ((size_t)split * rows_cap + row0 + q) * H + h;
+    float* orow = ws_o + base * HD;
+#pragma unroll
+    for (int t = 0; t < HD / 16; ++t)
+      *(float4*)(orow + t * 16 + 4 * g) = make_float4(oacc[t][0], oacc[t][1], oacc[t][2], oacc[t][3]);
+    if (g == 0) {
+      ws_ml[2 * base] = m_run;
+      ws_ml[2 * base + 1] = l;
+    }
+  }
+}
+
+// Merge of the key splits (fixed split order): O = sum_s 2^(m_s - M) O_s /
+// sum_s 2^(m_s - M) l_s with M = max_s m_s (scores kept in log2 units).
+__global__ __launch_bounds__(256) void k_attn_merge(const float* __restrict__ ws_o,
+                                                    const float* __restrict__ ws_ml, int kv_splits,
+                                                    const int32_t* __restrict__ Mp, int H, int hd,
+                                                    int rows_cap, bf16_t* __restrict__ O,
+                                                    size_t o_plane) {
+  const int item = blockIdx.x;                 // (row, head)
+  const int r = item / H, h = item % H;
+  if (r >= *Mp) return;
+  float M = -INFINITY;
+  for (int z = 0; z < kv_splits; ++z) M = fmaxf(M, ws_ml[2 * (((size_t)z * rows_cap + r) * H + h)]);
+  float L = 0.f;
+  for (int z = 0; z < kv_splits; ++z) {
+    const size_t b = ((size_t)z * rows_cap + r) * H + h;
+    const float m = ws_ml[2 * b];
+    if (m != -INFINITY) L += exp2f(m - M) * ws_ml[2 * b + 1];
+  }
+  for (int e = threadIdx.x; e < hd; e += blockDim.x) {
+    float acc = 0.f;
+    for (int z = 0; z < kv_splits; ++z) {
+      const size_t b = ((size_t)z * rows_cap + r) * H + h;
+      const float m = ws_ml[2 * b];
+      if (m != -INFINITY) acc += exp2f(m - M) * ws_o[b * hd + e];
+    }
+    const float y = acc / L;
+    const bf16_t hb = f2bf_a(y);
+    O[((size_t)r * H + h) * hd + e] = hb;
+    O[((size_t)r * H + h) * hd + e + o_plane] = f2bf_a(y - bf2f_a(hb));
   }
 }
 
@@ -220,25 +294,39 @@ __global__ __launch_bounds__(256) void k_attn_f32(const float* __restrict__ Q,
   for (int e = 0; e < per; ++e) o[lane * per + e] = acc[e] / l;
 }
 
+int attention_splits(int b, int win_cap, int H, int maxpos) {
+  const int wgs = ((win_cap + AQ - 1) / AQ) * H * b;
+  int splits = 1;
+  // aim for >= 1024 workgroups while every split keeps >= 2 key tiles
+  while (wgs * splits < 1024 && maxpos / (AK * 2 * splits) >= 2 && splits < 16) splits *= 2;
+  return splits;
+}
+
 hipError_t launch_attention(bool is_bf16, const void* Q, const void* Kc, const void* Vc, void* O,
-                            PlanView plan, int b, int win_cap, int H, int Hkv, int hd, int maxpos,
-                            int B, hipStream_t st) {
+                            size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
+                            int hd, int maxpos, int B, int kv_splits, float* ws_o, float* ws_ml,
+                            int rows_cap, hipStream_t st) {
   if (is_bf16) {
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
-    dim3 grid((win_cap + AQ - 1) / AQ, H, b);
+    if (kv_splits < 1 || (kv_splits > 1 && (!ws_o || !ws_ml))) return hipErrorInvalidValue;
+    dim3 grid((win_cap + AQ - 1) / AQ, H, b * kv_splits);
     if (hd == 128)
       k_attn_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)Q, (const bf16_t*)Kc, (const bf16_t*)Vc,
-                                             (float*)O, plan.seq_row_start, plan.seq_win_len,
-                                             plan.seq_win_start, H, Hkv, maxpos, B, scale_log2);
+                                             (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
+                                             plan.seq_win_start, H, Hkv, maxpos, B, scale_log2,
+                                             kv_splits, ws_o, ws_ml, rows_cap);
     else if (hd == 64)
       k_attn_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)Q, (const bf16_t*)Kc, (const bf16_t*)Vc,
-                                            (float*)O, plan.seq_row_start, plan.seq_win_len,
-                                            plan.seq_win_start, H, Hkv, maxpos, B, scale_log2);
+                                            (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
+                                            plan.seq_win_start, H, Hkv, maxpos, B, scale_log2,
+                                            kv_splits, ws_o, ws_ml, rows_cap);
     else
       return hipErrorInvalidValue;
+    if (kv_splits > 1)
+      k_attn_merge<<<rows_cap * H, 64, 0, st>>>(ws_o, ws_ml, kv_splits, plan.hdr, H, hd, rows_cap,
+                                                (bf16_t*)O, o_plane);
   } else {
     if (hd != 64 && hd != 128) return hipErrorInvalidValue;
-    const int rows_cap = win_cap * b;
     const int items = rows_cap * H;
     k_attn_f32<<<(items + 3) / 4, 256, 0, st>>>((const float*)Q, (const float*)Kc, (const float*)Vc,
                                                 (float*)O, plan.row_seq, plan.row_pos, plan.hdr, H,

@@ -3,11 +3,11 @@
 // All products are C = A . W^T with A [rows][K] (activations, row-major) and
 // W [N][K] (weights stored [out][in]), so both operands are K-contiguous.
 //
-// bf16 path (bf16 weights, fp32 activations): 128x128x32 workgroup tiles,
-// 4 wave64s in a 2x2 arrangement each owning a 64x64 sub-tile of 4x4 MFMA
-// 16x16x32 bf16 tiles (fp32 accumulate).  Operands are staged through LDS
-// (double-buffered, padded row stride) with 16-byte global loads; one barrier
-// per K-step.
+// bf16 path (bf16 weights, activations as bf16 hi/lo plane pairs): 128x128,
+// 64x128 or 64x64 workgroup tiles with K-steps of 64, 4 wave64s in a 2x2
+// arrangement, MFMA 16x16x32 bf16 with fp32 accumulate.  Operands are staged
+// through LDS (double-buffered, padded row stride) with 16-byte global loads;
+// one barrier per K-step; optional deterministic split-K.
 // f32 path (small fp32 models): 64x64x16 SIMT tiles.
 //
 // The row count M is read from device memory so that a launch sized for the
@@ -18,6 +18,8 @@
 
 namespace bd {
 
+static inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 __device__ __forceinline__ bf16_t f2bf(float f) {
   uint32_t u = __float_as_uint(f);
@@ -25,167 +27,236 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
   return (bf16_t)(u >> 16);
 }
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+// Store x as the bf16 pair (hi at p, lo at p + plane): hi = bf16(x), lo = bf16(x - hi).
+__device__ __forceinline__ void store_pair(bf16_t* p, size_t plane, float x) {
+  const bf16_t h = f2bf(x);
+  p[0] = h;
+  p[plane] = f2bf(x - bf2f(h));
+}
 
 // ------------------------------------------------------------------ bf16 MFMA
-// Activations are fp32 in memory.  While staging a tile into LDS each value
-// x is split into hi = bf16(x) and lo = bf16(x - hi), and the product is
-// accumulated as hi.W + lo.W: two MFMAs per weight fragment give the
-// activation operand 16 significant bits, so that the only activation
-// roundings of the forward are the Q/K/V values stored in the KV cache.
-constexpr int TBM = 128, TBN = 128, TBK = 32, LDSK = TBK + 8;
+// Activation operands are carried as two bf16 planes, hi = bf16(x) and
+// lo = bf16(x - hi), written by the producing kernel; the product is
+// accumulated as hi.W + lo.W, two MFMAs per weight fragment, which gives the
+// operand 16 significant bits, so that the only activation roundings of the
+// forward are the Q/K/V values stored in the KV cache.
+constexpr int TBK = 64, LDSK = TBK + 8;
 
+template <int BM, int BN>
 struct MfmaTile {
-  floatx4 acc[4][4];
+  floatx4 acc[BM / 32][BN / 32];
 };
 
+template <int BM, int BN>
 struct GemmSmem {
-  bf16_t ah[2][TBM * LDSK];
-  bf16_t al[2][TBM * LDSK];
-  bf16_t b[2][TBN * LDSK];
+  bf16_t ah[2][BM * LDSK];
+  bf16_t al[2][BM * LDSK];
+  bf16_t b[2][BN * LDSK];
 };
 
-__device__ __forceinline__ void split4(float4 v, uint2& hi, uint2& lo) {
-  const float x[4] = {v.x, v.y, v.z, v.w};
-  bf16_t h[4], l[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    h[e] = f2bf(x[e]);
-    l[e] = f2bf(x[e] - bf2f(h[e]));
-  }
-  hi = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
-  lo = make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
-}
-
-// Main loop: accumulates the 64x64 sub-tile of this wave.
-__device__ __forceinline__ void mfma_mainloop(const float* __restrict__ A, int lda,
-                                              const bf16_t* __restrict__ W, int ldw, int K, int m0,
-                                              int n0, MfmaTile& t, GemmSmem& sm) {
+// Main loop over K range [k0, k0 + klen): 4 waves in a 2x2 arrangement, each
+// accumulating a (BM/2)x(BN/2) sub-tile of (BM/32)x(BN/32) MFMA tiles.  The
+// activation operand comes as two bf16 planes (hi at A, lo at A + a_plane).
+template <int BM, int BN>
+__device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int lda, size_t a_plane,
+                                              const bf16_t* __restrict__ W, int ldw, int k0,
+                                              int klen, int m0, int n0, MfmaTile<BM, BN>& t,
+                                              GemmSmem<BM, BN>& sm) {
+  constexpr int FM = BM / 32, FN = BN / 32;
+  constexpr int CPR = TBK / 8;          // 16-byte chunks per tile row
+  constexpr int NA = BM * CPR / 256;    // u32x4 per thread and plane for the A tile
+  constexpr int NB = BN * CPR / 256;    // u32x4 per thread for the W tile
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  float4 ra[4];
-  uint4 rb[2];
+  u32x4 rah[NA], ral[NA];
+  u32x4 rb[NB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FN; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // A tile: 128 rows x 32 fp32 = 1024 float4 (4 per thread);
-  // W tile: 128 rows x 32 bf16 = 512 uint4 (2 per thread).
-#define GLOAD(k0)                                                                    \
-  do {                                                                               \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                  \
-      const int c = tid + 256 * i, r = c >> 3, kc = (c & 7) * 4;                     \
-      ra[i] = *(const float4*)(A + (size_t)(m0 + r) * lda + (k0) + kc);              \
-    }                                                                                \
-    _Pragma("unroll") for (int i = 0; i < 2; ++i) {                                  \
-      const int c = tid + 256 * i, r = c >> 2, kc = (c & 3) * 8;                     \
-      rb[i] = *(const uint4*)(W + (size_t)(n0 + r) * ldw + (k0) + kc);               \
-    }                                                                                \
-  } while (0)
-#define SSTORE(buf)                                                                  \
-  do {                                                                               \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                  \
-      const int c = tid + 256 * i, r = c >> 3, kc = (c & 7) * 4;                     \
-      uint2 hi, lo;                                                                  \
-      split4(ra[i], hi, lo);                                                         \
-      *(uint2*)(&sm.ah[buf][r * LDSK + kc]) = hi;                                    \
-      *(uint2*)(&sm.al[buf][r * LDSK + kc]) = lo;                                    \
-    }                                                                                \
-    _Pragma("unroll") for (int i = 0; i < 2; ++i) {                                  \
-      const int c = tid + 256 * i, r = c >> 2, kc = (c & 3) * 8;                     \
-      *(uint4*)(&sm.b[buf][r * LDSK + kc]) = rb[i];                                  \
-    }                                                                                \
-  } while (0)
-
-  GLOAD(0);
-  SSTORE(0);
-  __syncthreads();
-  const int nk = K / TBK;
-  const int arow = wm * 64 + (lane & 15), brow = wn * 64 + (lane & 15), koff = (lane >> 4) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) GLOAD((kt + 1) * TBK);
-    bf16x8 ah[4], al[4], bfr[4];
+  {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ah[i] = *(const bf16x8*)(&sm.ah[buf][(arow + i * 16) * LDSK + koff]);
-      al[i] = *(const bf16x8*)(&sm.al[buf][(arow + i * 16) * LDSK + koff]);
+    for (int i = 0; i < NA; ++i) {
+      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+      const bf16_t* src = A + (size_t)(m0 + r) * lda + k0 + kc;
+      rah[i] = *(const u32x4*)(src);
+      ral[i] = *(const u32x4*)(src + a_plane);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bfr[j] = *(const bf16x8*)(&sm.b[buf][(brow + j * 16) * LDSK + koff]);
+    for (int i = 0; i < NB; ++i) {
+      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+      rb[i] = *(const u32x4*)(W + (size_t)(n0 + r) * ldw + k0 + kc);
+    }
+  }
+  {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NA; ++i) {
+      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+      *(u32x4*)(&sm.ah[0][r * LDSK + kc]) = rah[i];
+      *(u32x4*)(&sm.al[0][r * LDSK + kc]) = ral[i];
+    }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[i], bfr[j], t.acc[i][j], 0, 0, 0);
-        t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[i], bfr[j], t.acc[i][j], 0, 0, 0);
+    for (int i = 0; i < NB; ++i) {
+      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+      *(u32x4*)(&sm.b[0][r * LDSK + kc]) = rb[i];
+    }
+  }
+  __syncthreads();
+  const int nk = klen / TBK;
+  const int arow = wm * (BM / 2) + (lane & 15), brow = wn * (BN / 2) + (lane & 15);
+  const int koff = (lane >> 4) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+        const bf16_t* src = A + (size_t)(m0 + r) * lda + (k0 + (kt + 1) * TBK) + kc;
+        rah[i] = *(const u32x4*)(src);
+        ral[i] = *(const u32x4*)(src + a_plane);
       }
-    if (kt + 1 < nk) SSTORE(buf ^ 1);
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+        rb[i] = *(const u32x4*)(W + (size_t)(n0 + r) * ldw + (k0 + (kt + 1) * TBK) + kc);
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < TBK; kk += 32) {
+      u32x4 bfr[FN];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&sm.b[buf][(brow + j * 16) * LDSK + kk + koff]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const bf16x8 ah = __builtin_bit_cast(bf16x8, *(const u32x4*)(&sm.ah[buf][(arow + i * 16) * LDSK + kk + koff]));
+        const bf16x8 al = __builtin_bit_cast(bf16x8, *(const u32x4*)(&sm.al[buf][(arow + i * 16) * LDSK + kk + koff]));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const bf16x8 bj = __builtin_bit_cast(bf16x8, bfr[j]);
+          t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bj, t.acc[i][j], 0, 0, 0);
+          t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bj, t.acc[i][j], 0, 0, 0);
+        }
+      }
+    }
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+        *(u32x4*)(&sm.ah[buf ^ 1][r * LDSK + kc]) = rah[i];
+        *(u32x4*)(&sm.al[buf ^ 1][r * LDSK + kc]) = ral[i];
+      }
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+        *(u32x4*)(&sm.b[buf ^ 1][r * LDSK + kc]) = rb[i];
+      }
+    }
     __syncthreads();
   }
-#undef GLOAD
-#undef SSTORE
 }
 
-template <int EPI>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const float* __restrict__ A, int lda,
-                                                   const bf16_t* __restrict__ W, int ldw, int N, int K,
+// Epilogue modes; with split-K (gridDim.z > 1) every split writes its raw
+// partial tile to ws[split][row][col] and k_splitk_reduce applies the mode.
+template <int BM, int BN, int EPI>
+__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
+                                                   size_t a_plane, const bf16_t* __restrict__ W,
+                                                   int ldw, int N, int K,
                                                    const int32_t* __restrict__ Mp,
-                                                   float* __restrict__ out, int ldo) {
+                                                   void* __restrict__ out, int ldo, size_t out_plane,
+                                                   float* __restrict__ ws, int rows_cap) {
+  constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
-  const int m0 = blockIdx.y * TBM;
+  const int m0 = blockIdx.y * BM;
   if (m0 >= M) return;
-  const int n0 = blockIdx.x * TBN;
-  __shared__ __attribute__((aligned(16))) GemmSmem sm;
-  MfmaTile t;
-  mfma_mainloop(A, lda, W, ldw, K, m0, n0, t, sm);
+  const int n0 = blockIdx.x * BN;
+  const int splits = gridDim.z, klen = K / splits, k0 = blockIdx.z * klen;
+  __shared__ __attribute__((aligned(16))) GemmSmem<BM, BN> sm;
+  MfmaTile<BM, BN> t;
+  mfma_mainloop<BM, BN>(A, lda, a_plane, W, ldw, k0, klen, m0, n0, t, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
+      const int m = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
       if (m >= M) continue;
-      if constexpr (EPI == EPI_SWIGLU) {
+      if (splits > 1) {
+        float* wrow = ws + ((size_t)blockIdx.z * rows_cap + m) * N;
 #pragma unroll
-        for (int j = 0; j < 4; j += 2) {
-          const int pb = n0 + wn * 64 + j * 16;          // packed column of the gate group
+        for (int j = 0; j < FN; ++j) wrow[n0 + wn * (BN / 2) + j * 16 + (lane & 15)] = t.acc[i][j][r];
+      } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int j = 0; j < FN; j += 2) {
+          const int pb = n0 + wn * (BN / 2) + j * 16;    // packed column of the gate group
           const int col = (pb >> 5) * 16 + (lane & 15);  // output feature
           const float g = t.acc[i][j][r], u = t.acc[i][j + 1][r];
-          out[(size_t)m * ldo + col] = silu(g) * u;
+          store_pair((bf16_t*)out + (size_t)m * ldo + col, out_plane, silu(g) * u);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = n0 + wn * 64 + j * 16 + (lane & 15);
+        for (int j = 0; j < FN; ++j) {
+          const int n = n0 + wn * (BN / 2) + j * 16 + (lane & 15);
           const float v = t.acc[i][j][r];
-          if constexpr (EPI == EPI_ADD_F32) out[(size_t)m * ldo + n] += v;
-          else out[(size_t)m * ldo + n] = v;
+          if constexpr (EPI == EPI_ADD_F32) ((float*)out)[(size_t)m * ldo + n] += v;
+          else ((float*)out)[(size_t)m * ldo + n] = v;
         }
       }
     }
+  }
+}
+
+// Deterministic split-K reduction: sums the splits in order, then applies
+// the epilogue.  One thread per output element (SwiGLU: per output feature).
+template <int EPI>
+__global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ ws, int splits,
+                                                       int N, int rows_cap,
+                                                       const int32_t* __restrict__ Mp,
+                                                       void* __restrict__ out, int ldo,
+                                                       size_t out_plane) {
+  const int M = *Mp;
+  const int ncols = (EPI == EPI_SWIGLU) ? N / 2 : N;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int m = (int)(idx / ncols), c = (int)(idx % ncols);
+  if (m >= M) return;
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int pg = (c >> 4) * 32 + (c & 15);
+    float g = 0.f, u = 0.f;
+    for (int z = 0; z < splits; ++z) {
+      const float* w = ws + ((size_t)z * rows_cap + m) * N;
+      g += w[pg];
+      u += w[pg + 16];
+    }
+    store_pair((bf16_t*)out + (size_t)m * ldo + c, out_plane, silu(g) * u);
+  } else {
+    float v = 0.f;
+    for (int z = 0; z < splits; ++z) v += ws[((size_t)z * rows_cap + m) * N + c];
+    if constexpr (EPI == EPI_ADD_F32) ((float*)out)[(size_t)m * ldo + c] += v;
+    else ((float*)out)[(size_t)m * ldo + c] = v;
   }
 }
 
 // Fused LM head: for its 128 vocabulary columns the workgroup reduces each row
 // to (max z, sum exp(z - max), lowest argmax) and writes one partial per
 // (column tile, row); logits never leave registers.
-__global__ __launch_bounds__(256) void k_lm_head_bf16(const float* __restrict__ A, int d,
+__global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__ A, int d,
+                                                      size_t a_plane,
                                                       const bf16_t* __restrict__ W, int mask_id,
                                                       float scale, const int32_t* __restrict__ Mp,
                                                       int rows_cap, float* __restrict__ pmax,
                                                       float* __restrict__ psum,
                                                       int32_t* __restrict__ parg) {
+  constexpr int TBM = 128, TBN = 128;
   const int M = *Mp;
   const int m0 = blockIdx.y * TBM;
   if (m0 >= M) return;
   const int n0 = blockIdx.x * TBN;
-  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  __shared__ __attribute__((aligned(16))) GemmSmem<TBM, TBN> sm;
   __shared__ float red_m[2][TBM], red_s[2][TBM];
   __shared__ int32_t red_a[2][TBM];
-  MfmaTile t;
-  mfma_mainloop(A, d, W, d, d, m0, n0, t, sm);
+  MfmaTile<TBM, TBN> t;
+  mfma_mainloop<TBM, TBN>(A, d, a_plane, W, d, 0, d, m0, n0, t, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -353,47 +424,107 @@ __global__ __launch_bounds__(256) void k_lm_head_f32(const float* __restrict__ A
   }
 }
 
-// Merge the per-tile partials of each row in tile order (deterministic):
-// conf = 1 / sum_t s_t exp(m_t - max), tok = lowest index attaining the max.
+// Merge the per-tile partials of each row (one wave per row, deterministic):
+// max and lowest argmax over tiles, then sum_t s_t exp(m_t - max) with a
+// fixed lane assignment and a fixed shuffle tree; conf = 1 / sum.
 __global__ __launch_bounds__(256) void k_lm_merge(const float* __restrict__ pmax,
                                                   const float* __restrict__ psum,
                                                   const int32_t* __restrict__ parg, int ntiles,
                                                   const int32_t* __restrict__ Mp, int rows_cap,
                                                   float* __restrict__ conf, int32_t* __restrict__ tok) {
-  const int M = *Mp;
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= M) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + wave;
+  if (m >= *Mp) return;
   float mx = -INFINITY;
-  int arg = 0;
-  for (int t = 0; t < ntiles; ++t) {
+  int arg = 0x7fffffff;
+  for (int t = lane; t < ntiles; t += 64) {
     const float v = pmax[(size_t)t * rows_cap + m];
-    if (v > mx) { mx = v; arg = parg[(size_t)t * rows_cap + m]; }
+    const int a = parg[(size_t)t * rows_cap + m];
+    if (v > mx || (v == mx && a < arg)) { mx = v; arg = a; }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float om = __shfl_xor(mx, off);
+    const int oa = __shfl_xor(arg, off);
+    if (om > mx || (om == mx && oa < arg)) { mx = om; arg = oa; }
   }
   float s = 0.f;
-  for (int t = 0; t < ntiles; ++t) {
+  for (int t = lane; t < ntiles; t += 64) {
     const size_t o = (size_t)t * rows_cap + m;
     s += psum[o] * expf(pmax[o] - mx);
   }
-  conf[m] = 1.0f / s;
-  tok[m] = arg;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane == 0) {
+    conf[m] = 1.0f / s;
+    tok[m] = arg;
+  }
 }
 
 // ------------------------------------------------------------------ launchers
-static inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, const void* W, int ldw, int N,
-                       int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       hipStream_t st) {
+template <int BM, int BN>
+static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const bf16_t* w,
+                            int ldw, int N, int K, const int32_t* M_dev, void* o, int ldo, size_t op,
+                            float* ws, int rows_cap, hipStream_t st) {
+  switch (epi) {
+    case EPI_ADD_F32:
+      k_gemm_bf16<BM, BN, EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, rows_cap);
+      break;
+    case EPI_SWIGLU:
+      k_gemm_bf16<BM, BN, EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, rows_cap);
+      break;
+    default:
+      k_gemm_bf16<BM, BN, EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, rows_cap);
+      break;
+  }
+}
+
+// Tile choice: the largest tile that still gives >= 512 workgroups over the
+// row capacity; otherwise 64x64 tiles with a deterministic split-K (each
+// split at least 512 deep, workspace permitting) to reach that count.
+GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap) {
+  GemmPlan p{64, 64, 1};
+  if (!is_bf16) return p;
+  const int target = 512;
+  const int cand[3][2] = {{128, 128}, {64, 128}, {64, 64}};
+  for (auto& c : cand) {
+    if (N % c[1]) continue;
+    const int wgs = (N / c[1]) * cdiv(rows_cap, c[0]);
+    if (wgs >= target) return GemmPlan{c[0], c[1], 1};
+  }
+  const int wgs = (N / 64) * cdiv(rows_cap, 64);
+  int splits = 1;
+  while (wgs * splits < target && K % (2 * splits * TBK) == 0 && K / (2 * splits) >= 512) splits *= 2;
+  return GemmPlan{64, 64, splits};
+}
+
+size_t gemm_workspace_floats(const GemmPlan& p, int N, int rows_cap) {
+  return p.splits > 1 ? (size_t)p.splits * rows_cap * N : 0;
+}
+
+hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
+                       int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
+                       size_t out_plane, float* ws, size_t ws_floats, hipStream_t st) {
   if (is_bf16) {
-    if (N % TBN || K % TBK) return hipErrorInvalidValue;
-    dim3 grid(N / TBN, cdiv(rows_cap, TBM));
-    const float* a = (const float*)A;
+    GemmPlan p = plan_gemm(true, N, K, rows_cap);
+    if (gemm_workspace_floats(p, N, rows_cap) > ws_floats || !ws) p.splits = 1;
+    if (N % p.bn || K % (TBK * p.splits)) return hipErrorInvalidValue;
+    dim3 grid(N / p.bn, cdiv(rows_cap, p.bm), p.splits);
+    const bf16_t* a = (const bf16_t*)A;
     const bf16_t* w = (const bf16_t*)W;
-    float* o = (float*)out;
-    switch (epi) {
-      case EPI_ADD_F32: k_gemm_bf16<EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, o, ldo); break;
-      case EPI_SWIGLU: k_gemm_bf16<EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, o, ldo); break;
-      default: k_gemm_bf16<EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, o, ldo); break;
+    if (p.bm == 128) launch_bf16_cfg<128, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, rows_cap, st);
+    else if (p.bn == 128) launch_bf16_cfg<64, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, rows_cap, st);
+    else launch_bf16_cfg<64, 64>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, rows_cap, st);
+    if (p.splits > 1) {
+      const int ncols = epi == EPI_SWIGLU ? N / 2 : N;
+      const size_t total = (size_t)rows_cap * ncols;
+      const int blocks = (int)((total + 255) / 256);
+      switch (epi) {
+        case EPI_ADD_F32: k_splitk_reduce<EPI_ADD_F32><<<blocks, 256, 0, st>>>(ws, p.splits, N, rows_cap, M_dev, out, ldo, out_plane); break;
+        case EPI_SWIGLU: k_splitk_reduce<EPI_SWIGLU><<<blocks, 256, 0, st>>>(ws, p.splits, N, rows_cap, M_dev, out, ldo, out_plane); break;
+        default: k_splitk_reduce<EPI_STORE_F32><<<blocks, 256, 0, st>>>(ws, p.splits, N, rows_cap, M_dev, out, ldo, out_plane); break;
+      }
     }
   } else {
     if (N % SBN || K % SBK) return hipErrorInvalidValue;
@@ -409,16 +540,17 @@ hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, const void
   return hipGetLastError();
 }
 
-hipError_t launch_lm_head(bool is_bf16, const void* A, int d, const void* W, int V, int mask_id,
-                          float scale, const int32_t* M_dev, int rows_cap, float* part_max,
+hipError_t launch_lm_head(bool is_bf16, const void* A, int d, size_t a_plane, const void* W, int V,
+                          int mask_id, float scale, const int32_t* M_dev, int rows_cap,
+                          float* part_max,
                           float* part_sum, int32_t* part_arg, float* conf, int32_t* tok,
                           hipStream_t st) {
   int ntiles;
   if (is_bf16) {
-    if (V % TBN || d % TBK) return hipErrorInvalidValue;
-    ntiles = V / TBN;
-    dim3 grid(ntiles, cdiv(rows_cap, TBM));
-    k_lm_head_bf16<<<grid, 256, 0, st>>>((const float*)A, d, (const bf16_t*)W, mask_id, scale, M_dev,
+    if (V % 128 || d % TBK) return hipErrorInvalidValue;
+    ntiles = V / 128;
+    dim3 grid(ntiles, cdiv(rows_cap, 128));
+    k_lm_head_bf16<<<grid, 256, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, mask_id, scale, M_dev,
                                         rows_cap, part_max, part_sum, part_arg);
   } else {
     if (V % SBN || d % SBK) return hipErrorInvalidValue;
@@ -427,8 +559,8 @@ hipError_t launch_lm_head(bool is_bf16, const void* A, int d, const void* W, int
     k_lm_head_f32<<<grid, 256, 0, st>>>((const float*)A, d, (const float*)W, mask_id, scale, M_dev,
                                        rows_cap, part_max, part_sum, part_arg);
   }
-  k_lm_merge<<<cdiv(rows_cap, 256), 256, 0, st>>>(part_max, part_sum, part_arg, ntiles, M_dev, rows_cap,
-                                                  conf, tok);
+  k_lm_merge<<<cdiv(rows_cap, 4), 256, 0, st>>>(part_max, part_sum, part_arg, ntiles, M_dev, rows_cap,
+                                                conf, tok);
   return hipGetLastError();
 }
 
@@ -442,10 +574,11 @@ __global__ void k_logits_post(float* __restrict__ z, int V, int mask_id, float s
   }
 }
 
-hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, const void* W, int V, int mask_id,
-                            float scale, const int32_t* M_dev, int rows_cap, float* logits,
-                            hipStream_t st) {
-  hipError_t e = launch_gemm(EPI_STORE_F32, is_bf16, A, d, W, d, V, d, M_dev, rows_cap, logits, V, st);
+hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, size_t a_plane, const void* W, int V,
+                            int mask_id, float scale, const int32_t* M_dev, int rows_cap,
+                            float* logits, hipStream_t st) {
+  hipError_t e = launch_gemm(EPI_STORE_F32, is_bf16, A, d, a_plane, W, d, V, d, M_dev, rows_cap,
+                             logits, V, 0, nullptr, 0, st);
   if (e != hipSuccess) return e;
   k_logits_post<<<dim3(cdiv(V, 256 * 8), rows_cap), 256, 0, st>>>(logits, V, mask_id, scale, M_dev);
   return hipGetLastError();

@@ -11,6 +11,9 @@ typedef uint16_t bf16_t;   // bfloat16 bit pattern in memory
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+// native 16-byte vector (HIP's uint4 is a struct, which keeps register arrays
+// of it on the stack)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Per-sequence decode descriptor, int32 fields of seq_state[b][SS_N].
 enum {
@@ -61,35 +64,52 @@ enum { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
 
 // ---- launchers (defined in the .hip files) ---------------------------------
 // C[M][N] (+)= A[M][K] . W[N][K]^T with M read from *M_dev; grid covers rows_cap.
-// A is fp32 for every model; W is bf16 (is_bf16) or fp32.  out is fp32:
-//   EPI_STORE_F32 / EPI_ADD_F32: [M][ldo]
-//   EPI_SWIGLU: silu(gate) * up [M][ldo], W packed gate/up in 16-row groups
-hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, const void* W, int ldw, int N,
-                       int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       hipStream_t st);
+// bf16 models: A is a bf16 plane pair (hi at A, lo at A + a_plane elements),
+// W bf16.  fp32 models: A and W fp32 (a_plane unused).
+//   EPI_STORE_F32 / EPI_ADD_F32: out fp32 [M][ldo]
+//   EPI_SWIGLU: silu(gate) * up [M][ldo] (W packed gate/up in 16-row groups),
+//   as a bf16 plane pair (out_plane) for bf16 models, fp32 otherwise
+//   ws (optional, ws_floats capacity): split-K workspace; without room the
+//   launch runs unsplit.
+hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
+                       int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
+                       size_t out_plane, float* ws, size_t ws_floats, hipStream_t st);
+struct GemmPlan {
+  int bm, bn, splits;
+};
+GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap);
+size_t gemm_workspace_floats(const GemmPlan& p, int N, int rows_cap);
 
 // LM head: per-row softmax statistics over the vocabulary of
 // z = scale * (A . W^T), mask column suppressed.  Writes per-(tile,row)
 // partials, then merges them into conf/tok.
-hipError_t launch_lm_head(bool is_bf16, const void* A, int d, const void* W, int V, int mask_id,
-                          float scale, const int32_t* M_dev, int rows_cap, float* part_max,
-                          float* part_sum, int32_t* part_arg, float* conf, int32_t* tok,
-                          hipStream_t st);
+hipError_t launch_lm_head(bool is_bf16, const void* A, int d, size_t a_plane, const void* W, int V,
+                          int mask_id, float scale, const int32_t* M_dev, int rows_cap,
+                          float* part_max, float* part_sum, int32_t* part_arg, float* conf,
+                          int32_t* tok, hipStream_t st);
 // Debug: full logits [rows][V] for the LM rows (scaled, mask column = -inf).
-hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, const void* W, int V, int mask_id,
-                            float scale, const int32_t* M_dev, int rows_cap, float* logits,
-                            hipStream_t st);
+hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, size_t a_plane, const void* W, int V,
+                            int mask_id, float scale, const int32_t* M_dev, int rows_cap,
+                            float* logits, hipStream_t st);
 
+// kv_splits > 1 splits every query tile's key range into that many
+// workgroups (partials in ws_o [splits][rows_cap][H][hd], ws_ml
+// [splits][rows_cap][H][2]) merged in split order.  rows_cap bounds the rows.
+// O: bf16 plane pair (lo at O + o_plane elements) for bf16 models, fp32 otherwise.
 hipError_t launch_attention(bool is_bf16, const void* Q, const void* Kc, const void* Vc, void* O,
-                            PlanView plan, int b, int win_cap, int H, int Hkv, int hd, int maxpos,
-                            int B, hipStream_t st);
+                            size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
+                            int hd, int maxpos, int B, int kv_splits, float* ws_o, float* ws_ml,
+                            int rows_cap, hipStream_t st);
+int attention_splits(int b, int win_cap, int H, int maxpos);
 
 hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
                         int vocab, PlanView plan, int rows_cap, float* X, int32_t* err_flag,
                         hipStream_t st);
+// out: fp32 [rows][d] (fp32 models) or a bf16 plane pair (bf16 models,
+// lo plane at out + out_plane elements).
 hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
-                          hipStream_t st);
+                          size_t out_plane, hipStream_t st);
 hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
                           int Hkv, int hd, const double* inv_freq, void* Q, void* Kc, void* Vc,
                           int maxpos, hipStream_t st);

@@ -50,31 +50,87 @@ hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, con
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One wave per row: y = x / sqrt(mean(x^2) + eps) * g in fp32 (the GEMMs take
-// fp32 activations).  `gather` (optional) picks the source row of each row.
+// One wave per row: y = x / sqrt(mean(x^2) + eps) * g in fp32.  Output as
+// fp32 (fp32 models) or as the bf16 pair hi = bf16(y), lo = bf16(y - hi) in
+// two planes (bf16 models: the matmul operand format).  Rows of d % 256 == 0
+// (d <= 4096) are read with all float4 loads in flight at once.
+__device__ __forceinline__ void put4(void* out, size_t plane, size_t idx, float4 y, bool pair) {
+  if (!pair) {
+    *(float4*)((float*)out + idx) = y;
+    return;
+  }
+  const float v[4] = {y.x, y.y, y.z, y.w};
+  bf16_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    h[e] = f2bf_m(v[e]);
+    l[e] = f2bf_m(v[e] - bf2f_m(h[e]));
+  }
+  bf16_t* o = (bf16_t*)out + idx;
+  *(uint2*)o = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+  *(uint2*)(o + plane) =
+      make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
+}
+
+template <bool PAIR>
 __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X,
                                                  const float* __restrict__ g, int d, float eps,
                                                  const int32_t* __restrict__ Mp,
                                                  const int32_t* __restrict__ gather,
-                                                 float* __restrict__ out) {
+                                                 void* __restrict__ out, size_t plane) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + wave;
   if (row >= *Mp) return;
   const int src = gather ? gather[row] : row;
   const float* x = X + (size_t)src * d;
+  if (d % 256 == 0 && d <= 4096) {
+    const int n4 = d / 256;
+    float4 v[16];
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < n4) v[i] = *(const float4*)(x + (i * 64 + lane) * 4);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < n4) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < n4) {
+        const int c = (i * 64 + lane) * 4;
+        const float4 gg = *(const float4*)(g + c);
+        const float4 y = make_float4(v[i].x * inv * gg.x, v[i].y * inv * gg.y, v[i].z * inv * gg.z,
+                                     v[i].w * inv * gg.w);
+        put4(out, plane, (size_t)row * d + c, y, PAIR);
+      }
+    return;
+  }
   float ss = 0.f;
   for (int c = lane; c < d; c += 64) ss += x[c] * x[c];
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int c = lane; c < d; c += 64) out[(size_t)row * d + c] = x[c] * inv * g[c];
+  for (int c = lane; c < d; c += 64) {
+    const float y = x[c] * inv * g[c];
+    if (PAIR) {
+      const bf16_t h = f2bf_m(y);
+      ((bf16_t*)out)[(size_t)row * d + c] = h;
+      ((bf16_t*)out)[(size_t)row * d + c + plane] = f2bf_m(y - bf2f_m(h));
+    } else {
+      ((float*)out)[(size_t)row * d + c] = y;
+    }
+  }
 }
 
 hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
-                          hipStream_t st) {
-  (void)is_bf16;
-  k_rmsnorm<<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, (float*)out);
+                          size_t out_plane, hipStream_t st) {
+  if (is_bf16)
+    k_rmsnorm<true><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, out_plane);
+  else
+    k_rmsnorm<false><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, 0);
   return hipGetLastError();
 }
 

@@ -48,6 +48,9 @@ SMALL = {
                      prompt_len=8, block_size=8, n_inflight=2, gen_len=48),
     "block1": small("block1", seed=93, batch=2, prompt_len=5, block_size=1, n_inflight=1, gen_len=12,
                     dtype="f32"),
+    # long prefix: the attention key range is split over several workgroups
+    "longprefix": small("longprefix", seed=94, n_heads=4, n_kv_heads=2, head_dim=128, batch=2,
+                        prompt_len=2048, block_size=32, n_inflight=2, gen_len=64),
 }
 
 _models = {}
