@@ -37,7 +37,8 @@ def algorithmic_work(w, stats):
     (counters summed over one decode).  Bytes count each weight once per
     forward, the K/V read once per (sequence, kv head, layer) and the window
     K/V written; FLOPs count only visible query-key pairs and masked LM rows."""
-    esz = 2 if w.dtype == "bf16" else 4
+    esz = 2 if w.dtype == "bf16" else 4     # weights
+    asz = 4                                  # activations / KV: fp32 or a bf16 hi/lo pair
     d, H, Hkv, hd, F, V, L = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.ffn_dim, w.vocab, w.n_layers
     qkv = (H + 2 * Hkv) * hd
     rows, lm_rows, fw = stats["rows"], stats["lm_rows"], stats["forwards"]
@@ -47,12 +48,12 @@ def algorithmic_work(w, stats):
     out = {}
     for k, (N, K) in gemm.items():
         flops = 2.0 * rows * N * K * L
-        byts = (N * K * esz * fw + rows * K * esz + rows * N * 4) * L
+        byts = (N * K * esz * fw + rows * K * asz + rows * N * 4) * L
         out[k] = (flops, byts)
     out["attn"] = (4.0 * hd * H * stats["pairs"] * L,
-                   (stats["keys"] * Hkv * hd * 2 * esz + rows * (H + 2 * Hkv) * hd * esz
-                    + rows * H * hd * esz) * L)
-    out["lm_head"] = (2.0 * lm_rows * V * d, V * d * esz * fw + lm_rows * d * esz)
+                   (stats["keys"] * Hkv * hd * 2 * asz + rows * H * hd * asz
+                    + rows * H * hd * asz) * L)
+    out["lm_head"] = (2.0 * lm_rows * V * d, V * d * esz * fw + lm_rows * d * asz)
     return out
 
 

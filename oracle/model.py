@@ -17,13 +17,11 @@ What is computed, and where it comes from:
 
 Precision modes
   ``"f64"``  every operand and every operation in float64.
-  ``"bf16"`` bf16 weights with the storage points of the bf16 kernels:
-             * Q, K and V after RoPE are stored as bfloat16 (the KV cache):
-               fp64 -> fp32 -> bf16, nearest-even;
-             * every matmul activation operand (RMSNorm outputs, attention
-               output, SwiGLU product, final-norm output) is carried as fp32
-               and fed as the bf16 pair hi = bf16(x), lo = bf16(x - hi), i.e.
-               x to 16 significant bits;
+  ``"bf16"`` bf16 weights; every stored activation -- the matmul operands
+             (RMSNorm outputs, attention output, SwiGLU product, final-norm
+             output) and Q, K, V after RoPE (the KV cache) -- is fp32(x)
+             carried as the bf16 pair hi = bf16(x), lo = bf16(x - hi), i.e.
+             x to 16 significant bits (nearest-even at both roundings);
              matmuls run as float32 BLAS on those operands; residual stream,
              attention softmax, norms and router in float64.
 """
@@ -128,8 +126,8 @@ class OracleModel:
 
     # -- storage points ---------------------------------------------------
     def _store(self, x: np.ndarray) -> np.ndarray:
-        """Q/K/V as stored in the cache: bf16 in bf16 mode, unchanged in f64."""
-        return round_bf16(x) if self.precision == "bf16" else x
+        """Q/K/V as stored in the cache: the bf16 pair value in bf16 mode."""
+        return split_bf16x2(x) if self.precision == "bf16" else x
 
     def _operand(self, x: np.ndarray) -> np.ndarray:
         """Matmul activation operand: the bf16 pair value in bf16 mode."""
@@ -162,15 +160,22 @@ class OracleModel:
         key j iff j // B <= p // B.  GQA: q-head h reads kv-head h // (H/Hkv)."""
         e = K.shape[0]
         kpos = np.arange(e)
-        visible = (kpos[None, :] // B) <= (qpos[:, None] // B)          # [W][e]
         group = self.H // self.Hkv
         out = np.empty(q.shape, dtype=np.float64)
         scale = 1.0 / math.sqrt(self.hd)
-        for h in range(self.H):
-            kv = h // group
-            s = (q[:, h, :] @ K[:, kv, :].astype(np.float64).T) * scale
-            s = np.where(visible, s, -np.inf)
-            out[:, h, :] = _softmax_rows(s) @ V[:, kv, :].astype(np.float64)
+        Kd = K.astype(np.float64)
+        Vd = V.astype(np.float64)
+        # query rows are independent; chunks of rows only bound the memory of
+        # the score matrix
+        for r0 in range(0, q.shape[0], 1024):
+            r1 = min(q.shape[0], r0 + 1024)
+            kend = int((qpos[r1 - 1] // B + 1) * B)                   # keys any row here sees
+            visible = (kpos[None, :kend] // B) <= (qpos[r0:r1, None] // B)
+            for h in range(self.H):
+                kv = h // group
+                s = (q[r0:r1, h, :] @ Kd[:kend, kv, :].T) * scale
+                s = np.where(visible, s, -np.inf)
+                out[r0:r1, h, :] = _softmax_rows(s) @ Vd[:kend, kv, :]
         return out
 
     def dense_ffn(self, a: np.ndarray, L) -> np.ndarray:

@@ -266,7 +266,11 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
   const hipStream_t st = m->stream;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int qkv = (H + 2 * Hkv) * hd;
+  // cache layout [layer][seq][kv head][pos][hd]; bf16 models keep the lo
+  // planes of Q and of the whole cache after the hi planes
   const size_t layer_kv = (size_t)s->b * Hkv * s->maxpos * hd * m->esz;
+  const size_t kv_plane = bf ? (size_t)c.n_layers * s->b * Hkv * s->maxpos * hd : 0;
+  const size_t q_plane = bf ? (size_t)s->rows_cap * H * hd : 0;
   const int kv_splits = (bf && lm) ? s->attn_splits : 1;
   LAUNCH(BD_PROF_EMBED, launch_embed(bf, s->tokens, s->P + s->G, m->embed, d, c.vocab, plan,
                                      rows_cap, s->X, m->err_flag, st));
@@ -280,8 +284,9 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
                                          plan.hdr, rows_cap, s->QKV, qkv, 0, s->gemm_ws,
                                          s->gemm_ws_floats, st));
     LAUNCH(BD_PROF_ROPE, launch_rope_kv(bf, s->QKV, plan, rows_cap, H, Hkv, hd, m->inv_freq, s->Qb,
-                                        Kl, Vl, s->maxpos, st));
-    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, Kl, Vl, s->Ob, s->pl_O, plan, s->b, win_cap, H, Hkv, hd,
+                                        q_plane, Kl, Vl, kv_plane, s->maxpos, st));
+    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, q_plane, Kl, Vl, kv_plane, s->Ob, s->pl_O, plan,
+                                          s->b, win_cap, H, Hkv, hd,
                                           s->maxpos, s->B, kv_splits, s->attn_ws_o, s->attn_ws_ml,
                                           rows_cap, st));
     LAUNCH(BD_PROF_GEMM_O, launch_gemm(EPI_ADD_F32, bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d,
@@ -370,7 +375,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
     s->pl_lm = (size_t)s->lm_cap * d;
   }
   ALLOC(s->QKV, (size_t)s->rows_cap * qkv * 4);
-  ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * esz);
+  ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * 4);     // fp32, or a bf16 plane pair
   ALLOC(s->Ob, (size_t)s->rows_cap * H * hd * 4);
   ALLOC(s->Hact, (size_t)s->rows_cap * c.ffn_dim * 4);
   ALLOC(s->Alm, (size_t)s->lm_cap * d * 4);
@@ -379,7 +384,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ALLOC(s->parg, (size_t)ntiles * s->lm_cap * 4);
   ALLOC(s->conf, (size_t)s->lm_cap * 4);
   ALLOC(s->tok, (size_t)s->lm_cap * 4);
-  const size_t kv_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * esz;
+  const size_t kv_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * 4;   // fp32 or 2 bf16 planes
   ALLOC(s->Kc, kv_bytes);
   ALLOC(s->Vc, kv_bytes);
   {

@@ -5,10 +5,12 @@
 // so one key range [0, end of the query's block) covers prefix and window.
 //
 // bf16 kernel: one workgroup = 64 query rows of one head (4 wave64s x 16
-// queries).  Key tiles of 64 positions stream from HBM through LDS with
-// 16-byte coalesced loads (K row-major, V transposed), and the wave computes
-// S^T = K Q^T and O^T += V^T P^T with MFMA 16x16x32 bf16 (P^T as a hi/lo
-// bf16 pair; the output leaves as the hi/lo pair of the next matmul operand),
+// queries).  Q, K and V are bf16 hi/lo pairs (two planes).  Key tiles of 64
+// positions stream from HBM through LDS with 16-byte coalesced loads (K
+// row-major, V transposed), and the wave computes
+// S^T = K Q^T and O^T += V^T P^T with MFMA 16x16x32 bf16 (three products
+// hi.hi + hi.lo + lo.hi per pair of operands; the output leaves as the hi/lo
+// pair of the next matmul operand),
 // so each lane owns
 // one query column: the online-softmax state and the O rescale stay in the
 // lane, and P^T is fed to the second MFMA straight from the score registers
@@ -31,9 +33,9 @@ constexpr int AQ = 64;    // query rows per workgroup
 constexpr int AK = 64;    // keys per tile
 
 template <int HD>
-__global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
+__global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q, size_t q_plane,
                                                    const bf16_t* __restrict__ Kc,
-                                                   const bf16_t* __restrict__ Vc,
+                                                   const bf16_t* __restrict__ Vc, size_t kv_plane,
                                                    bf16_t* __restrict__ O, size_t o_plane,
                                                    const int32_t* __restrict__ seq_row_start,
                                                    const int32_t* __restrict__ seq_win_len,
@@ -43,10 +45,12 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
                                                    float* __restrict__ ws_ml, int rows_cap) {
   constexpr int KP = HD + 8;        // padded K row (elements)
   constexpr int VP = AK + 8;        // padded transposed-V row
-  constexpr int CH = AK * HD / 8;   // 16-byte chunks per K (or V) tile
+  constexpr int CH = AK * HD / 8;   // 16-byte chunks per K (or V) tile and plane
   constexpr int NCH = CH / 256;     // chunks per thread
-  __shared__ __attribute__((aligned(16))) bf16_t sK[AK * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t sVt[HD * VP];
+  __shared__ __attribute__((aligned(16))) bf16_t sKh[AK * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t sKl[AK * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t sVh[HD * VP];
+  __shared__ __attribute__((aligned(16))) bf16_t sVl[HD * VP];
 
   const int s = blockIdx.z / kv_splits, split = blockIdx.z % kv_splits;
   const int h = blockIdx.y, qt = blockIdx.x;
@@ -72,36 +76,44 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
   const int qpos = pos0 + q;
   const int qend = ((qpos / B) + 1) * B;                      // this query's key bound
 
-  // Q^T fragments (B operand of S^T = K Q^T): dims [32 kc + 8 g, +8) of query c.
-  bf16x8 qf[HD / 32];
+  // Q^T fragments (B operand of S^T = K Q^T): dims [32 kc + 8 g, +8) of query c,
+  // hi and lo halves.
+  bf16x8 qh[HD / 32], ql[HD / 32];
 #pragma unroll
   for (int kc = 0; kc < HD / 32; ++kc) {
-    if (qvalid)
-      qf[kc] = *(const bf16x8*)(Q + ((size_t)(row0 + q) * H + h) * HD + kc * 32 + g * 8);
-    else
-      qf[kc] = bf16x8{};
+    if (qvalid) {
+      const bf16_t* qp = Q + ((size_t)(row0 + q) * H + h) * HD + kc * 32 + g * 8;
+      qh[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)qp);
+      ql[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + q_plane));
+    } else {
+      qh[kc] = bf16x8{};
+      ql[kc] = bf16x8{};
+    }
   }
   floatx4 oacc[HD / 16];
 #pragma unroll
   for (int t = 0; t < HD / 16; ++t) oacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
-  // register prefetch of the next K/V tile overlaps the loads with the MFMAs
-  u32x4 pk[NCH], pv[NCH];
-  auto fetch = [&](int k0) {
-#pragma unroll
-    for (int it = 0; it < NCH; ++it) {
-      const int ci = tid + 256 * it;
-      const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
-      pk[it] = u32x4{0u, 0u, 0u, 0u};
-      pv[it] = u32x4{0u, 0u, 0u, 0u};
-      if (k0 + key < kend) {
-        pk[it] = *(const u32x4*)(Kp + (size_t)(k0 + key) * HD + dc);
-        pv[it] = *(const u32x4*)(Vp + (size_t)(k0 + key) * HD + dc);
-      }
-    }
-  };
-  if (t_lo < t_hi) fetch(t_lo * AK);
+  // register prefetch of the next K/V tile (both planes) overlaps the loads
+  // with the MFMAs of the current tile
+  u32x4 pkh[NCH], pkl[NCH], pvh[NCH], pvl[NCH];
+#define BD_FETCH(K0)                                                            \
+  do {                                                                          \
+    _Pragma("unroll") for (int it = 0; it < NCH; ++it) {                        \
+      const int ci = tid + 256 * it;                                            \
+      const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;                  \
+      pkh[it] = pkl[it] = pvh[it] = pvl[it] = u32x4{0u, 0u, 0u, 0u};            \
+      if ((K0) + key < kend) {                                                  \
+        const size_t o = (size_t)((K0) + key) * HD + dc;                        \
+        pkh[it] = *(const u32x4*)(Kp + o);                                      \
+        pkl[it] = *(const u32x4*)(Kp + o + kv_plane);                           \
+        pvh[it] = *(const u32x4*)(Vp + o);                                      \
+        pvl[it] = *(const u32x4*)(Vp + o + kv_plane);                           \
+      }                                                                         \
+    }                                                                           \
+  } while (0)
+  if (t_lo < t_hi) BD_FETCH(t_lo * AK);
   for (int kt = t_lo; kt < t_hi; ++kt) {
     const int k0 = kt * AK;
     // stage K (row-major) and V (transposed); keys >= kend are zero
@@ -109,23 +121,32 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
     for (int it = 0; it < NCH; ++it) {
       const int ci = tid + 256 * it;
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
-      *(u32x4*)(sK + key * KP + dc) = pk[it];
-      const bf16_t* vv = (const bf16_t*)&pv[it];
+      *(u32x4*)(sKh + key * KP + dc) = pkh[it];
+      *(u32x4*)(sKl + key * KP + dc) = pkl[it];
+      const bf16_t* vh = (const bf16_t*)&pvh[it];
+      const bf16_t* vl = (const bf16_t*)&pvl[it];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sVt[(dc + e) * VP + key] = vv[e];
+      for (int e = 0; e < 8; ++e) {
+        sVh[(dc + e) * VP + key] = vh[e];
+        sVl[(dc + e) * VP + key] = vl[e];
+      }
     }
     __syncthreads();
-    if (kt + 1 < t_hi) fetch(k0 + AK);
+    if (kt + 1 < t_hi) BD_FETCH(k0 + AK);
 
-    // S^T sub-tiles: keys st*16 + 4g + r, query c
+    // S^T sub-tiles (keys st*16 + 4g + r, query c): Kh.Qh + Kh.Ql + Kl.Qh
     float sv[4][4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       floatx4 a = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kc = 0; kc < HD / 32; ++kc) {
-        const bf16x8 kf = *(const bf16x8*)(sK + (st * 16 + c) * KP + kc * 32 + g * 8);
-        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], a, 0, 0, 0);
+        const int off = (st * 16 + c) * KP + kc * 32 + g * 8;
+        const bf16x8 kh = __builtin_bit_cast(bf16x8, *(const u32x4*)(sKh + off));
+        const bf16x8 kl = __builtin_bit_cast(bf16x8, *(const u32x4*)(sKl + off));
+        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh[kc], a, 0, 0, 0);
+        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql[kc], a, 0, 0, 0);
+        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh[kc], a, 0, 0, 0);
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) sv[st][r] = a[r];
@@ -154,7 +175,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
     l_part *= alpha;
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t) oacc[t] *= alpha;
-    // P^T as a hi/lo bf16 pair (p = hi + lo to 16 significant bits)
+    // P^T as a hi/lo bf16 pair
     bf16x8 ph[2], pl[2];
 #pragma unroll
     for (int st = 0; st < 4; ++st)
@@ -168,23 +189,32 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
         pl[st >> 1][(st & 1) * 4 + r] = __builtin_bit_cast(__bf16, lb);
       }
     // O^T += V^T P^T over 2 chunks of 32 keys; k-slot 8g+r <-> key 32kc+4g+r,
-    // k-slot 8g+4+r <-> key 32kc+16+4g+r (same permutation as the scores).
+    // k-slot 8g+4+r <-> key 32kc+16+4g+r (same permutation as the scores):
+    // Vh.Ph + Vh.Pl + Vl.Ph
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
 #pragma unroll
       for (int t = 0; t < HD / 16; ++t) {
-        const bf16_t* vrow = sVt + (t * 16 + c) * VP + kc * 32 + 4 * g;
-        const bf16x4 lo = *(const bf16x4*)(vrow);
-        const bf16x4 hi = *(const bf16x4*)(vrow + 16);
-        bf16x8 vf;
-        vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
-        vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
-        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, ph[kc], oacc[t], 0, 0, 0);
-        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[kc], oacc[t], 0, 0, 0);
+        const int off = (t * 16 + c) * VP + kc * 32 + 4 * g;
+        bf16x8 vh, vl;
+        {
+          const bf16x4 a0 = *(const bf16x4*)(sVh + off);
+          const bf16x4 a1 = *(const bf16x4*)(sVh + off + 16);
+          const bf16x4 b0 = *(const bf16x4*)(sVl + off);
+          const bf16x4 b1 = *(const bf16x4*)(sVl + off + 16);
+          vh[0] = a0[0]; vh[1] = a0[1]; vh[2] = a0[2]; vh[3] = a0[3];
+          vh[4] = a1[0]; vh[5] = a1[1]; vh[6] = a1[2]; vh[7] = a1[3];
+          vl[0] = b0[0]; vl[1] = b0[1]; vl[2] = b0[2]; vl[3] = b0[3];
+          vl[4] = b1[0]; vl[5] = b1[1]; vl[6] = b1[2]; vl[7] = b1[3];
+        }
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, ph[kc], oacc[t], 0, 0, 0);
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, pl[kc], oacc[t], 0, 0, 0);
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl, ph[kc], oacc[t], 0, 0, 0);
       }
     }
     __syncthreads();
   }
+#undef BD_FETCH
   float l = l_part;
   l += __shfl_xor(l, 16);
   l += __shfl_xor(l, 32);
@@ -302,22 +332,22 @@ int attention_splits(int b, int win_cap, int H, int maxpos) {
   return splits;
 }
 
-hipError_t launch_attention(bool is_bf16, const void* Q, const void* Kc, const void* Vc, void* O,
-                            size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
-                            int hd, int maxpos, int B, int kv_splits, float* ws_o, float* ws_ml,
-                            int rows_cap, hipStream_t st) {
+hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const void* Kc,
+                            const void* Vc, size_t kv_plane, void* O, size_t o_plane, PlanView plan,
+                            int b, int win_cap, int H, int Hkv, int hd, int maxpos, int B,
+                            int kv_splits, float* ws_o, float* ws_ml, int rows_cap, hipStream_t st) {
   if (is_bf16) {
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
     if (kv_splits < 1 || (kv_splits > 1 && (!ws_o || !ws_ml))) return hipErrorInvalidValue;
     dim3 grid((win_cap + AQ - 1) / AQ, H, b * kv_splits);
     if (hd == 128)
-      k_attn_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)Q, (const bf16_t*)Kc, (const bf16_t*)Vc,
-                                             (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
+      k_attn_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)Q, q_plane, (const bf16_t*)Kc,
+                                             (const bf16_t*)Vc, kv_plane, (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
                                              plan.seq_win_start, H, Hkv, maxpos, B, scale_log2,
                                              kv_splits, ws_o, ws_ml, rows_cap);
     else if (hd == 64)
-      k_attn_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)Q, (const bf16_t*)Kc, (const bf16_t*)Vc,
-                                            (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
+      k_attn_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)Q, q_plane, (const bf16_t*)Kc,
+                                            (const bf16_t*)Vc, kv_plane, (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
                                             plan.seq_win_start, H, Hkv, maxpos, B, scale_log2,
                                             kv_splits, ws_o, ws_ml, rows_cap);
     else

@@ -96,10 +96,10 @@ hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, size_t a_plane, 
 // workgroups (partials in ws_o [splits][rows_cap][H][hd], ws_ml
 // [splits][rows_cap][H][2]) merged in split order.  rows_cap bounds the rows.
 // O: bf16 plane pair (lo at O + o_plane elements) for bf16 models, fp32 otherwise.
-hipError_t launch_attention(bool is_bf16, const void* Q, const void* Kc, const void* Vc, void* O,
-                            size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
-                            int hd, int maxpos, int B, int kv_splits, float* ws_o, float* ws_ml,
-                            int rows_cap, hipStream_t st);
+hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const void* Kc,
+                            const void* Vc, size_t kv_plane, void* O, size_t o_plane, PlanView plan,
+                            int b, int win_cap, int H, int Hkv, int hd, int maxpos, int B,
+                            int kv_splits, float* ws_o, float* ws_ml, int rows_cap, hipStream_t st);
 int attention_splits(int b, int win_cap, int H, int maxpos);
 
 hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
@@ -110,9 +110,11 @@ hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, con
 hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
                           size_t out_plane, hipStream_t st);
+// bf16 models: Q and the caches hold bf16 pairs (lo planes at + q_plane and
+// + kv_plane elements); fp32 models: fp32 values.
 hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
-                          int Hkv, int hd, const double* inv_freq, void* Q, void* Kc, void* Vc,
-                          int maxpos, hipStream_t st);
+                          int Hkv, int hd, const double* inv_freq, void* Q, size_t q_plane, void* Kc,
+                          void* Vc, size_t kv_plane, int maxpos, hipStream_t st);
 
 struct CommitArgs {
   PlanView in, out;

@@ -135,17 +135,31 @@ hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, f
 }
 
 // ------------------------------------------------------------------ RoPE + KV
-// Rotate-half RoPE of q and k at the row's absolute position (angle in fp64,
-// rotation in fp64, rounded once to the storage type); q -> Q[row][head][hd],
-// k and v -> the layer's cache slot [seq][kv head][pos][hd].
+// Rotate-half RoPE of q and k at the row's absolute position (angle and
+// rotation in fp64, one rounding to fp32); q -> Q[row][head][hd], k and v ->
+// the layer's cache slot [seq][kv head][pos][hd].  bf16 models store each
+// value as the bf16 pair hi = bf16(x), lo = bf16(x - hi) in two planes (lo at
+// + q_plane for Q, + kv_plane for the caches); fp32 models store fp32.
+template <bool BF16>
+__device__ __forceinline__ void put_val(void* base, size_t idx, size_t plane, float y) {
+  if constexpr (BF16) {
+    const bf16_t h = f2bf_m(y);
+    ((bf16_t*)base)[idx] = h;
+    ((bf16_t*)base)[idx + plane] = f2bf_m(y - bf2f_m(h));
+  } else {
+    ((float*)base)[idx] = y;
+  }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ QKV,
                                                  const int32_t* __restrict__ hdr,
                                                  const int32_t* __restrict__ row_seq,
                                                  const int32_t* __restrict__ row_pos, int H, int Hkv,
                                                  int hd, const double* __restrict__ inv_freq,
-                                                 void* __restrict__ Q, void* __restrict__ Kc,
-                                                 void* __restrict__ Vc, int maxpos) {
+                                                 void* __restrict__ Q, size_t q_plane,
+                                                 void* __restrict__ Kc, void* __restrict__ Vc,
+                                                 size_t kv_plane, int maxpos) {
   const int r = blockIdx.x;
   if (r >= hdr[0]) return;
   const int s = row_seq[r], pos = row_pos[r];
@@ -157,41 +171,32 @@ __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ QKV,
     sincos((double)pos * inv_freq[i], &sn, &cs);
     const double x1 = src[head * hd + i], x2 = src[head * hd + i + half];
     const float y1 = (float)(x1 * cs - x2 * sn), y2 = (float)(x2 * cs + x1 * sn);
-    size_t o;
-    void* dst;
     if (head < H) {
-      o = ((size_t)r * H + head) * hd;
-      dst = Q;
+      const size_t o = ((size_t)r * H + head) * hd;
+      put_val<BF16>(Q, o + i, q_plane, y1);
+      put_val<BF16>(Q, o + i + half, q_plane, y2);
     } else {
-      o = (((size_t)s * Hkv + (head - H)) * maxpos + pos) * hd;
-      dst = Kc;
-    }
-    if constexpr (BF16) {
-      ((bf16_t*)dst)[o + i] = f2bf_m(y1);
-      ((bf16_t*)dst)[o + i + half] = f2bf_m(y2);
-    } else {
-      ((float*)dst)[o + i] = y1;
-      ((float*)dst)[o + i + half] = y2;
+      const size_t o = (((size_t)s * Hkv + (head - H)) * maxpos + pos) * hd;
+      put_val<BF16>(Kc, o + i, kv_plane, y1);
+      put_val<BF16>(Kc, o + i + half, kv_plane, y2);
     }
   }
   for (int idx = threadIdx.x; idx < Hkv * hd; idx += blockDim.x) {
     const int kh = idx / hd, e = idx % hd;
     const size_t o = (((size_t)s * Hkv + kh) * maxpos + pos) * hd + e;
-    const float v = src[(H + Hkv) * hd + idx];
-    if constexpr (BF16) ((bf16_t*)Vc)[o] = f2bf_m(v);
-    else ((float*)Vc)[o] = v;
+    put_val<BF16>(Vc, o, kv_plane, src[(H + Hkv) * hd + idx]);
   }
 }
 
 hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
-                          int Hkv, int hd, const double* inv_freq, void* Q, void* Kc, void* Vc,
-                          int maxpos, hipStream_t st) {
+                          int Hkv, int hd, const double* inv_freq, void* Q, size_t q_plane, void* Kc,
+                          void* Vc, size_t kv_plane, int maxpos, hipStream_t st) {
   if (is_bf16)
     k_rope_kv<true><<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd,
-                                              inv_freq, Q, Kc, Vc, maxpos);
+                                              inv_freq, Q, q_plane, Kc, Vc, kv_plane, maxpos);
   else
     k_rope_kv<false><<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd,
-                                               inv_freq, Q, Kc, Vc, maxpos);
+                                               inv_freq, Q, 0, Kc, Vc, 0, maxpos);
   return hipGetLastError();
 }
 

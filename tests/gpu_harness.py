@@ -31,7 +31,8 @@ class GpuTrace:
     forwards: np.ndarray             # [b]
 
 
-def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=None):
+def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=None, logit_steps=None,
+                      progress=None):
     import torch
     from paper_2609_33887_amd import bd
     st = bd.State(model, prompts, G, tau, nb, B)
@@ -46,7 +47,8 @@ def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=No
     for s in range(limit):
         conf.fill_(-1.0)
         tok.fill_(-1)
-        st.step(conf, tok, logits)
+        want_logits = logits is not None and (logit_steps is None or s < logit_steps)
+        st.step(conf, tok, logits if want_logits else None)
         done = st.commit(want_done=True)
         c = conf.cpu().numpy()
         t = tok.cpu().numpy()
@@ -55,10 +57,12 @@ def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=No
             pos = np.nonzero(c[i] >= 0)[0]
             if pos.size:
                 lg = None
-                if i in logits_for:
+                if want_logits and i in logits_for:
                     lg = logits[i, torch.as_tensor(pos, device=dev)].cpu().numpy()
                 rec[i] = (pos, c[i, pos], t[i, pos], lg)
         steps.append(rec)
+        if progress and s % 50 == 0:
+            progress(f"  gpu step {s}")
         if done:
             break
     tokens, cstep, fwd = st.read()
@@ -77,17 +81,23 @@ class Report:
     failures: list = field(default_factory=list)
 
 
-def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, conf_tol, logit_tol):
-    """Replay the chosen sequences in the oracle against ``trace``."""
+def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, conf_tol, logit_tol,
+             max_steps=None, progress=None):
+    """Replay the chosen sequences in the oracle against ``trace`` (the first
+    ``max_steps`` steps of each when given)."""
     from oracle.decode import SeqDecoder
     rep = Report()
     tau32 = float(np.float32(tau))
     for i in seq_ids:
         d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau)
+        if progress:
+            progress(f"  oracle prefill of sequence {i}")
         d.prefill()
         P = d.P
         step = 0
-        while not d.done:
+        while not d.done and (max_steps is None or step < max_steps):
+            if progress and step % 10 == 0:
+                progress(f"  oracle step {step} of sequence {i}")
             if step >= len(trace.steps) or i not in trace.steps[step]:
                 rep.failures.append((i, step, "GPU finished this sequence earlier than the oracle"))
                 break

@@ -60,11 +60,12 @@ def get_model(w):
     from paper_2609_33887_amd import bd
     key = (w.name, w.seed)
     if key not in _models:
-        _models[key] = (bd.Model(w, make_weights(w)), make_weights(w))
+        ws = make_weights(w)
+        _models[key] = (bd.Model(w, ws), ws)
     return _models[key]
 
 
-def run_parity(w, tau, seq_ids=None, logits=True, max_seqs=None):
+def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None):
     from oracle.model import OracleModel
     from tests.gpu_harness import capture_gpu_trace, lockstep
     _need_gpu()
@@ -74,9 +75,10 @@ def run_parity(w, tau, seq_ids=None, logits=True, max_seqs=None):
     prompts = make_prompts(w)
     ids = list(range(w.batch)) if seq_ids is None else list(seq_ids)
     tr = capture_gpu_trace(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size,
-                           logits_for=set(ids) if logits else ())
+                           logits_for=set(ids) if logits else (), logit_steps=logit_steps, progress=_say)
     om = OracleModel(w, ws, "f64" if w.dtype == "f32" else "bf16")
-    rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, w.n_inflight, w.block_size, *TOL[w.dtype])
+    rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, w.n_inflight, w.block_size, *TOL[w.dtype],
+                   max_steps=max_steps, progress=_say)
     ctol, ltol = TOL[w.dtype]
     _say(f"  positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} max|dlogit|={rep.max_logit_diff:.3g} "
          f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
@@ -118,6 +120,22 @@ def test_config1_dense_bf16_full_size(tau):
     sequences (sequences are independent, so the subset is exact)."""
     w = workload(1)
     run_parity(w, tau, seq_ids=[0, 11], logits=True)
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
+def test_config2_multiblock_full_size(tau):
+    """Full-size multi-block GQA model (24 layers, d 2048, 16/4 heads x 128,
+    vocab 152064, batch 32, prompts 1024, 3 blocks in flight, 1024 generated
+    tokens): the GPU decodes the whole batch; the oracle replays sequence 5
+    for its first 16 steps (logits compared on the first 3)."""
+    run_parity(workload(2), tau, seq_ids=[5], max_steps=16, logit_steps=3)
+
+
+def test_config3_long_prefix_full_size():
+    """Full-size long-prefix model (prompts of 8192 tokens encoded by the
+    prefill, block 64, 2 blocks in flight, batch 8) at tau 0.8: the oracle
+    encodes one 8192-token prompt and replays sequence 3 for 8 steps."""
+    run_parity(workload(3), 0.8, seq_ids=[3], max_steps=8, logit_steps=2)
 
 
 def test_decode_entry_point_matches_stepwise_and_is_deterministic():

@@ -200,8 +200,8 @@ def test_cached_step_equals_full_recompute(precision):
         full = m.forward(d.tokens, 0, e, fresh, B)[s:]
         cached = m.forward(d.tokens, s, e, d.cache, B)
         # bf16 mode: BLAS may accumulate the two row sets in different orders
-        # before Q/K/V are rounded, so agreement is at the rounding level there
-        tol = 1e-12 if precision == "f64" else 2e-3
+        # before the 16-bit operand roundings
+        tol = 1e-12 if precision == "f64" else 2e-4
         np.testing.assert_allclose(cached, full, atol=tol, rtol=0)
         checked += 1
         d.step(step)
