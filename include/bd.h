@@ -89,9 +89,12 @@ typedef struct bd_state bd_state;
  *  The caller keeps the weights alive until bd_model_free; the library may
  *  keep private repacked copies, which it frees.
  *  stream: a hipStream_t (NULL = default stream).
+ *  With n_shared == 0 the three shared-expert pointers may be NULL.
  *  Errors: BD_EINVAL for inconsistent dimensions (head_dim not 64 or 128,
  *  n_heads not a multiple of n_kv_heads, mask_id out of range, wrong
- *  n_weights), BD_ENOMEM, BD_EHIP.
+ *  n_weights, top_k outside [1, n_experts], n_experts > 64),
+ *  BD_EUNSUPPORTED (MoE with the f32 dtype; shapes off the GEMM tiles),
+ *  BD_ENOMEM, BD_EHIP.
  */
 bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev, int32_t n_weights,
                         void* stream, bd_model** out);
@@ -181,7 +184,7 @@ bd_status bd_state_stats(bd_model* model, bd_state* st, int64_t* out, int32_t n)
 enum {
     BD_PROF_EMBED = 0, BD_PROF_NORM = 1, BD_PROF_GEMM_QKV = 2, BD_PROF_ROPE = 3, BD_PROF_ATTN = 4,
     BD_PROF_GEMM_O = 5, BD_PROF_GEMM_GU = 6, BD_PROF_GEMM_DOWN = 7, BD_PROF_LM_HEAD = 8,
-    BD_PROF_COMMIT = 9, BD_PROF_KINDS = 10
+    BD_PROF_COMMIT = 9, BD_PROF_MOE = 10, BD_PROF_KINDS = 11
 };
 
 /*

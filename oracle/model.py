@@ -123,6 +123,7 @@ class OracleModel:
         # RoPE inverse frequencies theta^(-2i/hd) for the rotate-half pairs (i, i + hd/2).
         i = np.arange(self.hd // 2, dtype=np.float64)
         self.inv_freq = cfg.rope_theta ** (-2.0 * i / self.hd)
+        self.router_gaps = []
 
     # -- storage points ---------------------------------------------------
     def _store(self, x: np.ndarray) -> np.ndarray:
@@ -184,12 +185,17 @@ class OracleModel:
 
     def router(self, a: np.ndarray, L):
         """Top-k routing: softmax over all experts, k largest (lowest expert id
-        first among equals), weights renormalised to sum to one."""
+        first among equals), weights renormalised to sum to one.  The gap
+        between the k-th and (k+1)-th largest router logits of every row is
+        appended to ``self.router_gaps`` (used to recognise routing near-ties)."""
         logits = a @ L["w_router"].T
         probs = _softmax_rows(logits)
         k = self.cfg.top_k
         order = np.argsort(-probs, axis=-1, kind="stable")[:, :k]
         w = np.take_along_axis(probs, order, axis=-1)
+        if k < logits.shape[1]:
+            srt = -np.sort(-logits, axis=-1)
+            self.router_gaps.append(srt[:, k - 1] - srt[:, k])
         return order, w / np.sum(w, axis=-1, keepdims=True), logits
 
     def moe_ffn(self, a: np.ndarray, L) -> np.ndarray:

@@ -22,7 +22,7 @@ EXPORTED = ["bd_init_model", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_s
             "bd_decode", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
             "bd_profile_read", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select"]
 PROF_KINDS = ["embed", "norm", "gemm_qkv", "rope", "attn", "gemm_o", "gemm_gu", "gemm_down", "lm_head",
-              "commit"]
+              "commit", "moe_route"]
 
 
 class bd_model_cfg(ctypes.Structure):

@@ -45,8 +45,14 @@ struct LayerW {
   const void* w_qkv;
   const void* w_o;
   const float* ffn_norm;
-  void* w_gu;           // packed gate/up (library-owned)
+  void* w_gu;           // dense: packed gate/up (library-owned)
   const void* w_down;
+  // MoE
+  float* wr_t;          // router weights transposed [d][E] (library-owned)
+  void* w_gu_e;         // packed gate/up per expert [E][2 Fe][d] (library-owned)
+  const void* w_down_e; // [E][d][Fe]
+  void* w_gu_s;         // packed shared-expert gate/up [2 Fs][d] (library-owned)
+  const void* w_down_s; // [d][Fs]
 };
 
 struct bd_model {
@@ -130,6 +136,14 @@ struct bd_state {
   int attn_splits;
   float* attn_ws_o;
   float* attn_ws_ml;
+  // MoE buffers
+  int32_t* top_e;
+  float* top_w;
+  MoeLists moe;
+  int moe_tiles;
+  void* act_sorted;      // bf16 plane pair [assign_cap][Fe]
+  size_t pl_act;
+  float* y_sorted;       // fp32 [assign_cap][d]
   void* Kc;
   void* Vc;
   int steps;
@@ -166,19 +180,32 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
   if (c.n_heads % c.n_kv_heads) return fail(BD_EINVAL, "n_heads must be a multiple of n_kv_heads");
   if (c.mask_id < 0 || c.mask_id >= c.vocab) return fail(BD_EINVAL, "mask_id outside [0, vocab)");
   if (c.dtype != BD_F32 && c.dtype != BD_BF16) return fail(BD_EINVAL, "unknown dtype");
-  if (c.n_experts != 0) return fail(BD_EUNSUPPORTED, "MoE layers are not supported by this build");
-  if (c.ffn_dim < 16 || c.ffn_dim % 16) return fail(BD_EINVAL, "ffn_dim must be a positive multiple of 16");
-  const int per_layer = 7;
+  const bool moe = c.n_experts > 0;
+  const bool bf16 = c.dtype == BD_BF16;
+  const int Fs = moe ? c.n_shared * c.expert_ffn : 0;
+  if (moe) {
+    if (!bf16) return fail(BD_EUNSUPPORTED, "MoE layers need the bf16 dtype");
+    if (c.n_experts > 64 || c.top_k < 1 || c.top_k > c.n_experts || c.expert_ffn < 1 || c.n_shared < 0)
+      return fail(BD_EINVAL, "need 1 <= top_k <= n_experts <= 64, expert_ffn >= 1, n_shared >= 0");
+    if (c.expert_ffn % 64 || c.d_model % 128)
+      return fail(BD_EUNSUPPORTED, "expert_ffn must be a multiple of 64 and d_model of 128");
+  } else if (c.ffn_dim < 16 || c.ffn_dim % 16) {
+    return fail(BD_EINVAL, "ffn_dim must be a positive multiple of 16");
+  }
+  const int per_layer = moe ? 11 : 7;
   const int need = 1 + per_layer * c.n_layers + 2;
   if (n_weights != need) return fail(BD_EINVAL, "expected %d weight tensors, got %d", need, n_weights);
-  for (int i = 0; i < n_weights; ++i)
-    if (!w[i]) return fail(BD_EINVAL, "weight %d is NULL", i);
-  const bool bf16 = c.dtype == BD_BF16;
+  for (int i = 0; i < n_weights; ++i) {
+    const int li = (i - 1) % per_layer;
+    const bool shared_slot = moe && i >= 1 && i < 1 + per_layer * c.n_layers && li >= 8;
+    if (!w[i] && !(shared_slot && Fs == 0)) return fail(BD_EINVAL, "weight %d is NULL", i);
+  }
   // GEMM tiling constraints (bf16: N % 128, K % 64; f32: N % 64, K % 16)
   const int nq = bf16 ? 128 : 64, kq = bf16 ? 64 : 16;
   const int qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
-  if (qkv % nq || c.d_model % nq || c.vocab % nq || (2 * c.ffn_dim) % nq || c.d_model % kq ||
-      (c.n_heads * c.head_dim) % kq || c.ffn_dim % kq)
+  const int Fd = moe ? (Fs > 0 ? Fs : 64) : c.ffn_dim;    // width of the dense / shared FFN
+  if (qkv % nq || c.d_model % nq || c.vocab % nq || (2 * Fd) % nq || c.d_model % kq ||
+      (c.n_heads * c.head_dim) % kq || Fd % kq)
     return fail(BD_EUNSUPPORTED, "dimensions do not fit the GEMM tiles (N %% %d, K %% %d)", nq, kq);
 
   bd_model* m = new bd_model();
@@ -190,27 +217,61 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
   m->embed = w[t++];
   m->layers.resize(c.n_layers);
   const size_t row_bytes = (size_t)c.d_model * m->esz;
+  // library-owned repacked copies (gate/up interleaved for the SwiGLU epilogue)
+  auto owned_alloc = [&](size_t bytes) -> void* {
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return nullptr;
+    m->owned.push_back(p);
+    return p;
+  };
+  auto pack = [&](const void* gate, const void* up, int F, void** out) -> bd_status {
+    *out = owned_alloc(2 * (size_t)F * row_bytes);
+    if (!*out) return fail(BD_ENOMEM, "hipMalloc for packed gate/up failed");
+    hipError_t e = launch_pack_gate_up(gate, up, *out, F, row_bytes, m->stream);
+    if (e != hipSuccess) return fail(BD_EHIP, "pack gate/up: %s", hipGetErrorString(e));
+    return BD_OK;
+  };
   for (int l = 0; l < c.n_layers; ++l) {
     LayerW& L = m->layers[l];
+    L = LayerW{};
     L.attn_norm = (const float*)w[t++];
     L.w_qkv = w[t++];
     L.w_o = w[t++];
     L.ffn_norm = (const float*)w[t++];
-    const void* gate = w[t++];
-    const void* up = w[t++];
-    L.w_down = w[t++];
-    void* packed = nullptr;
-    hipError_t e = hipMalloc(&packed, 2 * (size_t)c.ffn_dim * row_bytes);
-    if (e != hipSuccess) {
-      bd_model_free(m);
-      return fail(BD_ENOMEM, "hipMalloc for packed gate/up failed");
+    bd_status r = BD_OK;
+    if (!moe) {
+      const void* gate = w[t++];
+      const void* up = w[t++];
+      L.w_down = w[t++];
+      r = pack(gate, up, c.ffn_dim, &L.w_gu);
+    } else {
+      const int E = c.n_experts, Fe = c.expert_ffn;
+      const float* router = (const float*)w[t++];
+      const char* gate_e = (const char*)w[t++];
+      const char* up_e = (const char*)w[t++];
+      L.w_down_e = w[t++];
+      const void* gate_s = w[t++];
+      const void* up_s = w[t++];
+      L.w_down_s = w[t++];
+      L.wr_t = (float*)owned_alloc((size_t)E * c.d_model * sizeof(float));
+      if (!L.wr_t) r = fail(BD_ENOMEM, "hipMalloc for the router failed");
+      else if (launch_transpose_f32(router, L.wr_t, E, c.d_model, m->stream) != hipSuccess)
+        r = fail(BD_EHIP, "router transpose failed");
+      if (r == BD_OK) {
+        L.w_gu_e = owned_alloc((size_t)E * 2 * Fe * row_bytes);
+        if (!L.w_gu_e) r = fail(BD_ENOMEM, "hipMalloc for packed experts failed");
+        for (int e = 0; e < E && r == BD_OK; ++e) {
+          const size_t off = (size_t)e * Fe * row_bytes;
+          if (launch_pack_gate_up(gate_e + off, up_e + off, (char*)L.w_gu_e + 2 * off, Fe, row_bytes,
+                                  m->stream) != hipSuccess)
+            r = fail(BD_EHIP, "pack expert gate/up failed");
+        }
+      }
+      if (r == BD_OK && Fs > 0) r = pack(gate_s, up_s, Fs, &L.w_gu_s);
     }
-    m->owned.push_back(packed);
-    L.w_gu = packed;
-    e = launch_pack_gate_up(gate, up, packed, c.ffn_dim, row_bytes, m->stream);
-    if (e != hipSuccess) {
+    if (r != BD_OK) {
       bd_model_free(m);
-      return fail(BD_EHIP, "pack gate/up: %s", hipGetErrorString(e));
+      return r;
     }
   }
   m->final_norm = (const float*)w[t++];
@@ -259,6 +320,47 @@ extern "C" bd_status bd_state_free(bd_state* s) {
 }
 
 // One forward over the rows of `plan`; with `lm` the masked rows get the LM head.
+// MoE FFN of one layer (rows of `plan`, operand already in s->A): shared
+// expert as a dense SwiGLU FFN added to the residual, router, deterministic
+// dispatch, grouped expert GEMMs into expert-sorted buffers, fixed-order
+// weighted combine into the residual.
+static bd_status run_moe(bd_model* m, bd_state* s, const LayerW& L, const PlanView& plan,
+                         int rows_cap) {
+  const bd_model_cfg& c = m->cfg;
+  const hipStream_t st = m->stream;
+  const int d = c.d_model, E = c.n_experts, k = c.top_k, Fe = c.expert_ffn;
+  const int Fs = c.n_shared * Fe;
+  if (Fs > 0) {
+    LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, true, s->A, d, s->pl_A, L.w_gu_s, d, 2 * Fs, d,
+                                        plan.hdr, rows_cap, s->Hact, Fs, s->pl_H, s->gemm_ws,
+                                        s->gemm_ws_floats, st));
+    LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, true, s->Hact, Fs, s->pl_H, L.w_down_s, Fs, d,
+                                          Fs, plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
+                                          s->gemm_ws_floats, st));
+  }
+  LAUNCH(BD_PROF_MOE, launch_router(s->A, s->pl_A, d, L.wr_t, E, k, plan.hdr, rows_cap, s->top_e,
+                                    s->top_w, st));
+  LAUNCH(BD_PROF_MOE, launch_moe_dispatch(s->top_e, k, E, plan.hdr, s->moe, st));
+  GroupTiles g;
+  g.tile_e = s->moe.tile_e;
+  g.tile_m0 = s->moe.tile_m0;
+  g.ntiles = s->moe.ntiles;
+  g.e_off = s->moe.e_off;
+  g.e_cnt = s->moe.e_cnt;
+  g.a_rows = s->moe.list_row;
+  g.w_stride = (size_t)2 * Fe * d;
+  LAUNCH(BD_PROF_GEMM_GU, launch_gemm_grouped(EPI_SWIGLU, s->A, d, s->pl_A, L.w_gu_e, d, 2 * Fe, d, g,
+                                              s->moe_tiles, s->act_sorted, Fe, s->pl_act, st));
+  g.a_rows = nullptr;
+  g.w_stride = (size_t)d * Fe;
+  LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm_grouped(EPI_STORE_F32, s->act_sorted, Fe, s->pl_act,
+                                                L.w_down_e, Fe, d, Fe, g, s->moe_tiles, s->y_sorted,
+                                                d, 0, st));
+  LAUNCH(BD_PROF_MOE, launch_moe_combine(s->X, s->y_sorted, s->moe.pos_of, s->top_w, k, d, plan.hdr,
+                                         rows_cap, st));
+  return BD_OK;
+}
+
 static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int rows_cap,
                              int win_cap, bool lm) {
   const bd_model_cfg& c = m->cfg;
@@ -294,12 +396,17 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
                                        s->gemm_ws_floats, st));
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
                                         rows_cap, s->A, s->pl_A, st));
-    LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, s->pl_A, L.w_gu, d, 2 * F, d,
-                                        plan.hdr, rows_cap, s->Hact, F, s->pl_H, s->gemm_ws,
-                                        s->gemm_ws_floats, st));
-    LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
-                                          plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
+    if (c.n_experts == 0) {
+      LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, s->pl_A, L.w_gu, d, 2 * F, d,
+                                          plan.hdr, rows_cap, s->Hact, F, s->pl_H, s->gemm_ws,
                                           s->gemm_ws_floats, st));
+      LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
+                                            plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
+                                            s->gemm_ws_floats, st));
+    } else {
+      bd_status r = run_moe(m, s, L, plan, rows_cap);
+      if (r != BD_OK) return r;
+    }
   }
   if (lm) {
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, m->final_norm, d, c.rms_eps, plan.hdr + 1,
@@ -371,13 +478,14 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   if (m->bf16) {
     s->pl_A = (size_t)s->rows_cap * d;
     s->pl_O = (size_t)s->rows_cap * H * hd;
-    s->pl_H = (size_t)s->rows_cap * c.ffn_dim;
+    s->pl_H = (size_t)s->rows_cap * (c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim);
     s->pl_lm = (size_t)s->lm_cap * d;
   }
   ALLOC(s->QKV, (size_t)s->rows_cap * qkv * 4);
   ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * 4);     // fp32, or a bf16 plane pair
   ALLOC(s->Ob, (size_t)s->rows_cap * H * hd * 4);
-  ALLOC(s->Hact, (size_t)s->rows_cap * c.ffn_dim * 4);
+  const int Fh = c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim;   // dense / shared FFN width
+  ALLOC(s->Hact, (size_t)s->rows_cap * (Fh > 0 ? Fh : 1) * 4);
   ALLOC(s->Alm, (size_t)s->lm_cap * d * 4);
   ALLOC(s->pmax, (size_t)ntiles * s->lm_cap * 4);
   ALLOC(s->psum, (size_t)ntiles * s->lm_cap * 4);
@@ -389,7 +497,8 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ALLOC(s->Vc, kv_bytes);
   {
     // split-K workspace: the largest need of the projections at either row capacity
-    const int shapes[4][2] = {{qkv, d}, {d, H * hd}, {2 * c.ffn_dim, d}, {d, c.ffn_dim}};
+    const int Ff = c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim;
+    const int shapes[4][2] = {{qkv, d}, {d, H * hd}, {2 * Ff, d}, {d, Ff}};
     size_t need = 0;
     for (int rc : {s->rows_step, s->rows_pre})
       for (auto& sh : shapes) {
@@ -399,6 +508,28 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
       }
     s->gemm_ws_floats = need;
     if (need) ALLOC(s->gemm_ws, need * sizeof(float));
+  }
+  if (c.n_experts > 0) {
+    const int E = c.n_experts, k = c.top_k, Fe = c.expert_ffn;
+    const size_t assign_cap = (size_t)s->rows_cap * k + GROUP_BM;   // + one tile of padding rows
+    s->moe_tiles = (int)((size_t)s->rows_cap * k / GROUP_BM) + E + 1;
+    ALLOC(s->top_e, (size_t)s->rows_cap * k * 4);
+    ALLOC(s->top_w, (size_t)s->rows_cap * k * 4);
+    ALLOC(s->moe.e_cnt, (size_t)E * 4);
+    ALLOC(s->moe.e_off, (size_t)E * 4);
+    ALLOC(s->moe.list_row, assign_cap * 4);
+    ALLOC(s->moe.pos_of, (size_t)s->rows_cap * k * 4);
+    ALLOC(s->moe.tile_e, (size_t)s->moe_tiles * 4);
+    ALLOC(s->moe.tile_m0, (size_t)s->moe_tiles * 4);
+    ALLOC(s->moe.ntiles, 16);
+    ALLOC(s->act_sorted, assign_cap * Fe * 4);
+    s->pl_act = assign_cap * Fe;
+    ALLOC(s->y_sorted, assign_cap * d * 4);
+    hipError_t e2 = hipMemsetAsync(s->act_sorted, 0, assign_cap * Fe * 4, m->stream);
+    if (e2 != hipSuccess) {
+      bd_state_free(s);
+      return fail(BD_EHIP, "hipMemsetAsync: %s", hipGetErrorString(e2));
+    }
   }
   s->attn_splits = m->bf16 ? attention_splits(b, s->win_step, H, s->maxpos) : 1;
   if (s->attn_splits > 1) {
@@ -415,7 +546,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   // past the live count never hold NaN patterns.
   hipError_t e = hipMemsetAsync(s->A, 0, (size_t)s->rows_cap * d * 4, m->stream);
   if (e == hipSuccess) e = hipMemsetAsync(s->Ob, 0, (size_t)s->rows_cap * H * hd * 4, m->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(s->Hact, 0, (size_t)s->rows_cap * c.ffn_dim * 4, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(s->Hact, 0, (size_t)s->rows_cap * (Fh > 0 ? Fh : 1) * 4, m->stream);
   if (e == hipSuccess) e = hipMemsetAsync(s->Alm, 0, (size_t)s->lm_cap * d * 4, m->stream);
   if (e != hipSuccess) {
     bd_state_free(s);

@@ -61,7 +61,9 @@ template <int BM, int BN>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int lda, size_t a_plane,
                                               const bf16_t* __restrict__ W, int ldw, int k0,
                                               int klen, int m0, int n0, MfmaTile<BM, BN>& t,
-                                              GemmSmem<BM, BN>& sm) {
+                                              GemmSmem<BM, BN>& sm,
+                                              const int32_t* __restrict__ arows = nullptr,
+                                              int nvalid = 0) {
   constexpr int FM = BM / 32, FN = BN / 32;
   constexpr int CPR = TBK / 8;          // 16-byte chunks per tile row
   constexpr int NA = BM * CPR / 256;    // u32x4 per thread and plane for the A tile
@@ -74,12 +76,20 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // source rows of this thread's A chunks: m0 + r, or a gathered row list
+  // (rows past nvalid repeat the first row; their results are discarded)
+  const bf16_t* aptr[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+    const int grow = arows ? arows[r < nvalid ? r : 0] : m0 + r;
+    aptr[i] = A + (size_t)grow * lda + kc;
+  }
 
   {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
-      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-      const bf16_t* src = A + (size_t)(m0 + r) * lda + k0 + kc;
+      const bf16_t* src = aptr[i] + k0;
       rah[i] = *(const u32x4*)(src);
       ral[i] = *(const u32x4*)(src + a_plane);
     }
@@ -111,8 +121,7 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
     if (kt + 1 < nk) {
 #pragma unroll
       for (int i = 0; i < NA; ++i) {
-        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-        const bf16_t* src = A + (size_t)(m0 + r) * lda + (k0 + (kt + 1) * TBK) + kc;
+        const bf16_t* src = aptr[i] + (k0 + (kt + 1) * TBK);
         rah[i] = *(const u32x4*)(src);
         ral[i] = *(const u32x4*)(src + a_plane);
       }
@@ -205,6 +214,69 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
       }
     }
   }
+}
+
+// Grouped GEMM over experts: tile ti covers rows [m0, m0 + 128) of expert
+// tile_e[ti]; the expert's rows sit at [e_off[e], e_off[e] + e_cnt[e]) of the
+// expert-sorted outputs.  The A rows are gathered through a_rows (token rows
+// of the expert-sorted assignments) or, with a_rows == NULL, read from the
+// expert-sorted layout itself.  W of expert e starts at W + e * w_stride.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__ A, int lda,
+                                                      size_t a_plane, const bf16_t* __restrict__ W,
+                                                      int ldw, int K, GroupTiles g,
+                                                      void* __restrict__ out, int ldo,
+                                                      size_t out_plane) {
+  constexpr int BM = 128, BN = 128, FM = BM / 32, FN = BN / 32;
+  const int ti = blockIdx.y;
+  if (ti >= *g.ntiles) return;
+  const int e = g.tile_e[ti], m0 = g.tile_m0[ti];
+  const int cnt = g.e_cnt[e], base = g.e_off[e];
+  const int n0 = blockIdx.x * BN;
+  __shared__ __attribute__((aligned(16))) GemmSmem<BM, BN> sm;
+  MfmaTile<BM, BN> t;
+  const bf16_t* We = W + (size_t)e * g.w_stride;
+  if (g.a_rows)
+    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, 0, n0, t, sm, g.a_rows + base + m0, cnt - m0);
+  else
+    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, base + m0, n0, t, sm);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ml = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
+      if (ml >= cnt) continue;
+      const size_t orow = (size_t)(base + ml);
+      if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int j = 0; j < FN; j += 2) {
+          const int pb = n0 + wn * (BN / 2) + j * 16;
+          const int col = (pb >> 5) * 16 + (lane & 15);
+          store_pair((bf16_t*)out + orow * ldo + col, out_plane, silu(t.acc[i][j][r]) * t.acc[i][j + 1][r]);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          ((float*)out)[orow * ldo + n0 + wn * (BN / 2) + j * 16 + (lane & 15)] = t.acc[i][j][r];
+      }
+    }
+  }
+}
+
+hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
+                               int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
+                               int ldo, size_t out_plane, hipStream_t st) {
+  if (N % 128 || K % TBK) return hipErrorInvalidValue;
+  dim3 grid(N / 128, max_tiles);
+  if (epi == EPI_SWIGLU)
+    k_gemm_grouped<EPI_SWIGLU><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W,
+                                                     ldw, K, g, out, ldo, out_plane);
+  else
+    k_gemm_grouped<EPI_STORE_F32><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane,
+                                                        (const bf16_t*)W, ldw, K, g, out, ldo, 0);
+  return hipGetLastError();
 }
 
 // Deterministic split-K reduction: sums the splits in order, then applies

@@ -74,6 +74,45 @@ enum { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
                        size_t out_plane, float* ws, size_t ws_floats, hipStream_t st);
+// Expert tiles of a grouped GEMM (all device pointers).
+struct GroupTiles {
+  const int32_t* tile_e;    // [max_tiles] expert of each tile
+  const int32_t* tile_m0;   // [max_tiles] first expert-local row of each tile
+  const int32_t* ntiles;    // [1] live tile count
+  const int32_t* e_off;     // [E] first expert-sorted row of each expert
+  const int32_t* e_cnt;     // [E] rows of each expert
+  const int32_t* a_rows;    // optional [assignments] token row of each sorted row
+  size_t w_stride;          // elements between consecutive experts' weights
+};
+constexpr int GROUP_BM = 128;
+// out rows are expert-sorted rows; EPI_SWIGLU writes bf16 planes, EPI_STORE_F32 fp32.
+hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
+                               int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
+                               int ldo, size_t out_plane, hipStream_t st);
+
+// MoE routing: softmax over E router logits (fp32 weights, transposed
+// [d][E]), top_k experts (lowest id among equals), weights renormalised.
+hipError_t launch_router(const void* A, size_t a_plane, int d, const float* WrT, int E, int topk,
+                         const int32_t* M_dev, int rows_cap, int32_t* top_e, float* top_w,
+                         hipStream_t st);
+// Deterministic dispatch: expert-sorted assignment lists (token rows ascending
+// within each expert), positions of every (row, slot), and the tile list.
+struct MoeLists {
+  int32_t* e_cnt;    // [E]
+  int32_t* e_off;    // [E]
+  int32_t* list_row; // [rows_cap * topk]
+  int32_t* pos_of;   // [rows_cap * topk]
+  int32_t* tile_e;   // [max_tiles]
+  int32_t* tile_m0;  // [max_tiles]
+  int32_t* ntiles;   // [1]
+};
+hipError_t launch_moe_dispatch(const int32_t* top_e, int topk, int E, const int32_t* M_dev,
+                               const MoeLists& L, hipStream_t st);
+// X[row] += sum_j top_w[row][j] * Y[pos_of[row][j]] (fixed slot order).
+hipError_t launch_moe_combine(float* X, const float* Y, const int32_t* pos_of, const float* top_w,
+                              int topk, int d, const int32_t* M_dev, int rows_cap, hipStream_t st);
+hipError_t launch_transpose_f32(const float* in, float* out, int rows, int cols, hipStream_t st);
+
 struct GemmPlan {
   int bm, bn, splits;
 };

@@ -48,6 +48,10 @@ SMALL = {
                      prompt_len=8, block_size=8, n_inflight=2, gen_len=48),
     "block1": small("block1", seed=93, batch=2, prompt_len=5, block_size=1, n_inflight=1, gen_len=12,
                     dtype="f32"),
+    # MoE: 8 experts, top-2, expert FFN 128, one shared expert
+    "moe": small("moe", seed=96, n_heads=4, n_kv_heads=2, head_dim=128, ffn_dim=0, n_experts=8, top_k=2,
+                 expert_ffn=128, n_shared=1, batch=3, prompt_len=64, block_size=16, n_inflight=2,
+                 gen_len=64),
     # long prefix: the attention key range is split over several workgroups
     "longprefix": small("longprefix", seed=94, n_heads=4, n_kv_heads=2, head_dim=128, batch=2,
                         prompt_len=2048, block_size=32, n_inflight=2, gen_len=64),
@@ -81,7 +85,7 @@ def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=No
                    max_steps=max_steps, progress=_say)
     ctol, ltol = TOL[w.dtype]
     _say(f"  positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} max|dlogit|={rep.max_logit_diff:.3g} "
-         f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
+         f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} T4(steps)={rep.t4} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
     assert not rep.failures, rep.failures[:5]
     assert rep.max_conf_diff <= ctol
     assert rep.max_logit_diff <= ltol
@@ -136,6 +140,14 @@ def test_config3_long_prefix_full_size():
     prefill, block 64, 2 blocks in flight, batch 8) at tau 0.8: the oracle
     encodes one 8192-token prompt and replays sequence 3 for 8 steps."""
     run_parity(workload(3), 0.8, seq_ids=[3], max_steps=8, logit_steps=2)
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
+def test_config4_moe_full_size(tau):
+    """Full-size MoE model (20 layers, d 2048, 64 experts top-8 with FFN 512
+    plus a shared expert, vocab 152064, batch 64, prompts 256, 128 generated
+    tokens); the oracle replays sequence 17 for 12 steps."""
+    run_parity(workload(4), tau, seq_ids=[17], max_steps=12, logit_steps=2)
 
 
 def test_decode_entry_point_matches_stepwise_and_is_deterministic():
