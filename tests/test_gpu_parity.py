@@ -219,3 +219,28 @@ def test_error_paths():
         st.commit(want_done=True)
     assert e.value.status == bd.BD_EINVAL
     st.close()
+
+
+def test_config4_redline_sweep_matches_oracle():
+    """Redline on the GPU-decoded MoE sweep: 12 candidates (tau x in-flight
+    blocks) plus the reference (tau > 1, one block) on one batch of 64
+    calibration prompts; correctness = the final 16 tokens equal the
+    reference's.  Violation counts, valid set and selection of the C
+    implementation equal the oracle's on the same matrix, bit for bit."""
+    from paper_2609_33887_amd.sweep import redline_sweep
+    from oracle import redline as orl
+    _need_gpu()
+    w = workload(4)
+    model, _ = get_model(w)
+    prompts = make_prompts(w, 64)
+    cands = [(t, nb) for t in (0.95, 0.9, 0.8, 0.7) for nb in (1, 2, 3)]
+    r = redline_sweep(model, prompts, w.gen_len, w.block_size, cands, (2.0, 1), 0.10, 0.05, batch=64,
+                      progress=_say)
+    assert r["tpf"][0] == 1.0                      # tau > 1: one token per forward
+    o = orl.risk_select(r["correct"], r["tpf"], 0, 0.10, 0.05)
+    assert r["V"].tolist() == o.V.tolist()
+    assert r["valid"].tolist() == o.valid.tolist()
+    assert r["selected"] == o.selected
+    for a, b in zip(r["p"], o.p):
+        assert abs(a - float(b)) <= 1e-11 * float(b) + 1e-300
+    _say(f"  TPF {['%.3f' % t for t in r['tpf']]} V {r['V'].tolist()} selected {r['grid'][r['selected']]}")
