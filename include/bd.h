@@ -93,7 +93,9 @@ typedef struct bd_state bd_state;
  *  Errors: BD_EINVAL for inconsistent dimensions (head_dim not 64 or 128,
  *  n_heads not a multiple of n_kv_heads, mask_id out of range, wrong
  *  n_weights, top_k outside [1, n_experts], n_experts > 64),
- *  BD_EUNSUPPORTED (MoE with the f32 dtype; shapes off the GEMM tiles),
+ *  BD_EUNSUPPORTED (MoE with the f32 dtype; shapes off the GEMM tiles: with
+ *  bf16 every projection's output and input widths -- (H + 2 Hkv) hd, d,
+ *  H hd, vocab, 2 ffn or 2 Fe, ffn or Fe -- must be multiples of 128),
  *  BD_ENOMEM, BD_EHIP.
  */
 bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev, int32_t n_weights,

@@ -123,14 +123,13 @@ struct bd_state {
   void* Qb;
   void* Ob;
   void* Hact;
+  float* resid_ws;         // residual split-K partials (RESID_WS_FLOATS, bf16 models)
   void* Alm;
   float *pmax, *psum;
   int32_t* parg;
   float* conf;
   int32_t* tok;
   float* logits_tmp;
-  float* gemm_ws;
-  size_t gemm_ws_floats;
   // bf16 models: plane offsets (elements) of the lo halves of A, Ob, Hact, Alm
   size_t pl_A, pl_O, pl_H, pl_lm;
   int attn_splits;
@@ -187,8 +186,8 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
     if (!bf16) return fail(BD_EUNSUPPORTED, "MoE layers need the bf16 dtype");
     if (c.n_experts > 64 || c.top_k < 1 || c.top_k > c.n_experts || c.expert_ffn < 1 || c.n_shared < 0)
       return fail(BD_EINVAL, "need 1 <= top_k <= n_experts <= 64, expert_ffn >= 1, n_shared >= 0");
-    if (c.expert_ffn % 64 || c.d_model % 128)
-      return fail(BD_EUNSUPPORTED, "expert_ffn must be a multiple of 64 and d_model of 128");
+    if (c.expert_ffn % 128 || c.d_model % 128)
+      return fail(BD_EUNSUPPORTED, "expert_ffn and d_model must be multiples of 128");
   } else if (c.ffn_dim < 16 || c.ffn_dim % 16) {
     return fail(BD_EINVAL, "ffn_dim must be a positive multiple of 16");
   }
@@ -200,10 +199,10 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
     const bool shared_slot = moe && i >= 1 && i < 1 + per_layer * c.n_layers && li >= 8;
     if (!w[i] && !(shared_slot && Fs == 0)) return fail(BD_EINVAL, "weight %d is NULL", i);
   }
-  // GEMM tiling constraints (bf16: N % 128, K % 64; f32: N % 64, K % 16)
-  const int nq = bf16 ? 128 : 64, kq = bf16 ? 64 : 16;
+  // GEMM tiling constraints (bf16: N % 128, K % 128; f32: N % 64, K % 16)
+  const int nq = bf16 ? 128 : 64, kq = bf16 ? 128 : 16;
   const int qkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
-  const int Fd = moe ? (Fs > 0 ? Fs : 64) : c.ffn_dim;    // width of the dense / shared FFN
+  const int Fd = moe ? (Fs > 0 ? Fs : 128) : c.ffn_dim;    // width of the dense / shared FFN
   if (qkv % nq || c.d_model % nq || c.vocab % nq || (2 * Fd) % nq || c.d_model % kq ||
       (c.n_heads * c.head_dim) % kq || Fd % kq)
     return fail(BD_EUNSUPPORTED, "dimensions do not fit the GEMM tiles (N %% %d, K %% %d)", nq, kq);
@@ -332,11 +331,9 @@ static bd_status run_moe(bd_model* m, bd_state* s, const LayerW& L, const PlanVi
   const int Fs = c.n_shared * Fe;
   if (Fs > 0) {
     LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, true, s->A, d, s->pl_A, L.w_gu_s, d, 2 * Fs, d,
-                                        plan.hdr, rows_cap, s->Hact, Fs, s->pl_H, s->gemm_ws,
-                                        s->gemm_ws_floats, st));
+                                        plan.hdr, rows_cap, s->Hact, Fs, s->pl_H, st));
     LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, true, s->Hact, Fs, s->pl_H, L.w_down_s, Fs, d,
-                                          Fs, plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
-                                          s->gemm_ws_floats, st));
+                                          Fs, plan.hdr, rows_cap, s->X, d, 0, st));
   }
   LAUNCH(BD_PROF_MOE, launch_router(s->A, s->pl_A, d, L.wr_t, E, k, plan.hdr, rows_cap, s->top_e,
                                     s->top_w, st));
@@ -376,33 +373,33 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
   const int kv_splits = (bf && lm) ? s->attn_splits : 1;
   LAUNCH(BD_PROF_EMBED, launch_embed(bf, s->tokens, s->P + s->G, m->embed, d, c.vocab, plan,
                                      rows_cap, s->X, m->err_flag, st));
+  ResidSplit pend{};     // residual split partials not yet folded into X
   for (int l = 0; l < c.n_layers; ++l) {
     const LayerW& L = m->layers[l];
     void* Kl = (char*)s->Kc + l * layer_kv;
     void* Vl = (char*)s->Vc + l * layer_kv;
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.attn_norm, d, c.rms_eps, plan.hdr, nullptr,
-                                        rows_cap, s->A, s->pl_A, st));
+                                        rows_cap, s->A, s->pl_A, pend, st));
+    pend.ws = nullptr;
     LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, s->pl_A, L.w_qkv, d, qkv, d,
-                                         plan.hdr, rows_cap, s->QKV, qkv, 0, s->gemm_ws,
-                                         s->gemm_ws_floats, st));
+                                         plan.hdr, rows_cap, s->QKV, qkv, 0, st));
     LAUNCH(BD_PROF_ROPE, launch_rope_kv(bf, s->QKV, plan, rows_cap, H, Hkv, hd, m->inv_freq, s->Qb,
                                         q_plane, Kl, Vl, kv_plane, s->maxpos, st));
     LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, q_plane, Kl, Vl, kv_plane, s->Ob, s->pl_O, plan,
                                           s->b, win_cap, H, Hkv, hd,
                                           s->maxpos, s->B, kv_splits, s->attn_ws_o, s->attn_ws_ml,
                                           rows_cap, st));
-    LAUNCH(BD_PROF_GEMM_O, launch_gemm(EPI_ADD_F32, bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d,
-                                       H * hd, plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
-                                       s->gemm_ws_floats, st));
+    LAUNCH(BD_PROF_GEMM_O, launch_gemm_resid(bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d, H * hd,
+                                             plan.hdr, rows_cap, s->X, d, s->resid_ws, &pend, st));
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
-                                        rows_cap, s->A, s->pl_A, st));
+                                        rows_cap, s->A, s->pl_A, pend, st));
+    pend.ws = nullptr;
     if (c.n_experts == 0) {
       LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, s->pl_A, L.w_gu, d, 2 * F, d,
-                                          plan.hdr, rows_cap, s->Hact, F, s->pl_H, s->gemm_ws,
-                                          s->gemm_ws_floats, st));
-      LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
-                                            plan.hdr, rows_cap, s->X, d, 0, s->gemm_ws,
-                                            s->gemm_ws_floats, st));
+                                          plan.hdr, rows_cap, s->Hact, F, s->pl_H, st));
+      LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm_resid(bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
+                                                  plan.hdr, rows_cap, s->X, d, s->resid_ws, &pend,
+                                                  st));
     } else {
       bd_status r = run_moe(m, s, L, plan, rows_cap);
       if (r != BD_OK) return r;
@@ -410,7 +407,7 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
   }
   if (lm) {
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, m->final_norm, d, c.rms_eps, plan.hdr + 1,
-                                        plan.lm_row, s->lm_cap, s->Alm, s->pl_lm, st));
+                                        plan.lm_row, s->lm_cap, s->Alm, s->pl_lm, pend, st));
     LAUNCH(BD_PROF_LM_HEAD, launch_lm_head(bf, s->Alm, d, s->pl_lm, m->lm_head, c.vocab, c.mask_id,
                                            c.logit_scale, plan.hdr + 1, s->lm_cap, s->pmax, s->psum,
                                            s->parg, s->conf, s->tok, st));
@@ -495,20 +492,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   const size_t kv_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * 4;   // fp32 or 2 bf16 planes
   ALLOC(s->Kc, kv_bytes);
   ALLOC(s->Vc, kv_bytes);
-  {
-    // split-K workspace: the largest need of the projections at either row capacity
-    const int Ff = c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim;
-    const int shapes[4][2] = {{qkv, d}, {d, H * hd}, {2 * Ff, d}, {d, Ff}};
-    size_t need = 0;
-    for (int rc : {s->rows_step, s->rows_pre})
-      for (auto& sh : shapes) {
-        const GemmPlan gp = plan_gemm(m->bf16, sh[0], sh[1], rc);
-        const size_t f = gemm_workspace_floats(gp, sh[0], rc);
-        if (f > need) need = f;
-      }
-    s->gemm_ws_floats = need;
-    if (need) ALLOC(s->gemm_ws, need * sizeof(float));
-  }
+  if (m->bf16) ALLOC(s->resid_ws, RESID_WS_FLOATS * sizeof(float));
   if (c.n_experts > 0) {
     const int E = c.n_experts, k = c.top_k, Fe = c.expert_ffn;
     const size_t assign_cap = (size_t)s->rows_cap * k + GROUP_BM;   // + one tile of padding rows

@@ -3,11 +3,12 @@
 // All products are C = A . W^T with A [rows][K] (activations, row-major) and
 // W [N][K] (weights stored [out][in]), so both operands are K-contiguous.
 //
-// bf16 path (bf16 weights, activations as bf16 hi/lo plane pairs): 128x128,
-// 64x128 or 64x64 workgroup tiles with K-steps of 64, 4 wave64s in a 2x2
-// arrangement, MFMA 16x16x32 bf16 with fp32 accumulate.  Operands are staged
-// through LDS (double-buffered, padded row stride) with 16-byte global loads;
-// one barrier per K-step; optional deterministic split-K.
+// bf16 path (bf16 weights, activations as bf16 hi/lo plane pairs): 128x128
+// or 64x64 workgroup tiles, 4 wave64s in a 2x2 arrangement, MFMA 16x16x32
+// bf16 with fp32 accumulate.  Operands reach LDS through direct
+// global-to-LDS loads into a four-stage ring (K-stages of 32, swizzled rows);
+// one barrier per stage; the residual projections may split K (the partial
+// sums are folded in by the next RMSNorm).
 // f32 path (small fp32 models): 64x64x16 SIMT tiles.
 //
 // The row count M is read from device memory so that a launch sized for the
@@ -40,162 +41,200 @@ __device__ __forceinline__ void store_pair(bf16_t* p, size_t plane, float x) {
 // accumulated as hi.W + lo.W, two MFMAs per weight fragment, which gives the
 // operand 16 significant bits, so that the only activation roundings of the
 // forward are the Q/K/V values stored in the KV cache.
-constexpr int TBK = 64, LDSK = TBK + 8;
+//
+// Main loop: K advances in stages of SK = 32 through a ring of four LDS
+// stages filled by direct global-to-LDS 16-byte loads (no register staging,
+// no LDS store instructions); three stages are in flight while the fourth is
+// consumed, and one barrier per stage both publishes the stage and retires
+// the one the next loads overwrite.  A wave's load instruction writes 1 KiB of
+// LDS = 16 rows x 64 B, lane l at byte 16 l; in LDS the 16-byte chunk c of row r
+// sits at position c ^ ((r >> 2) & 3), so that the 16 rows a quarter-wave
+// reads for one MFMA fragment fall on distinct bank groups.
+constexpr int SK = 32;       // K per pipeline stage (KALIGN = 4 stages)
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int BM, int BN>
+struct GemmStage {
+  bf16_t ah[BM * SK];
+  bf16_t al[BM * SK];
+  bf16_t b[BN * SK];
+};
 
 template <int BM, int BN>
 struct MfmaTile {
   floatx4 acc[BM / 32][BN / 32];
 };
 
+// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Per-thread source pointers of one tile's loads: A rows (hi plane; lo at
+// + a_plane) and W rows, each already offset to this lane's 16-byte chunk.
 template <int BM, int BN>
-struct GemmSmem {
-  bf16_t ah[2][BM * LDSK];
-  bf16_t al[2][BM * LDSK];
-  bf16_t b[2][BN * LDSK];
+struct TileSrc {
+  const bf16_t* a[BM / 64];
+  const bf16_t* w[BN / 64];
 };
 
-// Main loop over K range [k0, k0 + klen): 4 waves in a 2x2 arrangement, each
-// accumulating a (BM/2)x(BN/2) sub-tile of (BM/32)x(BN/32) MFMA tiles.  The
-// activation operand comes as two bf16 planes (hi at A, lo at A + a_plane).
+template <int BM, int BN>
+__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN>& src, size_t a_plane, int k,
+                                            GemmStage<BM, BN>& s, int wave) {
+#pragma unroll
+  for (int i = 0; i < BM / 64; ++i) {
+    const int r = (i * 4 + wave) * 16;
+    __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k), (lds_void_t*)(s.ah + r * SK), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k + a_plane), (lds_void_t*)(s.al + r * SK), 16, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < BN / 64; ++i) {
+    const int r = (i * 4 + wave) * 16;
+    __builtin_amdgcn_global_load_lds((const void*)(src.w[i] + k), (lds_void_t*)(s.b + r * SK), 16, 0, 0);
+  }
+}
+
+// One stage of MFMAs: 4 waves in a 2x2 arrangement, each accumulating a
+// (BM/2)x(BN/2) sub-tile of (BM/32)x(BN/32) MFMA 16x16x32 tiles.
+template <int BM, int BN>
+__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN>& s, MfmaTile<BM, BN>& t, int wave) {
+  constexpr int FM = BM / 32, FN = BN / 32;
+  const int lane = threadIdx.x & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r16 = lane & 15;
+  const int pos = ((lane >> 4) ^ ((r16 >> 2) & 3)) * 8;   // fragment rows are r16 + 16 j
+  u32x4 bfr[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&s.b[(wn * (BN / 2) + j * 16 + r16) * SK + pos]);
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int row = wm * (BM / 2) + i * 16 + r16;
+    const bf16x8 ah = __builtin_bit_cast(bf16x8, *(const u32x4*)(&s.ah[row * SK + pos]));
+    const bf16x8 al = __builtin_bit_cast(bf16x8, *(const u32x4*)(&s.al[row * SK + pos]));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const bf16x8 bj = __builtin_bit_cast(bf16x8, bfr[j]);
+      t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bj, t.acc[i][j], 0, 0, 0);
+      t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bj, t.acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// Main loop of one group of 4 waves (wave = 0..3 within the group) over the
+// K range [k0, k0 + klen), klen a positive multiple of KALIGN.  The A rows
+// are m0 + r, or gathered through arows (rows past nvalid repeat the first
+// listed row; their results are discarded by the caller).  The four stages
+// are separate LDS objects so the compiler can tell the loads into one stage
+// from the reads of another.  All waves of the workgroup must run the same
+// number of stages (the barriers are workgroup-wide).
 template <int BM, int BN>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int lda, size_t a_plane,
                                               const bf16_t* __restrict__ W, int ldw, int k0,
                                               int klen, int m0, int n0, MfmaTile<BM, BN>& t,
-                                              GemmSmem<BM, BN>& sm,
-                                              const int32_t* __restrict__ arows = nullptr,
+                                              GemmStage<BM, BN>& s0, GemmStage<BM, BN>& s1,
+                                              GemmStage<BM, BN>& s2, GemmStage<BM, BN>& s3,
+                                              int wave, const int32_t* __restrict__ arows = nullptr,
                                               int nvalid = 0) {
-  constexpr int FM = BM / 32, FN = BN / 32;
-  constexpr int CPR = TBK / 8;          // 16-byte chunks per tile row
-  constexpr int NA = BM * CPR / 256;    // u32x4 per thread and plane for the A tile
-  constexpr int NB = BN * CPR / 256;    // u32x4 per thread for the W tile
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  u32x4 rah[NA], ral[NA];
-  u32x4 rb[NB];
+  constexpr int LPS = 2 * (BM / 64) + BN / 64;   // load instructions per thread per stage
+  const int lane = threadIdx.x & 63;
+  const int rsub = lane >> 2, chunk = (lane & 3) ^ ((rsub >> 2) & 3);
+  TileSrc<BM, BN> src;
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  // source rows of this thread's A chunks: m0 + r, or a gathered row list
-  // (rows past nvalid repeat the first row; their results are discarded)
-  const bf16_t* aptr[NA];
-#pragma unroll
-  for (int i = 0; i < NA; ++i) {
-    const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
+  for (int i = 0; i < BM / 64; ++i) {
+    const int r = (i * 4 + wave) * 16 + rsub;
     const int grow = arows ? arows[r < nvalid ? r : 0] : m0 + r;
-    aptr[i] = A + (size_t)grow * lda + kc;
+    src.a[i] = A + (size_t)grow * lda + k0 + chunk * 8;
   }
+#pragma unroll
+  for (int i = 0; i < BN / 64; ++i)
+    src.w[i] = W + (size_t)(n0 + (i * 4 + wave) * 16 + rsub) * ldw + k0 + chunk * 8;
+#pragma unroll
+  for (int i = 0; i < BM / 32; ++i)
+#pragma unroll
+    for (int j = 0; j < BN / 32; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  {
-#pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const bf16_t* src = aptr[i] + k0;
-      rah[i] = *(const u32x4*)(src);
-      ral[i] = *(const u32x4*)(src + a_plane);
-    }
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-      rb[i] = *(const u32x4*)(W + (size_t)(n0 + r) * ldw + k0 + kc);
-    }
+  const int nk = klen / SK;     // multiple of 4, >= 4
+  stage_issue<BM, BN>(src, a_plane, 0, s0, wave);
+  stage_issue<BM, BN>(src, a_plane, SK, s1, wave);
+  stage_issue<BM, BN>(src, a_plane, 2 * SK, s2, wave);
+  int kt = 0;
+  // each step: own loads of stage kt done (the two younger stages may still
+  // be in flight), barrier (everyone's loads done, everyone past stage kt-1),
+  // refill the stage of kt-1 with kt+3, compute stage kt
+#define BD_GEMM_STEP(CUR, NXT, KNEXT)                            \
+  wait_vmcnt<2 * LPS>();                                         \
+  __builtin_amdgcn_s_barrier();                                  \
+  stage_issue<BM, BN>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
+  stage_mfma<BM, BN>(CUR, t, wave);
+  for (; kt + 4 < nk; kt += 4) {
+    BD_GEMM_STEP(s0, s3, kt + 3)
+    BD_GEMM_STEP(s1, s0, kt + 4)
+    BD_GEMM_STEP(s2, s1, kt + 5)
+    BD_GEMM_STEP(s3, s2, kt + 6)
   }
-  {
-#pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-      *(u32x4*)(&sm.ah[0][r * LDSK + kc]) = rah[i];
-      *(u32x4*)(&sm.al[0][r * LDSK + kc]) = ral[i];
-    }
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-      *(u32x4*)(&sm.b[0][r * LDSK + kc]) = rb[i];
-    }
-  }
-  __syncthreads();
-  const int nk = klen / TBK;
-  const int arow = wm * (BM / 2) + (lane & 15), brow = wn * (BN / 2) + (lane & 15);
-  const int koff = (lane >> 4) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) {
-#pragma unroll
-      for (int i = 0; i < NA; ++i) {
-        const bf16_t* src = aptr[i] + (k0 + (kt + 1) * TBK);
-        rah[i] = *(const u32x4*)(src);
-        ral[i] = *(const u32x4*)(src + a_plane);
-      }
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-        rb[i] = *(const u32x4*)(W + (size_t)(n0 + r) * ldw + (k0 + (kt + 1) * TBK) + kc);
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < TBK; kk += 32) {
-      u32x4 bfr[FN];
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&sm.b[buf][(brow + j * 16) * LDSK + kk + koff]);
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const bf16x8 ah = __builtin_bit_cast(bf16x8, *(const u32x4*)(&sm.ah[buf][(arow + i * 16) * LDSK + kk + koff]));
-        const bf16x8 al = __builtin_bit_cast(bf16x8, *(const u32x4*)(&sm.al[buf][(arow + i * 16) * LDSK + kk + koff]));
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const bf16x8 bj = __builtin_bit_cast(bf16x8, bfr[j]);
-          t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bj, t.acc[i][j], 0, 0, 0);
-          t.acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bj, t.acc[i][j], 0, 0, 0);
-        }
-      }
-    }
-    if (kt + 1 < nk) {
-#pragma unroll
-      for (int i = 0; i < NA; ++i) {
-        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-        *(u32x4*)(&sm.ah[buf ^ 1][r * LDSK + kc]) = rah[i];
-        *(u32x4*)(&sm.al[buf ^ 1][r * LDSK + kc]) = ral[i];
-      }
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        const int c = tid + 256 * i, r = c / CPR, kc = (c % CPR) * 8;
-        *(u32x4*)(&sm.b[buf ^ 1][r * LDSK + kc]) = rb[i];
-      }
-    }
-    __syncthreads();
-  }
+#undef BD_GEMM_STEP
+  // the last four stages (kt + 3 == nk - 1)
+  wait_vmcnt<2 * LPS>();
+  __builtin_amdgcn_s_barrier();
+  stage_issue<BM, BN>(src, a_plane, (kt + 3) * SK, s3, wave);
+  stage_mfma<BM, BN>(s0, t, wave);
+  wait_vmcnt<2 * LPS>();
+  __builtin_amdgcn_s_barrier();
+  stage_mfma<BM, BN>(s1, t, wave);
+  wait_vmcnt<LPS>();
+  __builtin_amdgcn_s_barrier();
+  stage_mfma<BM, BN>(s2, t, wave);
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  stage_mfma<BM, BN>(s3, t, wave);
 }
 
-// Epilogue modes; with split-K (gridDim.z > 1) every split writes its raw
-// partial tile to ws[split][row][col] and k_splitk_reduce applies the mode.
+#define BD_GEMM_SMEM(BM, BN)                                                     \
+  __shared__ __attribute__((aligned(1024))) GemmStage<BM, BN> gs0, gs1, gs2, gs3
+
+// GEMM, epilogue applied in registers.  For EPI_ADD_F32 with a split
+// workspace, the kernel picks S = resid_splits(M) K-splits on the device
+// (gridDim.z is the largest allowed); with S > 1 every split stores its raw
+// partial tile to ws[split][row][col] (rows padded to whole tiles) and the
+// next RMSNorm of the residual stream adds the partials in split order.
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
                                                    size_t a_plane, const bf16_t* __restrict__ W,
                                                    int ldw, int N, int K,
                                                    const int32_t* __restrict__ Mp,
                                                    void* __restrict__ out, int ldo, size_t out_plane,
-                                                   float* __restrict__ ws, int rows_cap) {
+                                                   float* __restrict__ ws) {
   constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
   const int m0 = blockIdx.y * BM;
   if (m0 >= M) return;
+  int S = 1;
+  if (EPI == EPI_ADD_F32 && ws) {
+    ResidSplit r;
+    r.nx = gridDim.x; r.bm = BM; r.K = K; r.zmax = gridDim.z;
+    S = resid_splits(M, r);
+  }
+  if ((int)blockIdx.z >= S) return;
+  const int klen = K / S;
   const int n0 = blockIdx.x * BN;
-  const int splits = gridDim.z, klen = K / splits, k0 = blockIdx.z * klen;
-  __shared__ __attribute__((aligned(16))) GemmSmem<BM, BN> sm;
-  MfmaTile<BM, BN> t;
-  mfma_mainloop<BM, BN>(A, lda, a_plane, W, ldw, k0, klen, m0, n0, t, sm);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  BD_GEMM_SMEM(BM, BN);
+  MfmaTile<BM, BN> t;
+  mfma_mainloop<BM, BN>(A, lda, a_plane, W, ldw, blockIdx.z * klen, klen, m0, n0, t, gs0, gs1, gs2,
+                        gs3, wave);
   const int wm = wave >> 1, wn = wave & 1;
+  float* wz = (EPI == EPI_ADD_F32 && S > 1) ? ws + (size_t)blockIdx.z * ((M + BM - 1) / BM) * BM * N
+                                            : nullptr;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4 + r;
       if (m >= M) continue;
-      if (splits > 1) {
-        float* wrow = ws + ((size_t)blockIdx.z * rows_cap + m) * N;
-#pragma unroll
-        for (int j = 0; j < FN; ++j) wrow[n0 + wn * (BN / 2) + j * 16 + (lane & 15)] = t.acc[i][j][r];
-      } else if constexpr (EPI == EPI_SWIGLU) {
+      if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll
         for (int j = 0; j < FN; j += 2) {
           const int pb = n0 + wn * (BN / 2) + j * 16;    // packed column of the gate group
@@ -208,7 +247,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
         for (int j = 0; j < FN; ++j) {
           const int n = n0 + wn * (BN / 2) + j * 16 + (lane & 15);
           const float v = t.acc[i][j][r];
-          if constexpr (EPI == EPI_ADD_F32) ((float*)out)[(size_t)m * ldo + n] += v;
+          if (EPI == EPI_ADD_F32 && S > 1) wz[(size_t)m * N + n] = v;
+          else if (EPI == EPI_ADD_F32) ((float*)out)[(size_t)m * ldo + n] += v;
           else ((float*)out)[(size_t)m * ldo + n] = v;
         }
       }
@@ -233,13 +273,15 @@ __global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__
   const int e = g.tile_e[ti], m0 = g.tile_m0[ti];
   const int cnt = g.e_cnt[e], base = g.e_off[e];
   const int n0 = blockIdx.x * BN;
-  __shared__ __attribute__((aligned(16))) GemmSmem<BM, BN> sm;
+  BD_GEMM_SMEM(BM, BN);
   MfmaTile<BM, BN> t;
   const bf16_t* We = W + (size_t)e * g.w_stride;
   if (g.a_rows)
-    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, 0, n0, t, sm, g.a_rows + base + m0, cnt - m0);
+    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, 0, n0, t, gs0, gs1, gs2, gs3,
+                          threadIdx.x >> 6, g.a_rows + base + m0, cnt - m0);
   else
-    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, base + m0, n0, t, sm);
+    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, base + m0, n0, t, gs0, gs1, gs2, gs3,
+                          threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -268,7 +310,7 @@ __global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__
 hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
                                int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
                                int ldo, size_t out_plane, hipStream_t st) {
-  if (N % 128 || K % TBK) return hipErrorInvalidValue;
+  if (N % 128 || K % KALIGN) return hipErrorInvalidValue;
   dim3 grid(N / 128, max_tiles);
   if (epi == EPI_SWIGLU)
     k_gemm_grouped<EPI_SWIGLU><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W,
@@ -277,36 +319,6 @@ hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, 
     k_gemm_grouped<EPI_STORE_F32><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane,
                                                         (const bf16_t*)W, ldw, K, g, out, ldo, 0);
   return hipGetLastError();
-}
-
-// Deterministic split-K reduction: sums the splits in order, then applies
-// the epilogue.  One thread per output element (SwiGLU: per output feature).
-template <int EPI>
-__global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ ws, int splits,
-                                                       int N, int rows_cap,
-                                                       const int32_t* __restrict__ Mp,
-                                                       void* __restrict__ out, int ldo,
-                                                       size_t out_plane) {
-  const int M = *Mp;
-  const int ncols = (EPI == EPI_SWIGLU) ? N / 2 : N;
-  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int m = (int)(idx / ncols), c = (int)(idx % ncols);
-  if (m >= M) return;
-  if constexpr (EPI == EPI_SWIGLU) {
-    const int pg = (c >> 4) * 32 + (c & 15);
-    float g = 0.f, u = 0.f;
-    for (int z = 0; z < splits; ++z) {
-      const float* w = ws + ((size_t)z * rows_cap + m) * N;
-      g += w[pg];
-      u += w[pg + 16];
-    }
-    store_pair((bf16_t*)out + (size_t)m * ldo + c, out_plane, silu(g) * u);
-  } else {
-    float v = 0.f;
-    for (int z = 0; z < splits; ++z) v += ws[((size_t)z * rows_cap + m) * N + c];
-    if constexpr (EPI == EPI_ADD_F32) ((float*)out)[(size_t)m * ldo + c] += v;
-    else ((float*)out)[(size_t)m * ldo + c] = v;
-  }
 }
 
 // Fused LM head: for its 128 vocabulary columns the workgroup reduces each row
@@ -324,11 +336,11 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
   const int m0 = blockIdx.y * TBM;
   if (m0 >= M) return;
   const int n0 = blockIdx.x * TBN;
-  __shared__ __attribute__((aligned(16))) GemmSmem<TBM, TBN> sm;
+  BD_GEMM_SMEM(TBM, TBN);
   __shared__ float red_m[2][TBM], red_s[2][TBM];
   __shared__ int32_t red_a[2][TBM];
   MfmaTile<TBM, TBN> t;
-  mfma_mainloop<TBM, TBN>(A, d, a_plane, W, d, 0, d, m0, n0, t, sm);
+  mfma_mainloop<TBM, TBN>(A, d, a_plane, W, d, 0, d, m0, n0, t, gs0, gs1, gs2, gs3, threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -538,76 +550,83 @@ __global__ __launch_bounds__(256) void k_lm_merge(const float* __restrict__ pmax
 template <int BM, int BN>
 static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const bf16_t* w,
                             int ldw, int N, int K, const int32_t* M_dev, void* o, int ldo, size_t op,
-                            float* ws, int rows_cap, hipStream_t st) {
+                            float* ws, hipStream_t st) {
   switch (epi) {
     case EPI_ADD_F32:
-      k_gemm_bf16<BM, BN, EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, rows_cap);
+      k_gemm_bf16<BM, BN, EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws);
       break;
     case EPI_SWIGLU:
-      k_gemm_bf16<BM, BN, EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, rows_cap);
+      k_gemm_bf16<BM, BN, EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr);
       break;
     default:
-      k_gemm_bf16<BM, BN, EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, rows_cap);
+      k_gemm_bf16<BM, BN, EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr);
       break;
   }
 }
 
-// Tile choice: the largest tile that still gives >= 512 workgroups over the
-// row capacity; otherwise 64x64 tiles with a deterministic split-K (each
-// split at least 512 deep, workspace permitting) to reach that count.
+// Tile choice: 128x128 when that tiling gives at least 512 workgroups over
+// the row capacity (the 64x64 tile runs out of LDS bandwidth on large
+// products), else 64x64.  zmax: the largest residual split (1 = none).
 GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap) {
-  GemmPlan p{64, 64, 1};
-  if (!is_bf16) return p;
-  const int target = 512;
-  const int cand[3][2] = {{128, 128}, {64, 128}, {64, 64}};
-  for (auto& c : cand) {
-    if (N % c[1]) continue;
-    const int wgs = (N / c[1]) * cdiv(rows_cap, c[0]);
-    if (wgs >= target) return GemmPlan{c[0], c[1], 1};
-  }
-  const int wgs = (N / 64) * cdiv(rows_cap, 64);
-  int splits = 1;
-  while (wgs * splits < target && K % (2 * splits * TBK) == 0 && K / (2 * splits) >= 512) splits *= 2;
-  return GemmPlan{64, 64, splits};
+  (void)K;
+  if (!is_bf16) return GemmPlan{64, 64, 1};
+  if (N % 128 == 0 && (N / 128) * cdiv(rows_cap, 128) >= 512) return GemmPlan{128, 128, 1};
+  return GemmPlan{64, 64, 1};
 }
 
-size_t gemm_workspace_floats(const GemmPlan& p, int N, int rows_cap) {
-  return p.splits > 1 ? (size_t)p.splits * rows_cap * N : 0;
+hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
+                               const void* W, int ldw, int N, int K, const int32_t* M_dev,
+                               int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
+                               hipStream_t st) {
+  const bool big = p.bm == 128 && p.bn == 128, small = p.bm == 64 && p.bn == 64;
+  if ((!big && !small) || p.zmax < 1 || p.zmax > 8) return hipErrorInvalidValue;
+  if (N % p.bn || K % KALIGN) return hipErrorInvalidValue;
+  if (p.zmax > 1 && (epi != EPI_ADD_F32 || !ws)) return hipErrorInvalidValue;
+  dim3 grid(N / p.bn, cdiv(rows_cap, p.bm), p.zmax);
+  const bf16_t* a = (const bf16_t*)A;
+  const bf16_t* w = (const bf16_t*)W;
+  if (big) launch_bf16_cfg<128, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, st);
+  else launch_bf16_cfg<64, 64>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
+                             int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
+                             int ldx, float* ws, ResidSplit* fold, hipStream_t st) {
+  fold->ws = nullptr;
+  if (!is_bf16 || !ws)
+    return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st);
+  // deep products (K >= 4096) take 128x128 tiles: with K split, their A and
+  // W re-reads halve against 64x64 at the same parallelism
+  GemmPlan p = plan_gemm(true, N, K, rows_cap);
+  if (K >= 4096 && N % 128 == 0) p = GemmPlan{128, 128, 1};
+  p.zmax = 8;
+  hipError_t e = launch_gemm_planned(p, EPI_ADD_F32, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap,
+                                     X, ldx, 0, ws, st);
+  if (e != hipSuccess) return e;
+  fold->ws = ws;
+  fold->Mp = M_dev;
+  fold->nx = N / p.bn;
+  fold->bm = p.bm;
+  fold->K = K;
+  fold->zmax = p.zmax;
+  return hipSuccess;
 }
 
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       size_t out_plane, float* ws, size_t ws_floats, hipStream_t st) {
-  if (is_bf16) {
-    GemmPlan p = plan_gemm(true, N, K, rows_cap);
-    if (gemm_workspace_floats(p, N, rows_cap) > ws_floats || !ws) p.splits = 1;
-    if (N % p.bn || K % (TBK * p.splits)) return hipErrorInvalidValue;
-    dim3 grid(N / p.bn, cdiv(rows_cap, p.bm), p.splits);
-    const bf16_t* a = (const bf16_t*)A;
-    const bf16_t* w = (const bf16_t*)W;
-    if (p.bm == 128) launch_bf16_cfg<128, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, rows_cap, st);
-    else if (p.bn == 128) launch_bf16_cfg<64, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, rows_cap, st);
-    else launch_bf16_cfg<64, 64>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, rows_cap, st);
-    if (p.splits > 1) {
-      const int ncols = epi == EPI_SWIGLU ? N / 2 : N;
-      const size_t total = (size_t)rows_cap * ncols;
-      const int blocks = (int)((total + 255) / 256);
-      switch (epi) {
-        case EPI_ADD_F32: k_splitk_reduce<EPI_ADD_F32><<<blocks, 256, 0, st>>>(ws, p.splits, N, rows_cap, M_dev, out, ldo, out_plane); break;
-        case EPI_SWIGLU: k_splitk_reduce<EPI_SWIGLU><<<blocks, 256, 0, st>>>(ws, p.splits, N, rows_cap, M_dev, out, ldo, out_plane); break;
-        default: k_splitk_reduce<EPI_STORE_F32><<<blocks, 256, 0, st>>>(ws, p.splits, N, rows_cap, M_dev, out, ldo, out_plane); break;
-      }
-    }
-  } else {
-    if (N % SBN || K % SBK) return hipErrorInvalidValue;
-    dim3 grid(N / SBN, cdiv(rows_cap, SBM));
-    const float* a = (const float*)A;
-    const float* w = (const float*)W;
-    switch (epi) {
-      case EPI_ADD_F32: k_gemm_f32<EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, out, ldo); break;
-      case EPI_SWIGLU: k_gemm_f32<EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, out, ldo); break;
-      default: k_gemm_f32<EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, out, ldo); break;
-    }
+                       size_t out_plane, hipStream_t st) {
+  if (is_bf16)
+    return launch_gemm_planned(plan_gemm(true, N, K, rows_cap), epi, A, lda, a_plane, W, ldw, N, K,
+                               M_dev, rows_cap, out, ldo, out_plane, nullptr, st);
+  if (N % SBN || K % SBK) return hipErrorInvalidValue;
+  dim3 grid(N / SBN, cdiv(rows_cap, SBM));
+  const float* a = (const float*)A;
+  const float* w = (const float*)W;
+  switch (epi) {
+    case EPI_ADD_F32: k_gemm_f32<EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, out, ldo); break;
+    case EPI_SWIGLU: k_gemm_f32<EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, out, ldo); break;
+    default: k_gemm_f32<EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, w, ldw, N, K, M_dev, out, ldo); break;
   }
   return hipGetLastError();
 }
@@ -619,7 +638,7 @@ hipError_t launch_lm_head(bool is_bf16, const void* A, int d, size_t a_plane, co
                           hipStream_t st) {
   int ntiles;
   if (is_bf16) {
-    if (V % 128 || d % TBK) return hipErrorInvalidValue;
+    if (V % 128 || d % KALIGN) return hipErrorInvalidValue;
     ntiles = V / 128;
     dim3 grid(ntiles, cdiv(rows_cap, 128));
     k_lm_head_bf16<<<grid, 256, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, mask_id, scale, M_dev,
@@ -650,7 +669,7 @@ hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, size_t a_plane, 
                             int mask_id, float scale, const int32_t* M_dev, int rows_cap,
                             float* logits, hipStream_t st) {
   hipError_t e = launch_gemm(EPI_STORE_F32, is_bf16, A, d, a_plane, W, d, V, d, M_dev, rows_cap,
-                             logits, V, 0, nullptr, 0, st);
+                             logits, V, 0, st);
   if (e != hipSuccess) return e;
   k_logits_post<<<dim3(cdiv(V, 256 * 8), rows_cap), 256, 0, st>>>(logits, V, mask_id, scale, M_dev);
   return hipGetLastError();

@@ -62,6 +62,35 @@ inline PlanView plan_view(int32_t* base, int rows_cap, int lm_cap, int b) {
 // GEMM epilogues.
 enum { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
 
+// bf16 GEMM depth granularity: K (per split) is a multiple of 4 pipeline
+// stages of 32.
+constexpr int KALIGN = 128;
+
+// Split-K of the residual-adding projections (O and down).  When the live
+// row count M leaves too few output tiles to occupy the chip, the GEMM
+// splits K into S parts; each writes its raw partial to ws[S][mt*bm][N]
+// (mt = row tiles of M) and the next RMSNorm of the residual stream adds
+// x += partial_0 + ... + partial_{S-1} (split order) before normalising.
+// Both kernels derive S from M with resid_splits, so no host round trip.
+struct ResidSplit {
+  float* ws;            // NULL: nothing pending
+  const int32_t* Mp;    // row count of the producing GEMM
+  int nx, bm, K, zmax;  // its column tiles, row tile, depth and largest split
+};
+constexpr int RESID_TARGET_128 = 256;   // workgroups aimed at with 128-row tiles
+constexpr int RESID_TARGET_64 = 512;    // ... with 64-row tiles
+// S > 1 only when tiles * S <= target, so partials fit target * 128 * 128 floats
+constexpr size_t RESID_WS_FLOATS = (size_t)RESID_TARGET_128 * 128 * 128;
+__device__ __forceinline__ int resid_splits(int M, const ResidSplit& r) {
+  const int tiles = r.nx * ((M + r.bm - 1) / r.bm);
+  const int target = r.bm == 128 ? RESID_TARGET_128 : RESID_TARGET_64;
+  int S = 1;
+  while (S * 2 <= r.zmax && tiles * S * 2 <= target && r.K % (S * 2 * KALIGN) == 0 &&
+         r.K / (S * 2) >= 256)
+    S *= 2;
+  return S;
+}
+
 // ---- launchers (defined in the .hip files) ---------------------------------
 // C[M][N] (+)= A[M][K] . W[N][K]^T with M read from *M_dev; grid covers rows_cap.
 // bf16 models: A is a bf16 plane pair (hi at A, lo at A + a_plane elements),
@@ -69,11 +98,9 @@ enum { EPI_STORE_F32 = 0, EPI_ADD_F32 = 1, EPI_SWIGLU = 2 };
 //   EPI_STORE_F32 / EPI_ADD_F32: out fp32 [M][ldo]
 //   EPI_SWIGLU: silu(gate) * up [M][ldo] (W packed gate/up in 16-row groups),
 //   as a bf16 plane pair (out_plane) for bf16 models, fp32 otherwise
-//   ws (optional, ws_floats capacity): split-K workspace; without room the
-//   launch runs unsplit.
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       size_t out_plane, float* ws, size_t ws_floats, hipStream_t st);
+                       size_t out_plane, hipStream_t st);
 // Expert tiles of a grouped GEMM (all device pointers).
 struct GroupTiles {
   const int32_t* tile_e;    // [max_tiles] expert of each tile
@@ -114,10 +141,22 @@ hipError_t launch_moe_combine(float* X, const float* Y, const int32_t* pos_of, c
 hipError_t launch_transpose_f32(const float* in, float* out, int rows, int cols, hipStream_t st);
 
 struct GemmPlan {
-  int bm, bn, splits;
+  int bm, bn, zmax;        // tile; largest residual K-split (1 = none)
 };
 GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap);
-size_t gemm_workspace_floats(const GemmPlan& p, int N, int rows_cap);
+// bf16 GEMM with an explicit plan (128x128 or 64x64; K % KALIGN == 0;
+// zmax > 1 only for EPI_ADD_F32 with a residual-split workspace ws).
+hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
+                               const void* W, int ldw, int N, int K, const int32_t* M_dev,
+                               int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
+                               hipStream_t st);
+// X[M][N] += A . W^T for the residual stream.  bf16 with ws (RESID_WS_FLOATS
+// floats): the kernel may split K (see ResidSplit) and *fold describes the
+// pending partials, which the next launch_rmsnorm of X must be given; else
+// the add is done in place and fold->ws is NULL.
+hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
+                             int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
+                             int ldx, float* ws, ResidSplit* fold, hipStream_t st);
 
 // LM head: per-row softmax statistics over the vocabulary of
 // z = scale * (A . W^T), mask column suppressed.  Writes per-(tile,row)
@@ -146,9 +185,11 @@ hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, con
                         hipStream_t st);
 // out: fp32 [rows][d] (fp32 models) or a bf16 plane pair (bf16 models,
 // lo plane at out + out_plane elements).
-hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
+// fold: pending residual split partials of the GEMM that produced X (ws
+// NULL for none); folded into X (rows reached through gather) first.
+hipError_t launch_rmsnorm(bool is_bf16, float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
-                          size_t out_plane, hipStream_t st);
+                          size_t out_plane, const ResidSplit& fold, hipStream_t st);
 // bf16 models: Q and the caches hold bf16 pairs (lo planes at + q_plane and
 // + kv_plane elements); fp32 models: fp32 values.
 hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,

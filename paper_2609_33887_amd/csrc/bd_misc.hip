@@ -73,16 +73,26 @@ __device__ __forceinline__ void put4(void* out, size_t plane, size_t idx, float4
 }
 
 template <bool PAIR>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X,
+__global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ X,
                                                  const float* __restrict__ g, int d, float eps,
                                                  const int32_t* __restrict__ Mp,
                                                  const int32_t* __restrict__ gather,
-                                                 void* __restrict__ out, size_t plane) {
+                                                 void* __restrict__ out, size_t plane,
+                                                 ResidSplit fold) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + wave;
   if (row >= *Mp) return;
   const int src = gather ? gather[row] : row;
-  const float* x = X + (size_t)src * d;
+  float* x = X + (size_t)src * d;
+  // pending residual split partials: x += p_0 + ... + p_{S-1}, written back
+  int S = 1;
+  size_t zstride = 0;
+  if (fold.ws) {
+    const int Mg = *fold.Mp;
+    S = resid_splits(Mg, fold);
+    zstride = (size_t)((Mg + fold.bm - 1) / fold.bm) * fold.bm * d;
+  }
+  const float* pz = fold.ws ? fold.ws + (size_t)src * d : nullptr;
   if (d % 256 == 0 && d <= 4096) {
     const int n4 = d / 256;
     float4 v[16];
@@ -90,6 +100,31 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X,
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       if (i < n4) v[i] = *(const float4*)(x + (i * 64 + lane) * 4);
+    if (S > 1) {
+      // four columns groups at a time, all S partials loaded before adding
+      // (S <= 8), then added in split order
+#pragma unroll
+      for (int i0 = 0; i0 < 16; i0 += 4) {
+        if (i0 >= n4) break;
+        float4 p[4][8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int z = 0; z < 8; ++z)
+            if (i0 + i < n4 && z < S) p[i][z] = *(const float4*)(pz + z * zstride + ((i0 + i) * 64 + lane) * 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int z = 0; z < 8; ++z)
+            if (i0 + i < n4 && z < S) {
+              v[i0 + i].x += p[i][z].x; v[i0 + i].y += p[i][z].y;
+              v[i0 + i].z += p[i][z].z; v[i0 + i].w += p[i][z].w;
+            }
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (i < n4) *(float4*)(x + (i * 64 + lane) * 4) = v[i];
+    }
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       if (i < n4) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
@@ -107,6 +142,12 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X,
       }
     return;
   }
+  if (S > 1)
+    for (int c = lane; c < d; c += 64) {
+      float v = x[c];
+      for (int z = 0; z < S; ++z) v += pz[z * zstride + c];
+      x[c] = v;
+    }
   float ss = 0.f;
   for (int c = lane; c < d; c += 64) ss += x[c] * x[c];
 #pragma unroll
@@ -124,13 +165,13 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X,
   }
 }
 
-hipError_t launch_rmsnorm(bool is_bf16, const float* X, const float* g, int d, float eps,
+hipError_t launch_rmsnorm(bool is_bf16, float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
-                          size_t out_plane, hipStream_t st) {
+                          size_t out_plane, const ResidSplit& fold, hipStream_t st) {
   if (is_bf16)
-    k_rmsnorm<true><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, out_plane);
+    k_rmsnorm<true><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, out_plane, fold);
   else
-    k_rmsnorm<false><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, 0);
+    k_rmsnorm<false><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, 0, fold);
   return hipGetLastError();
 }
 
