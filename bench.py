@@ -98,6 +98,9 @@ def main():
     ap.add_argument("--tau", type=float, default=0.9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--trace-steps", type=int, default=0, metavar="N",
+                    help="only encode the prompts and run N denoising steps (a short program for "
+                         "rocprofv3 counter passes), print the per-step work counters and exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device 5 times (a known-size kernel that scales "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -127,6 +130,17 @@ def main():
     prompts = make_prompts(w)
     model = bd.Model(w, weights)
     st = bd.State(model, prompts, w.gen_len, args.tau, w.n_inflight, w.block_size)
+    if args.trace_steps:
+        torch.cuda.synchronize()
+        print(f"[bench] prefill done; running {args.trace_steps} denoising steps", file=sys.stderr, flush=True)
+        for _ in range(args.trace_steps):
+            st.step()
+            st.commit()
+        torch.cuda.synchronize()
+        print(json.dumps({"workload": w.name, "trace_steps": args.trace_steps, "stats": st.stats()}))
+        st.close()
+        model.close()
+        return
     # untimed reference decode: learn the step count, keep the trace
     done, S = False, 0
     while not done:

@@ -42,7 +42,8 @@ static bd_status fail(bd_status st, const char* fmt, ...) {
 
 struct LayerW {
   const float* attn_norm;
-  const void* w_qkv;
+  const void* w_qkv;    // caller's; bf16 models use the pair-interleaved copy w_qkv_p
+  void* w_qkv_p;
   const void* w_o;
   const float* ffn_norm;
   void* w_gu;           // dense: packed gate/up (library-owned)
@@ -145,6 +146,8 @@ struct bd_state {
   float* y_sorted;       // fp32 [assign_cap][d]
   void* Kc;
   void* Vc;
+  int vstride;           // V positions per (seq, kv head) slice (bf16: maxpos rounded up to 64)
+  double* rope;          // bf16: [maxpos][hd/2] (cos, sin) for the fused QKV epilogue
   int steps;
   bool pending;
   int32_t* host_flag;    // pinned
@@ -235,6 +238,15 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
     L = LayerW{};
     L.attn_norm = (const float*)w[t++];
     L.w_qkv = w[t++];
+    if (bf16) {
+      const int qkv_rows = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+      L.w_qkv_p = owned_alloc((size_t)qkv_rows * row_bytes);
+      if (!L.w_qkv_p || launch_permute_qk_rows(L.w_qkv, L.w_qkv_p, c.n_heads, c.n_kv_heads, c.head_dim,
+                                               row_bytes, m->stream) != hipSuccess) {
+        bd_model_free(m);
+        return fail(BD_ENOMEM, "QKV weight copy failed");
+      }
+    }
     L.w_o = w[t++];
     L.ffn_norm = (const float*)w[t++];
     bd_status r = BD_OK;
@@ -365,10 +377,11 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
   const hipStream_t st = m->stream;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
   const int qkv = (H + 2 * Hkv) * hd;
-  // cache layout [layer][seq][kv head][pos][hd]; bf16 models keep the lo
-  // planes of Q and of the whole cache after the hi planes
-  const size_t layer_kv = (size_t)s->b * Hkv * s->maxpos * hd * m->esz;
-  const size_t kv_plane = bf ? (size_t)c.n_layers * s->b * Hkv * s->maxpos * hd : 0;
+  // cache layout: K [layer][seq][kv head][pos][hd], V [layer][seq][kv head]
+  // [vstride / 64][hd][64] (bf16) or as K (fp32); bf16 models keep the lo
+  // planes of Q and of each whole cache after the hi planes
+  const size_t layer_k = (size_t)s->b * Hkv * s->maxpos * hd;
+  const size_t layer_v = (size_t)s->b * Hkv * hd * s->vstride;
   const size_t q_plane = bf ? (size_t)s->rows_cap * H * hd : 0;
   const int kv_splits = (bf && lm) ? s->attn_splits : 1;
   LAUNCH(BD_PROF_EMBED, launch_embed(bf, s->tokens, s->P + s->G, m->embed, d, c.vocab, plan,
@@ -376,19 +389,38 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
   ResidSplit pend{};     // residual split partials not yet folded into X
   for (int l = 0; l < c.n_layers; ++l) {
     const LayerW& L = m->layers[l];
-    void* Kl = (char*)s->Kc + l * layer_kv;
-    void* Vl = (char*)s->Vc + l * layer_kv;
+    KvView kv;
+    kv.K = (char*)s->Kc + l * layer_k * m->esz;
+    kv.V = (char*)s->Vc + l * layer_v * m->esz;
+    kv.k_plane = bf ? (size_t)c.n_layers * layer_k : 0;
+    kv.v_plane = bf ? (size_t)c.n_layers * layer_v : 0;
+    kv.maxpos = s->maxpos;
+    kv.vstride = s->vstride;
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.attn_norm, d, c.rms_eps, plan.hdr, nullptr,
                                         rows_cap, s->A, s->pl_A, pend, st));
     pend.ws = nullptr;
-    LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, s->pl_A, L.w_qkv, d, qkv, d,
-                                         plan.hdr, rows_cap, s->QKV, qkv, 0, st));
-    LAUNCH(BD_PROF_ROPE, launch_rope_kv(bf, s->QKV, plan, rows_cap, H, Hkv, hd, m->inv_freq, s->Qb,
-                                        q_plane, Kl, Vl, kv_plane, s->maxpos, st));
-    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, q_plane, Kl, Vl, kv_plane, s->Ob, s->pl_O, plan,
-                                          s->b, win_cap, H, Hkv, hd,
-                                          s->maxpos, s->B, kv_splits, s->attn_ws_o, s->attn_ws_ml,
-                                          rows_cap, st));
+    if (bf) {
+      QkvEpi e;
+      e.row_seq = plan.row_seq;
+      e.row_pos = plan.row_pos;
+      e.rope = s->rope;
+      e.Q = s->Qb;
+      e.q_plane = q_plane;
+      e.kv = kv;
+      e.H = H;
+      e.Hkv = Hkv;
+      e.hd = hd;
+      e.rows4 = s->B % 4 == 0;
+      LAUNCH(BD_PROF_GEMM_QKV, launch_gemm_qkv(s->A, d, s->pl_A, L.w_qkv_p, d, plan.hdr, rows_cap, e, st));
+    } else {
+      LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, s->pl_A, L.w_qkv, d, qkv, d,
+                                           plan.hdr, rows_cap, s->QKV, qkv, 0, st));
+      LAUNCH(BD_PROF_ROPE, launch_rope_kv(s->QKV, plan, rows_cap, H, Hkv, hd, m->inv_freq,
+                                          (float*)s->Qb, kv, st));
+    }
+    LAUNCH(BD_PROF_ATTN, launch_attention(bf, s->Qb, q_plane, kv,
+                                          s->Ob, s->pl_O, plan, s->b, win_cap, H, Hkv, hd, s->B,
+                                          kv_splits, s->attn_ws_o, s->attn_ws_ml, rows_cap, st));
     LAUNCH(BD_PROF_GEMM_O, launch_gemm_resid(bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d, H * hd,
                                              plan.hdr, rows_cap, s->X, d, s->resid_ws, &pend, st));
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
@@ -478,7 +510,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
     s->pl_H = (size_t)s->rows_cap * (c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim);
     s->pl_lm = (size_t)s->lm_cap * d;
   }
-  ALLOC(s->QKV, (size_t)s->rows_cap * qkv * 4);
+  if (!m->bf16) ALLOC(s->QKV, (size_t)s->rows_cap * qkv * 4);
   ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * 4);     // fp32, or a bf16 plane pair
   ALLOC(s->Ob, (size_t)s->rows_cap * H * hd * 4);
   const int Fh = c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim;   // dense / shared FFN width
@@ -489,9 +521,20 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ALLOC(s->parg, (size_t)ntiles * s->lm_cap * 4);
   ALLOC(s->conf, (size_t)s->lm_cap * 4);
   ALLOC(s->tok, (size_t)s->lm_cap * 4);
-  const size_t kv_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * 4;   // fp32 or 2 bf16 planes
-  ALLOC(s->Kc, kv_bytes);
-  ALLOC(s->Vc, kv_bytes);
+  // fp32 values or 2 bf16 planes: 4 bytes per element either way
+  s->vstride = m->bf16 ? round_up(s->maxpos, 64) : s->maxpos;
+  const size_t k_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * 4;
+  const size_t v_bytes = (size_t)c.n_layers * b * Hkv * hd * s->vstride * 4;
+  ALLOC(s->Kc, k_bytes);
+  ALLOC(s->Vc, v_bytes);
+  if (m->bf16) {
+    ALLOC(s->rope, (size_t)s->maxpos * hd * sizeof(double));
+    hipError_t er = launch_rope_table(m->inv_freq, hd, s->maxpos, s->rope, m->stream);
+    if (er != hipSuccess) {
+      bd_state_free(s);
+      return fail(BD_EHIP, "rope table: %s", hipGetErrorString(er));
+    }
+  }
   if (m->bf16) ALLOC(s->resid_ws, RESID_WS_FLOATS * sizeof(float));
   if (c.n_experts > 0) {
     const int E = c.n_experts, k = c.top_k, Fe = c.expert_ffn;
@@ -528,7 +571,11 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   }
   // Row buffers are read in whole GEMM tiles: clear them once so that rows
   // past the live count never hold NaN patterns.
+  // The caches are cleared too: attention tiles read (and weigh by zero)
+  // positions past the live keys.
   hipError_t e = hipMemsetAsync(s->A, 0, (size_t)s->rows_cap * d * 4, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(s->Kc, 0, k_bytes, m->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(s->Vc, 0, v_bytes, m->stream);
   if (e == hipSuccess) e = hipMemsetAsync(s->Ob, 0, (size_t)s->rows_cap * H * hd * 4, m->stream);
   if (e == hipSuccess) e = hipMemsetAsync(s->Hact, 0, (size_t)s->rows_cap * (Fh > 0 ? Fh : 1) * 4, m->stream);
   if (e == hipSuccess) e = hipMemsetAsync(s->Alm, 0, (size_t)s->lm_cap * d * 4, m->stream);

@@ -4,18 +4,18 @@
 // K/V have already been written into the cache at their absolute positions,
 // so one key range [0, end of the query's block) covers prefix and window.
 //
-// bf16 kernel: one workgroup = 64 query rows of one head (4 wave64s x 16
-// queries).  Q, K and V are bf16 hi/lo pairs (two planes).  Key tiles of 64
-// positions stream from HBM through LDS with 16-byte coalesced loads (K
-// row-major, V transposed), and the wave computes
+// bf16 kernel (Q, K and V are bf16 hi/lo pairs in two planes; V is kept
+// transposed in the cache, in tiles of 64 keys [dim][64]): one workgroup =
+// 64 query rows of one head (4 wave64s x 16 queries).  Key tiles of 64
+// positions stream from HBM through LDS with 16-byte coalesced loads (K rows
+// and V^T tile rows, each tile a contiguous block), and the wave computes
 // S^T = K Q^T and O^T += V^T P^T with MFMA 16x16x32 bf16 (three products
 // hi.hi + hi.lo + lo.hi per pair of operands; the output leaves as the hi/lo
-// pair of the next matmul operand),
-// so each lane owns
-// one query column: the online-softmax state and the O rescale stay in the
-// lane, and P^T is fed to the second MFMA straight from the score registers
-// (the two products use the same permutation of the key index).  The block
-// mask is applied in registers, only on tiles that reach the query's block.
+// pair of the next matmul operand), so each lane owns one query column: the
+// online-softmax state and the O rescale stay in the lane, and P^T is fed to
+// the second MFMA straight from the score registers (the two products use
+// the same permutation of the key index).  The block mask is applied in
+// registers, only on tiles that reach the query's block.
 #include "bd_internal.h"
 
 #include <math.h>
@@ -34,9 +34,10 @@ constexpr int AK = 64;    // keys per tile
 
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q, size_t q_plane,
-                                                   const bf16_t* __restrict__ Kc,
-                                                   const bf16_t* __restrict__ Vc, size_t kv_plane,
-                                                   bf16_t* __restrict__ O, size_t o_plane,
+                                                   const bf16_t* __restrict__ Kc, size_t k_plane,
+                                                   const bf16_t* __restrict__ Vt, size_t v_plane,
+                                                   int vstride, bf16_t* __restrict__ O,
+                                                   size_t o_plane,
                                                    const int32_t* __restrict__ seq_row_start,
                                                    const int32_t* __restrict__ seq_win_len,
                                                    const int32_t* __restrict__ seq_win_start, int H,
@@ -65,9 +66,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
   const int per = (ntiles_all + kv_splits - 1) / kv_splits;
   const int t_lo = split * per, t_hi = min(ntiles_all, t_lo + per);
   const int kv = h / (H / Hkv);
-  const size_t kvbase = ((size_t)s * Hkv + kv) * (size_t)maxpos * HD;
-  const bf16_t* Kp = Kc + kvbase;
-  const bf16_t* Vp = Vc + kvbase;
+  const bf16_t* Kp = Kc + ((size_t)s * Hkv + kv) * (size_t)maxpos * HD;
+  const bf16_t* Vp = Vt + ((size_t)s * Hkv + kv) * (size_t)HD * vstride;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
@@ -96,40 +96,41 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
   float m_run = -INFINITY, l_part = 0.f;
 
   // register prefetch of the next K/V tile (both planes) overlaps the loads
-  // with the MFMAs of the current tile
+  // with the MFMAs of the current tile.  K: chunk ci = (key, 8 dims), keys
+  // >= kend read as zero.  V^T: chunk ci = (dim, 8 keys); a tile never
+  // reaches past vstride and the keys past kend there are finite cache
+  // contents that meet zero probabilities.
   u32x4 pkh[NCH], pkl[NCH], pvh[NCH], pvl[NCH];
 #define BD_FETCH(K0)                                                            \
   do {                                                                          \
     _Pragma("unroll") for (int it = 0; it < NCH; ++it) {                        \
       const int ci = tid + 256 * it;                                            \
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;                  \
-      pkh[it] = pkl[it] = pvh[it] = pvl[it] = u32x4{0u, 0u, 0u, 0u};            \
+      pkh[it] = pkl[it] = u32x4{0u, 0u, 0u, 0u};                                \
       if ((K0) + key < kend) {                                                  \
         const size_t o = (size_t)((K0) + key) * HD + dc;                        \
         pkh[it] = *(const u32x4*)(Kp + o);                                      \
-        pkl[it] = *(const u32x4*)(Kp + o + kv_plane);                           \
-        pvh[it] = *(const u32x4*)(Vp + o);                                      \
-        pvl[it] = *(const u32x4*)(Vp + o + kv_plane);                           \
+        pkl[it] = *(const u32x4*)(Kp + o + k_plane);                            \
       }                                                                         \
+      const int dim = ci / (AK / 8), kc8 = (ci % (AK / 8)) * 8;                 \
+      const size_t ov = vt_off((K0) + kc8, dim, HD);                            \
+      pvh[it] = *(const u32x4*)(Vp + ov);                                       \
+      pvl[it] = *(const u32x4*)(Vp + ov + v_plane);                             \
     }                                                                           \
   } while (0)
   if (t_lo < t_hi) BD_FETCH(t_lo * AK);
   for (int kt = t_lo; kt < t_hi; ++kt) {
     const int k0 = kt * AK;
-    // stage K (row-major) and V (transposed); keys >= kend are zero
+    // stage K (row-major) and V^T
 #pragma unroll
     for (int it = 0; it < NCH; ++it) {
       const int ci = tid + 256 * it;
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
       *(u32x4*)(sKh + key * KP + dc) = pkh[it];
       *(u32x4*)(sKl + key * KP + dc) = pkl[it];
-      const bf16_t* vh = (const bf16_t*)&pvh[it];
-      const bf16_t* vl = (const bf16_t*)&pvl[it];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sVh[(dc + e) * VP + key] = vh[e];
-        sVl[(dc + e) * VP + key] = vl[e];
-      }
+      const int dim = ci / (AK / 8), kc8 = (ci % (AK / 8)) * 8;
+      *(u32x4*)(sVh + dim * VP + kc8) = pvh[it];
+      *(u32x4*)(sVl + dim * VP + kc8) = pvl[it];
     }
     __syncthreads();
     if (kt + 1 < t_hi) BD_FETCH(k0 + AK);
@@ -332,35 +333,38 @@ int attention_splits(int b, int win_cap, int H, int maxpos) {
   return splits;
 }
 
-hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const void* Kc,
-                            const void* Vc, size_t kv_plane, void* O, size_t o_plane, PlanView plan,
-                            int b, int win_cap, int H, int Hkv, int hd, int maxpos, int B,
-                            int kv_splits, float* ws_o, float* ws_ml, int rows_cap, hipStream_t st) {
+hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const KvView& kv,
+                            void* O, size_t o_plane, PlanView plan, int b, int win_cap, int H,
+                            int Hkv, int hd, int B, int kv_splits, float* ws_o, float* ws_ml,
+                            int rows_cap, hipStream_t st) {
   if (is_bf16) {
+    if (hd != 64 && hd != 128) return hipErrorInvalidValue;
+    if (kv.vstride % 64 || kv.vstride < kv.maxpos) return hipErrorInvalidValue;
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)hd));
+    const bf16_t* q = (const bf16_t*)Q;
+    const bf16_t* k = (const bf16_t*)kv.K;
+    const bf16_t* v = (const bf16_t*)kv.V;
     if (kv_splits < 1 || (kv_splits > 1 && (!ws_o || !ws_ml))) return hipErrorInvalidValue;
     dim3 grid((win_cap + AQ - 1) / AQ, H, b * kv_splits);
     if (hd == 128)
-      k_attn_bf16<128><<<grid, 256, 0, st>>>((const bf16_t*)Q, q_plane, (const bf16_t*)Kc,
-                                             (const bf16_t*)Vc, kv_plane, (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
-                                             plan.seq_win_start, H, Hkv, maxpos, B, scale_log2,
+      k_attn_bf16<128><<<grid, 256, 0, st>>>(q, q_plane, k, kv.k_plane, v, kv.v_plane, kv.vstride,
+                                             (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
+                                             plan.seq_win_start, H, Hkv, kv.maxpos, B, scale_log2,
                                              kv_splits, ws_o, ws_ml, rows_cap);
-    else if (hd == 64)
-      k_attn_bf16<64><<<grid, 256, 0, st>>>((const bf16_t*)Q, q_plane, (const bf16_t*)Kc,
-                                            (const bf16_t*)Vc, kv_plane, (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
-                                            plan.seq_win_start, H, Hkv, maxpos, B, scale_log2,
-                                            kv_splits, ws_o, ws_ml, rows_cap);
     else
-      return hipErrorInvalidValue;
+      k_attn_bf16<64><<<grid, 256, 0, st>>>(q, q_plane, k, kv.k_plane, v, kv.v_plane, kv.vstride,
+                                            (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
+                                            plan.seq_win_start, H, Hkv, kv.maxpos, B, scale_log2,
+                                            kv_splits, ws_o, ws_ml, rows_cap);
     if (kv_splits > 1)
       k_attn_merge<<<rows_cap * H, 64, 0, st>>>(ws_o, ws_ml, kv_splits, plan.hdr, H, hd, rows_cap,
                                                 (bf16_t*)O, o_plane);
   } else {
     if (hd != 64 && hd != 128) return hipErrorInvalidValue;
     const int items = rows_cap * H;
-    k_attn_f32<<<(items + 3) / 4, 256, 0, st>>>((const float*)Q, (const float*)Kc, (const float*)Vc,
+    k_attn_f32<<<(items + 3) / 4, 256, 0, st>>>((const float*)Q, (const float*)kv.K, (const float*)kv.V,
                                                 (float*)O, plan.row_seq, plan.row_pos, plan.hdr, H,
-                                                Hkv, hd, maxpos, B, (float)(1.0 / sqrt((double)hd)));
+                                                Hkv, hd, kv.maxpos, B, (float)(1.0 / sqrt((double)hd)));
   }
   return hipGetLastError();
 }

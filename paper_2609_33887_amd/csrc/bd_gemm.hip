@@ -256,6 +256,101 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
   }
 }
 
+// QKV projection with RoPE and the K/V cache write in the epilogue (bf16).
+// In the accumulator layout a lane holds rows mb + r (r < 4) of column n;
+// the pair-interleaved weight puts the rotation partner of column n in
+// column n ^ 1, i.e. lane ^ 1.  q and k: y(i) = x(i) cos - x(i + hd/2) sin,
+// y(i + hd/2) = x(i + hd/2) cos + x(i) sin in fp64 with one rounding to
+// fp32, stored at the original dimension; v: four consecutive rows of one
+// sequence are four consecutive positions of one V^T tile row (one 8-byte store
+// per plane).
+__device__ __forceinline__ void store_pair4(bf16_t* p, size_t plane, const float v[4]) {
+  bf16_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    h[e] = f2bf(v[e]);
+    l[e] = f2bf(v[e] - bf2f(h[e]));
+  }
+  *(uint2*)p = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+  *(uint2*)(p + plane) =
+      make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
+}
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, int lda,
+                                                  size_t a_plane, const bf16_t* __restrict__ W,
+                                                  int K, const int32_t* __restrict__ Mp, QkvEpi e) {
+  constexpr int FM = BM / 32, FN = BN / 32;
+  const int M = *Mp;
+  const int m0 = blockIdx.y * BM;
+  if (m0 >= M) return;
+  const int n0 = blockIdx.x * BN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  BD_GEMM_SMEM(BM, BN);
+  MfmaTile<BM, BN> t;
+  mfma_mainloop<BM, BN>(A, lda, a_plane, W, K, 0, K, m0, n0, t, gs0, gs1, gs2, gs3, wave);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int hd = e.hd, half = hd >> 1;
+  const int qcols = e.H * hd, qkcols = (e.H + e.Hkv) * hd;
+  bf16_t* Q = (bf16_t*)e.Q;
+  bf16_t* Kc = (bf16_t*)e.kv.K;
+  bf16_t* Vc = (bf16_t*)e.kv.V;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int mb = m0 + wm * (BM / 2) + i * 16 + (lane >> 4) * 4;   // the lane's first row
+    int seq[4], pos[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool ok = mb + r < M;
+      seq[r] = ok ? e.row_seq[mb + r] : 0;
+      pos[r] = ok ? e.row_pos[mb + r] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * (BN / 2) + j * 16 + (lane & 15);
+      float v[4], pv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[r] = t.acc[i][j][r];
+        pv[r] = __shfl_xor(v[r], 1);
+      }
+      // a 16-column fragment lies inside one head, so the branch is uniform
+      if (n < qkcols) {
+        const int cp = n % hd, ip = cp >> 1;
+        const bool odd = cp & 1;
+        const int dim = odd ? ip + half : ip;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (mb + r >= M) continue;
+          const double* cs = e.rope + ((size_t)pos[r] * half + ip) * 2;
+          const double x1 = odd ? (double)pv[r] : (double)v[r];
+          const double x2 = odd ? (double)v[r] : (double)pv[r];
+          const float y = odd ? (float)(x2 * cs[0] + x1 * cs[1]) : (float)(x1 * cs[0] - x2 * cs[1]);
+          if (n < qcols) {
+            store_pair(Q + ((size_t)(mb + r) * e.H + n / hd) * hd + dim, e.q_plane, y);
+          } else {
+            const int kh = (n - qcols) / hd;
+            store_pair(Kc + (((size_t)seq[r] * e.Hkv + kh) * e.kv.maxpos + pos[r]) * hd + dim,
+                       e.kv.k_plane, y);
+          }
+        }
+      } else {
+        const int vn = n - qkcols, kh = vn / hd, dim = vn % hd;
+        if (e.rows4 && mb + 3 < M) {
+          store_pair4(Vc + ((size_t)seq[0] * e.Hkv + kh) * hd * e.kv.vstride + vt_off(pos[0], dim, hd),
+                      e.kv.v_plane, v);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (mb + r < M)
+              store_pair(Vc + ((size_t)seq[r] * e.Hkv + kh) * hd * e.kv.vstride + vt_off(pos[r], dim, hd),
+                         e.kv.v_plane, v[r]);
+        }
+      }
+    }
+  }
+}
+
 // Grouped GEMM over experts: tile ti covers rows [m0, m0 + 128) of expert
 // tile_e[ti]; the expert's rows sit at [e_off[e], e_off[e] + e_cnt[e]) of the
 // expert-sorted outputs.  The A rows are gathered through a_rows (token rows
@@ -611,6 +706,22 @@ hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plan
   fold->K = K;
   fold->zmax = p.zmax;
   return hipSuccess;
+}
+
+hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W, int K,
+                           const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st) {
+  const int N = (e.H + 2 * e.Hkv) * e.hd;
+  if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
+  const GemmPlan p = plan_gemm(true, N, K, rows_cap);
+  if (N % p.bn) return hipErrorInvalidValue;
+  dim3 grid(N / p.bn, cdiv(rows_cap, p.bm));
+  if (p.bm == 128)
+    k_gemm_qkv<128, 128><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W, K,
+                                                M_dev, e);
+  else
+    k_gemm_qkv<64, 64><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W, K, M_dev,
+                                              e);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,

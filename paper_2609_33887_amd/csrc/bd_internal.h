@@ -170,14 +170,36 @@ hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, size_t a_plane, 
                             int mask_id, float scale, const int32_t* M_dev, int rows_cap,
                             float* logits, hipStream_t st);
 
-// kv_splits > 1 splits every query tile's key range into that many
-// workgroups (partials in ws_o [splits][rows_cap][H][hd], ws_ml
-// [splits][rows_cap][H][2]) merged in split order.  rows_cap bounds the rows.
-// O: bf16 plane pair (lo at O + o_plane elements) for bf16 models, fp32 otherwise.
-hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const void* Kc,
-                            const void* Vc, size_t kv_plane, void* O, size_t o_plane, PlanView plan,
-                            int b, int win_cap, int H, int Hkv, int hd, int maxpos, int B,
-                            int kv_splits, float* ws_o, float* ws_ml, int rows_cap, hipStream_t st);
+// One layer's KV cache.  K: [seq][kv head][pos][hd].  V: bf16 models keep
+// it transposed in tiles of 64 keys, [seq][kv head][pos / 64][hd][64]: a
+// tile is one contiguous block per plane (DRAM page locality when streamed)
+// and a 16-byte load holds 8 consecutive keys of one dimension (the MFMA
+// operand layout of P.V); vt_off gives the offset inside a (seq, kv head)
+// slice of hd * vstride elements, vstride = maxpos rounded up to 64.  fp32
+// models keep V as K.  bf16 models store pairs: lo planes at + k_plane /
+// + v_plane elements.  The whole cache is cleared at allocation, so padding
+// and not yet written positions are finite.
+constexpr int VTILE = 64;
+__host__ __device__ __forceinline__ size_t vt_off(int pos, int dim, int hd) {
+  return ((size_t)(pos / VTILE) * hd + dim) * VTILE + (pos % VTILE);
+}
+struct KvView {
+  void* K;
+  void* V;
+  size_t k_plane, v_plane;
+  int maxpos, vstride;
+};
+
+// Attention of the rows of `plan` over the cache.  bf16 models: 64-query
+// tiles of one head, 64-key tiles staged in LDS; kv_splits > 1 splits every
+// query tile's key range into that many workgroups (partials in ws_o
+// [splits][rows_cap][H][hd], ws_ml [splits][rows_cap][H][2]) merged in split
+// order.  O: bf16 plane pair (lo at O + o_plane elements) for bf16 models,
+// fp32 otherwise.
+hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const KvView& kv, void* O,
+                            size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
+                            int hd, int B, int kv_splits, float* ws_o, float* ws_ml, int rows_cap,
+                            hipStream_t st);
 int attention_splits(int b, int win_cap, int H, int maxpos);
 
 hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
@@ -190,11 +212,10 @@ hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, con
 hipError_t launch_rmsnorm(bool is_bf16, float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
                           size_t out_plane, const ResidSplit& fold, hipStream_t st);
-// bf16 models: Q and the caches hold bf16 pairs (lo planes at + q_plane and
-// + kv_plane elements); fp32 models: fp32 values.
-hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
-                          int Hkv, int hd, const double* inv_freq, void* Q, size_t q_plane, void* Kc,
-                          void* Vc, size_t kv_plane, int maxpos, hipStream_t st);
+// fp32 models: RoPE of q and k at the rows' absolute positions; q ->
+// Q[row][head][hd], k and v -> the cache (layout of KvView, fp32).
+hipError_t launch_rope_kv(const float* QKV, PlanView plan, int rows_cap, int H, int Hkv, int hd,
+                          const double* inv_freq, float* Q, const KvView& kv, hipStream_t st);
 
 struct CommitArgs {
   PlanView in, out;
@@ -227,6 +248,32 @@ hipError_t launch_init_decode(const InitArgs& a, hipStream_t st);
 // Debug scatter of per-LM-row conf/tok to [b][G].
 hipError_t launch_scatter_stats(const float* conf, const int32_t* tok, PlanView plan, int P, int G,
                                 float* dconf, int32_t* dtok, int lm_cap, hipStream_t st);
+// QKV projection of bf16 models with RoPE and the cache write in the
+// epilogue.  W is the pair-interleaved copy made by launch_permute_qk_rows
+// (in each q and k head, packed row 2i = dim i, 2i + 1 = dim i + hd/2, so a
+// rotation pair sits in adjacent accumulator lanes); the rotation uses the
+// fp64 table of launch_rope_table.  Q -> [rows][H][hd], K and V -> the cache
+// (layout of KvView), all as bf16 pairs in the original dimension order.
+struct QkvEpi {
+  const int32_t* row_seq;   // [rows] plan: sequence of each row
+  const int32_t* row_pos;   // [rows] plan: absolute position of each row
+  const double* rope;       // [maxpos][hd/2][2]: cos, sin
+  void* Q;
+  size_t q_plane;
+  KvView kv;
+  int H, Hkv, hd;
+  int rows4;                // 1: every aligned group of 4 rows is 4 consecutive
+                            // positions of one sequence (block size % 4 == 0)
+};
+hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W, int K,
+                           const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st);
+// Copy of a [(H + 2 Hkv) hd][d] QKV weight with the q and k head rows
+// pair-interleaved (see QkvEpi); v rows unchanged.
+hipError_t launch_permute_qk_rows(const void* W, void* out, int H, int Hkv, int hd, size_t row_bytes,
+                                  hipStream_t st);
+// tab[pos][i] = (cos, sin) of pos * inv_freq[i] in fp64, pos < maxpos, i < hd/2.
+hipError_t launch_rope_table(const double* inv_freq, int hd, int maxpos, double* tab, hipStream_t st);
+
 // Interleave gate/up projections in groups of 16 rows (SwiGLU epilogue layout).
 hipError_t launch_pack_gate_up(const void* gate, const void* up, void* out, int F, size_t row_bytes,
                                hipStream_t st);

@@ -50,10 +50,13 @@ hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, con
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One wave per row: y = x / sqrt(mean(x^2) + eps) * g in fp32.  Output as
-// fp32 (fp32 models) or as the bf16 pair hi = bf16(y), lo = bf16(y - hi) in
-// two planes (bf16 models: the matmul operand format).  Rows of d % 256 == 0
-// (d <= 4096) are read with all float4 loads in flight at once.
+// y = x / sqrt(mean(x^2) + eps) * g in fp32.  Output as fp32 (fp32 models)
+// or as the bf16 pair hi = bf16(y), lo = bf16(y - hi) in two planes (bf16
+// models: the matmul operand format).  Rows with d % 256 == 0 (d <= 4096)
+// are spread over min(256, d / 4) threads, one to four float4 per thread,
+// all loads (x and the pending split partials) in flight at once; the sum of
+// squares is reduced in a fixed order (lane shuffles, then the row's waves).
+// Other widths take one wave per row.
 __device__ __forceinline__ void put4(void* out, size_t plane, size_t idx, float4 y, bool pair) {
   if (!pair) {
     *(float4*)((float*)out + idx) = y;
@@ -79,11 +82,9 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ X,
                                                  const int32_t* __restrict__ gather,
                                                  void* __restrict__ out, size_t plane,
                                                  ResidSplit fold) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + wave;
-  if (row >= *Mp) return;
-  const int src = gather ? gather[row] : row;
-  float* x = X + (size_t)src * d;
+  __shared__ float red[4];
+  const int M = *Mp;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // pending residual split partials: x += p_0 + ... + p_{S-1}, written back
   int S = 1;
   size_t zstride = 0;
@@ -92,56 +93,73 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ X,
     S = resid_splits(Mg, fold);
     zstride = (size_t)((Mg + fold.bm - 1) / fold.bm) * fold.bm * d;
   }
-  const float* pz = fold.ws ? fold.ws + (size_t)src * d : nullptr;
   if (d % 256 == 0 && d <= 4096) {
-    const int n4 = d / 256;
-    float4 v[16];
+    const int tpr = min(256, d >> 2);          // threads per row: 64, 128 or 256
+    const int rpb = 256 / tpr;
+    const int row = blockIdx.x * rpb + (int)threadIdx.x / tpr;
+    const int t = (int)threadIdx.x % tpr;
+    const int nv = (d >> 2) / tpr;             // float4 per thread, <= 4
+    const bool valid = row < M;
+    const int src = valid ? (gather ? gather[row] : row) : 0;
+    float4* x4 = (float4*)(X + (size_t)src * d);
+    float4 v[4];
     float ss = 0.f;
+    if (valid) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < n4) v[i] = *(const float4*)(x + (i * 64 + lane) * 4);
-    if (S > 1) {
-      // four columns groups at a time, all S partials loaded before adding
-      // (S <= 8), then added in split order
-#pragma unroll
-      for (int i0 = 0; i0 < 16; i0 += 4) {
-        if (i0 >= n4) break;
+      for (int i = 0; i < 4; ++i)
+        if (i < nv) v[i] = x4[t + i * tpr];
+      if (S > 1) {
+        const float4* pz = (const float4*)(fold.ws + (size_t)src * d);
         float4 p[4][8];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int z = 0; z < 8; ++z)
-            if (i0 + i < n4 && z < S) p[i][z] = *(const float4*)(pz + z * zstride + ((i0 + i) * 64 + lane) * 4);
+            if (i < nv && z < S) p[i][z] = pz[z * (zstride >> 2) + t + i * tpr];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int z = 0; z < 8; ++z)
-            if (i0 + i < n4 && z < S) {
-              v[i0 + i].x += p[i][z].x; v[i0 + i].y += p[i][z].y;
-              v[i0 + i].z += p[i][z].z; v[i0 + i].w += p[i][z].w;
+            if (i < nv && z < S) {
+              v[i].x += p[i][z].x; v[i].y += p[i][z].y; v[i].z += p[i][z].z; v[i].w += p[i][z].w;
             }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (i < nv) x4[t + i * tpr] = v[i];
       }
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (i < n4) *(float4*)(x + (i * 64 + lane) * 4) = v[i];
+      for (int i = 0; i < 4; ++i)
+        if (i < nv) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < n4) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
-#pragma unroll
     for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    const int wpr = tpr >> 6;                  // waves per row
+    if (wpr > 1) {
+      if (lane == 0) red[wave] = ss;
+      __syncthreads();
+      const int w0 = (wave / wpr) * wpr;
+      ss = 0.f;
+      for (int w = 0; w < wpr; ++w) ss += red[w0 + w];
+    }
+    if (!valid) return;
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+    const float4* g4 = (const float4*)g;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < n4) {
-        const int c = (i * 64 + lane) * 4;
-        const float4 gg = *(const float4*)(g + c);
+    for (int i = 0; i < 4; ++i)
+      if (i < nv) {
+        const int c4 = t + i * tpr;
+        const float4 gg = g4[c4];
         const float4 y = make_float4(v[i].x * inv * gg.x, v[i].y * inv * gg.y, v[i].z * inv * gg.z,
                                      v[i].w * inv * gg.w);
-        put4(out, plane, (size_t)row * d + c, y, PAIR);
+        put4(out, plane, (size_t)row * d + 4 * c4, y, PAIR);
       }
     return;
   }
+  const int row = blockIdx.x * 4 + wave;
+  if (row >= M) return;
+  const int src = gather ? gather[row] : row;
+  float* x = X + (size_t)src * d;
+  const float* pz = fold.ws ? fold.ws + (size_t)src * d : nullptr;
   if (S > 1)
     for (int c = lane; c < d; c += 64) {
       float v = x[c];
@@ -168,76 +186,54 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ X,
 hipError_t launch_rmsnorm(bool is_bf16, float* X, const float* g, int d, float eps,
                           const int32_t* M_dev, const int32_t* gather, int rows_cap, void* out,
                           size_t out_plane, const ResidSplit& fold, hipStream_t st) {
+  const int rpb = (d % 256 == 0 && d <= 4096) ? 256 / min(256, d >> 2) : 4;   // rows per block
+  const int blocks = (rows_cap + rpb - 1) / rpb;
   if (is_bf16)
-    k_rmsnorm<true><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, out_plane, fold);
+    k_rmsnorm<true><<<blocks, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, out_plane, fold);
   else
-    k_rmsnorm<false><<<(rows_cap + 3) / 4, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, 0, fold);
+    k_rmsnorm<false><<<blocks, 256, 0, st>>>(X, g, d, eps, M_dev, gather, out, 0, fold);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ RoPE + KV
-// Rotate-half RoPE of q and k at the row's absolute position (angle and
-// rotation in fp64, one rounding to fp32); q -> Q[row][head][hd], k and v ->
-// the layer's cache slot [seq][kv head][pos][hd].  bf16 models store each
-// value as the bf16 pair hi = bf16(x), lo = bf16(x - hi) in two planes (lo at
-// + q_plane for Q, + kv_plane for the caches); fp32 models store fp32.
-template <bool BF16>
-__device__ __forceinline__ void put_val(void* base, size_t idx, size_t plane, float y) {
-  if constexpr (BF16) {
-    const bf16_t h = f2bf_m(y);
-    ((bf16_t*)base)[idx] = h;
-    ((bf16_t*)base)[idx + plane] = f2bf_m(y - bf2f_m(h));
-  } else {
-    ((float*)base)[idx] = y;
-  }
-}
-
-template <bool BF16>
+// fp32 models: rotate-half RoPE of q and k at the row's absolute position
+// (angle and rotation in fp64, one rounding to fp32); q -> Q[row][head][hd],
+// k and v -> the layer's cache slots [seq][kv head][pos][hd].  (bf16 models
+// do this in the QKV GEMM epilogue.)
 __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ QKV,
                                                  const int32_t* __restrict__ hdr,
                                                  const int32_t* __restrict__ row_seq,
                                                  const int32_t* __restrict__ row_pos, int H, int Hkv,
                                                  int hd, const double* __restrict__ inv_freq,
-                                                 void* __restrict__ Q, size_t q_plane,
-                                                 void* __restrict__ Kc, void* __restrict__ Vc,
-                                                 size_t kv_plane, int maxpos) {
+                                                 float* __restrict__ Q, KvView kv) {
   const int r = blockIdx.x;
   if (r >= hdr[0]) return;
   const int s = row_seq[r], pos = row_pos[r];
   const int half = hd / 2, qkv = (H + 2 * Hkv) * hd;
   const float* src = QKV + (size_t)r * qkv;
+  float* K = (float*)kv.K;
+  float* V = (float*)kv.V;
   for (int idx = threadIdx.x; idx < (H + Hkv) * half; idx += blockDim.x) {
     const int head = idx / half, i = idx % half;
     double sn, cs;
     sincos((double)pos * inv_freq[i], &sn, &cs);
     const double x1 = src[head * hd + i], x2 = src[head * hd + i + half];
     const float y1 = (float)(x1 * cs - x2 * sn), y2 = (float)(x2 * cs + x1 * sn);
-    if (head < H) {
-      const size_t o = ((size_t)r * H + head) * hd;
-      put_val<BF16>(Q, o + i, q_plane, y1);
-      put_val<BF16>(Q, o + i + half, q_plane, y2);
-    } else {
-      const size_t o = (((size_t)s * Hkv + (head - H)) * maxpos + pos) * hd;
-      put_val<BF16>(Kc, o + i, kv_plane, y1);
-      put_val<BF16>(Kc, o + i + half, kv_plane, y2);
-    }
+    float* o = (head < H) ? Q + ((size_t)r * H + head) * hd
+                          : K + (((size_t)s * Hkv + (head - H)) * kv.maxpos + pos) * hd;
+    o[i] = y1;
+    o[i + half] = y2;
   }
   for (int idx = threadIdx.x; idx < Hkv * hd; idx += blockDim.x) {
     const int kh = idx / hd, e = idx % hd;
-    const size_t o = (((size_t)s * Hkv + kh) * maxpos + pos) * hd + e;
-    put_val<BF16>(Vc, o, kv_plane, src[(H + Hkv) * hd + idx]);
+    V[(((size_t)s * Hkv + kh) * kv.maxpos + pos) * hd + e] = src[(H + Hkv) * hd + idx];
   }
 }
 
-hipError_t launch_rope_kv(bool is_bf16, const float* QKV, PlanView plan, int rows_cap, int H,
-                          int Hkv, int hd, const double* inv_freq, void* Q, size_t q_plane, void* Kc,
-                          void* Vc, size_t kv_plane, int maxpos, hipStream_t st) {
-  if (is_bf16)
-    k_rope_kv<true><<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd,
-                                              inv_freq, Q, q_plane, Kc, Vc, kv_plane, maxpos);
-  else
-    k_rope_kv<false><<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd,
-                                               inv_freq, Q, 0, Kc, Vc, 0, maxpos);
+hipError_t launch_rope_kv(const float* QKV, PlanView plan, int rows_cap, int H, int Hkv, int hd,
+                          const double* inv_freq, float* Q, const KvView& kv, hipStream_t st) {
+  k_rope_kv<<<rows_cap, 256, 0, st>>>(QKV, plan.hdr, plan.row_seq, plan.row_pos, H, Hkv, hd, inv_freq,
+                                      Q, kv);
   return hipGetLastError();
 }
 
@@ -548,6 +544,49 @@ hipError_t launch_pack_gate_up(const void* gate, const void* up, void* out, int 
   if (F % 16 || row_bytes % 4) return hipErrorInvalidValue;
   k_pack_gate_up<<<2 * F, 256, 0, st>>>((const uint8_t*)gate, (const uint8_t*)up, (uint8_t*)out,
                                         row_bytes);
+  return hipGetLastError();
+}
+
+// Pair-interleave the q and k head rows of a QKV weight: in each head,
+// packed row 2i <- dim i, 2i + 1 <- dim i + hd/2.  v rows are copied as is.
+__global__ void k_permute_qk_rows(const uint8_t* __restrict__ W, uint8_t* __restrict__ out, int qk_rows,
+                                  int hd, size_t row_bytes) {
+  const int pr = blockIdx.x;
+  int src = pr;
+  if (pr < qk_rows) {
+    const int head = pr / hd, cp = pr % hd;
+    src = head * hd + ((cp & 1) ? (cp >> 1) + hd / 2 : (cp >> 1));
+  }
+  const uint8_t* s = W + (size_t)src * row_bytes;
+  uint8_t* d = out + (size_t)pr * row_bytes;
+  for (size_t c = threadIdx.x * 4; c < row_bytes; c += blockDim.x * 4)
+    *(uint32_t*)(d + c) = *(const uint32_t*)(s + c);
+}
+
+hipError_t launch_permute_qk_rows(const void* W, void* out, int H, int Hkv, int hd, size_t row_bytes,
+                                  hipStream_t st) {
+  if (hd % 2 || row_bytes % 4) return hipErrorInvalidValue;
+  k_permute_qk_rows<<<(H + 2 * Hkv) * hd, 256, 0, st>>>((const uint8_t*)W, (uint8_t*)out,
+                                                        (H + Hkv) * hd, hd, row_bytes);
+  return hipGetLastError();
+}
+
+// cos/sin of pos * inv_freq[i] in fp64 (the angle and its sine and cosine
+// computed as in k_rope_kv).
+__global__ void k_rope_table(const double* __restrict__ inv_freq, int half, int maxpos,
+                             double* __restrict__ tab) {
+  const int pos = blockIdx.x;
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    double sn, cs;
+    sincos((double)pos * inv_freq[i], &sn, &cs);
+    tab[((size_t)pos * half + i) * 2] = cs;
+    tab[((size_t)pos * half + i) * 2 + 1] = sn;
+  }
+}
+
+hipError_t launch_rope_table(const double* inv_freq, int hd, int maxpos, double* tab, hipStream_t st) {
+  if (maxpos < 1) return hipSuccess;
+  k_rope_table<<<maxpos, 64, 0, st>>>(inv_freq, hd / 2, maxpos, tab);
   return hipGetLastError();
 }
 

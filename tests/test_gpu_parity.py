@@ -52,6 +52,10 @@ SMALL = {
     "moe": small("moe", seed=96, n_heads=4, n_kv_heads=2, head_dim=128, ffn_dim=0, n_experts=8, top_k=2,
                  expert_ffn=128, n_shared=1, batch=3, prompt_len=64, block_size=16, n_inflight=2,
                  gen_len=64),
+    # two q-heads per kv head, head_dim 128, one block of 16 in flight (small
+    # windows, ragged prompt of 5 blocks)
+    "stream128": small("stream128", seed=97, n_heads=4, n_kv_heads=2, head_dim=128, batch=3,
+                       prompt_len=80, block_size=16, n_inflight=1, gen_len=48),
     # long prefix: the attention key range is split over several workgroups
     "longprefix": small("longprefix", seed=94, n_heads=4, n_kv_heads=2, head_dim=128, batch=2,
                         prompt_len=2048, block_size=32, n_inflight=2, gen_len=64),
