@@ -48,9 +48,24 @@ __device__ __forceinline__ void store_pair(bf16_t* p, size_t plane, float x) {
 // consumed, and one barrier per stage both publishes the stage and retires
 // the one the next loads overwrite.  A wave's load instruction writes 1 KiB of
 // LDS = 16 rows x 64 B, lane l at byte 16 l; in LDS the 16-byte chunk c of row r
-// sits at position c ^ ((r >> 2) & 3), so that the 16 rows a quarter-wave
-// reads for one MFMA fragment fall on distinct bank groups.
+// sits at position c ^ swz(r), swz(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1), so
+// that the rows read together for one MFMA fragment fall on distinct bank
+// groups whether the LDS serves 8 lanes from 32 banks or 16 lanes from 64
+// banks per cycle.
 constexpr int SK = 32;       // K per pipeline stage (KALIGN = 4 stages)
+
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
+
+// Work item of a GEMM workgroup.  Launches are 1-D with at least items + 7
+// workgroups; the dispatcher deals consecutive workgroups to the 8 XCDs in
+// turn, and item u = (id % 8) * ceil(items / 8) + id / 8 gives each XCD a
+// contiguous range of items (items are numbered so that neighbours share
+// operand tiles), which then stay in that XCD's L2.  Workgroups with
+// id >= 8 ceil(items / 8), and those whose u >= items, get u = items (none).
+__device__ __forceinline__ int xcd_item(int id, int items) {
+  const int per = (items + 7) / 8;
+  return id < 8 * per ? (id % 8) * per + id / 8 : items;
+}
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -105,7 +120,7 @@ __device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN>& s, MfmaTile<
   const int lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int r16 = lane & 15;
-  const int pos = ((lane >> 4) ^ ((r16 >> 2) & 3)) * 8;   // fragment rows are r16 + 16 j
+  const int pos = ((lane >> 4) ^ swz(r16)) * 8;   // fragment rows are r16 + 16 j
   u32x4 bfr[FN];
 #pragma unroll
   for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&s.b[(wn * (BN / 2) + j * 16 + r16) * SK + pos]);
@@ -140,7 +155,7 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
                                               int nvalid = 0) {
   constexpr int LPS = 2 * (BM / 64) + BN / 64;   // load instructions per thread per stage
   const int lane = threadIdx.x & 63;
-  const int rsub = lane >> 2, chunk = (lane & 3) ^ ((rsub >> 2) & 3);
+  const int rsub = lane >> 2, chunk = (lane & 3) ^ swz(rsub);
   TileSrc<BM, BN> src;
 #pragma unroll
   for (int i = 0; i < BM / 64; ++i) {
@@ -195,38 +210,43 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
 #define BD_GEMM_SMEM(BM, BN)                                                     \
   __shared__ __attribute__((aligned(1024))) GemmStage<BM, BN> gs0, gs1, gs2, gs3
 
-// GEMM, epilogue applied in registers.  For EPI_ADD_F32 with a split
-// workspace, the kernel picks S = resid_splits(M) K-splits on the device
-// (gridDim.z is the largest allowed); with S > 1 every split stores its raw
-// partial tile to ws[split][row][col] (rows padded to whole tiles) and the
-// next RMSNorm of the residual stream adds the partials in split order.
+// GEMM, epilogue applied in registers.  Items (split z, column tile x, row
+// tile y) are numbered z-major, then x, then y: an XCD's range shares the A
+// and W slices of one split and the W tiles of a few column tiles.  For
+// EPI_ADD_F32 with a split workspace, the kernel picks S = resid_splits(M)
+// K-splits on the device (zmax is the largest allowed); with S > 1 every
+// split stores its raw partial tile to ws[split][row][col] (rows padded to
+// whole tiles) and the next RMSNorm of the residual stream adds the partials
+// in split order.
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
                                                    size_t a_plane, const bf16_t* __restrict__ W,
                                                    int ldw, int N, int K,
                                                    const int32_t* __restrict__ Mp,
                                                    void* __restrict__ out, int ldo, size_t out_plane,
-                                                   float* __restrict__ ws) {
+                                                   float* __restrict__ ws, int zmax) {
   constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
-  const int m0 = blockIdx.y * BM;
-  if (m0 >= M) return;
+  const int X = N / BN, Y = (M + BM - 1) / BM;
   int S = 1;
   if (EPI == EPI_ADD_F32 && ws) {
     ResidSplit r;
-    r.nx = gridDim.x; r.bm = BM; r.K = K; r.zmax = gridDim.z;
+    r.nx = X; r.bm = BM; r.K = K; r.zmax = zmax;
     S = resid_splits(M, r);
   }
-  if ((int)blockIdx.z >= S) return;
+  const int items = X * Y * S;
+  const int u = xcd_item(blockIdx.x, items);
+  if (u >= items) return;
+  const int z = u / (X * Y), xy = u % (X * Y);
+  const int m0 = (xy % Y) * BM, n0 = (xy / Y) * BN;
   const int klen = K / S;
-  const int n0 = blockIdx.x * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   BD_GEMM_SMEM(BM, BN);
   MfmaTile<BM, BN> t;
-  mfma_mainloop<BM, BN>(A, lda, a_plane, W, ldw, blockIdx.z * klen, klen, m0, n0, t, gs0, gs1, gs2,
+  mfma_mainloop<BM, BN>(A, lda, a_plane, W, ldw, z * klen, klen, m0, n0, t, gs0, gs1, gs2,
                         gs3, wave);
   const int wm = wave >> 1, wn = wave & 1;
-  float* wz = (EPI == EPI_ADD_F32 && S > 1) ? ws + (size_t)blockIdx.z * ((M + BM - 1) / BM) * BM * N
+  float* wz = (EPI == EPI_ADD_F32 && S > 1) ? ws + (size_t)z * ((M + BM - 1) / BM) * BM * N
                                             : nullptr;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
@@ -282,9 +302,10 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, 
                                                   int K, const int32_t* __restrict__ Mp, QkvEpi e) {
   constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
-  const int m0 = blockIdx.y * BM;
-  if (m0 >= M) return;
-  const int n0 = blockIdx.x * BN;
+  const int X = (e.H + 2 * e.Hkv) * e.hd / BN, Y = (M + BM - 1) / BM;
+  const int u = xcd_item(blockIdx.x, X * Y);      // items: column tile major, row tile minor
+  if (u >= X * Y) return;
+  const int m0 = (u % Y) * BM, n0 = (u / Y) * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   BD_GEMM_SMEM(BM, BN);
   MfmaTile<BM, BN> t;
@@ -421,16 +442,20 @@ hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, 
 // (column tile, row); logits never leave registers.
 __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__ A, int d,
                                                       size_t a_plane,
-                                                      const bf16_t* __restrict__ W, int mask_id,
+                                                      const bf16_t* __restrict__ W, int V, int mask_id,
                                                       float scale, const int32_t* __restrict__ Mp,
                                                       int rows_cap, float* __restrict__ pmax,
                                                       float* __restrict__ psum,
                                                       int32_t* __restrict__ parg) {
   constexpr int TBM = 128, TBN = 128;
   const int M = *Mp;
-  const int m0 = blockIdx.y * TBM;
-  if (m0 >= M) return;
-  const int n0 = blockIdx.x * TBN;
+  // items: vocabulary tile major, row tile minor (an XCD streams its share of
+  // the head once, every row tile of a vocabulary tile running together)
+  const int X = V / TBN, Y = (M + TBM - 1) / TBM;
+  const int u = xcd_item(blockIdx.x, X * Y);
+  if (u >= X * Y) return;
+  const int m0 = (u % Y) * TBM, n0 = (u / Y) * TBN;
+  const int vt = u / Y;
   BD_GEMM_SMEM(TBM, TBN);
   __shared__ float red_m[2][TBM], red_s[2][TBM];
   __shared__ int32_t red_a[2][TBM];
@@ -478,7 +503,7 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
       const float mm = fmaxf(ma, mb);
       const float s = red_s[0][rl] * expf(ma - mm) + red_s[1][rl] * expf(mb - mm);
       const int a = (ma >= mb) ? red_a[0][rl] : red_a[1][rl];
-      const size_t o = (size_t)blockIdx.x * rows_cap + m;
+      const size_t o = (size_t)vt * rows_cap + m;
       pmax[o] = mm;
       psum[o] = s;
       parg[o] = a;
@@ -645,16 +670,16 @@ __global__ __launch_bounds__(256) void k_lm_merge(const float* __restrict__ pmax
 template <int BM, int BN>
 static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const bf16_t* w,
                             int ldw, int N, int K, const int32_t* M_dev, void* o, int ldo, size_t op,
-                            float* ws, hipStream_t st) {
+                            float* ws, int zmax, hipStream_t st) {
   switch (epi) {
     case EPI_ADD_F32:
-      k_gemm_bf16<BM, BN, EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws);
+      k_gemm_bf16<BM, BN, EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, zmax);
       break;
     case EPI_SWIGLU:
-      k_gemm_bf16<BM, BN, EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr);
+      k_gemm_bf16<BM, BN, EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr, 1);
       break;
     default:
-      k_gemm_bf16<BM, BN, EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr);
+      k_gemm_bf16<BM, BN, EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr, 1);
       break;
   }
 }
@@ -677,11 +702,13 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
   if ((!big && !small) || p.zmax < 1 || p.zmax > 8) return hipErrorInvalidValue;
   if (N % p.bn || K % KALIGN) return hipErrorInvalidValue;
   if (p.zmax > 1 && (epi != EPI_ADD_F32 || !ws)) return hipErrorInvalidValue;
-  dim3 grid(N / p.bn, cdiv(rows_cap, p.bm), p.zmax);
+  // 1-D grid: every (split, column tile, row tile) of the row capacity, + 7
+  // (see xcd_item)
+  dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) * p.zmax + 7);
   const bf16_t* a = (const bf16_t*)A;
   const bf16_t* w = (const bf16_t*)W;
-  if (big) launch_bf16_cfg<128, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, st);
-  else launch_bf16_cfg<64, 64>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, st);
+  if (big) launch_bf16_cfg<128, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, st);
+  else launch_bf16_cfg<64, 64>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, st);
   return hipGetLastError();
 }
 
@@ -714,7 +741,7 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
   if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
   const GemmPlan p = plan_gemm(true, N, K, rows_cap);
   if (N % p.bn) return hipErrorInvalidValue;
-  dim3 grid(N / p.bn, cdiv(rows_cap, p.bm));
+  dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) + 7);
   if (p.bm == 128)
     k_gemm_qkv<128, 128><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W, K,
                                                 M_dev, e);
@@ -751,8 +778,8 @@ hipError_t launch_lm_head(bool is_bf16, const void* A, int d, size_t a_plane, co
   if (is_bf16) {
     if (V % 128 || d % KALIGN) return hipErrorInvalidValue;
     ntiles = V / 128;
-    dim3 grid(ntiles, cdiv(rows_cap, 128));
-    k_lm_head_bf16<<<grid, 256, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, mask_id, scale, M_dev,
+    dim3 grid(ntiles * cdiv(rows_cap, 128) + 7);
+    k_lm_head_bf16<<<grid, 256, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, V, mask_id, scale, M_dev,
                                         rows_cap, part_max, part_sum, part_arg);
   } else {
     if (V % SBN || d % SBK) return hipErrorInvalidValue;
