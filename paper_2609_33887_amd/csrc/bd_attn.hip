@@ -255,34 +255,41 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
 
 // Merge of the key splits (fixed split order): O = sum_s 2^(m_s - M) O_s /
 // sum_s 2^(m_s - M) l_s with M = max_s m_s (scores kept in log2 units).
+// A workgroup of 256 threads takes 256 / (hd / 4) (row, head) items, each
+// thread 4 consecutive dims of one item.
 __global__ __launch_bounds__(256) void k_attn_merge(const float* __restrict__ ws_o,
                                                     const float* __restrict__ ws_ml, int kv_splits,
                                                     const int32_t* __restrict__ Mp, int H, int hd,
                                                     int rows_cap, bf16_t* __restrict__ O,
                                                     size_t o_plane) {
-  const int item = blockIdx.x;                 // (row, head)
+  const int tpi = hd / 4;                                   // threads per item
+  const int item = blockIdx.x * (256 / tpi) + threadIdx.x / tpi;
+  const int e0 = (threadIdx.x % tpi) * 4;
   const int r = item / H, h = item % H;
   if (r >= *Mp) return;
   float M = -INFINITY;
   for (int z = 0; z < kv_splits; ++z) M = fmaxf(M, ws_ml[2 * (((size_t)z * rows_cap + r) * H + h)]);
-  float L = 0.f;
+  float L = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int z = 0; z < kv_splits; ++z) {
     const size_t b = ((size_t)z * rows_cap + r) * H + h;
     const float m = ws_ml[2 * b];
-    if (m != -INFINITY) L += exp2f(m - M) * ws_ml[2 * b + 1];
+    if (m == -INFINITY) continue;
+    const float w = exp2f(m - M);
+    L += w * ws_ml[2 * b + 1];
+    const float4 o = *(const float4*)(ws_o + b * hd + e0);
+    acc[0] += w * o.x; acc[1] += w * o.y; acc[2] += w * o.z; acc[3] += w * o.w;
   }
-  for (int e = threadIdx.x; e < hd; e += blockDim.x) {
-    float acc = 0.f;
-    for (int z = 0; z < kv_splits; ++z) {
-      const size_t b = ((size_t)z * rows_cap + r) * H + h;
-      const float m = ws_ml[2 * b];
-      if (m != -INFINITY) acc += exp2f(m - M) * ws_o[b * hd + e];
-    }
-    const float y = acc / L;
-    const bf16_t hb = f2bf_a(y);
-    O[((size_t)r * H + h) * hd + e] = hb;
-    O[((size_t)r * H + h) * hd + e + o_plane] = f2bf_a(y - bf2f_a(hb));
+  bf16_t hb[4], lb[4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+    const float y = acc[x] / L;
+    hb[x] = f2bf_a(y);
+    lb[x] = f2bf_a(y - bf2f_a(hb[x]));
   }
+  bf16_t* orow = O + ((size_t)r * H + h) * hd + e0;
+  *(uint2*)orow = make_uint2((uint32_t)hb[0] | ((uint32_t)hb[1] << 16), (uint32_t)hb[2] | ((uint32_t)hb[3] << 16));
+  *(uint2*)(orow + o_plane) =
+      make_uint2((uint32_t)lb[0] | ((uint32_t)lb[1] << 16), (uint32_t)lb[2] | ((uint32_t)lb[3] << 16));
 }
 
 // fp32 reference-precision kernel for small fp32 models: one wave64 per
@@ -325,11 +332,14 @@ __global__ __launch_bounds__(256) void k_attn_f32(const float* __restrict__ Q,
   for (int e = 0; e < per; ++e) o[lane * per + e] = acc[e] / l;
 }
 
-int attention_splits(int b, int win_cap, int H, int maxpos) {
+int attention_splits(int b, int win_cap, int H, int hd, int maxpos) {
   const int wgs = ((win_cap + AQ - 1) / AQ) * H * b;
+  // the query-tile kernel keeps 3 (hd 64) or 2 (hd 128) workgroups per CU
+  // resident: split the key range until the grid fills one resident round of
+  // 256 CUs, while every split keeps >= 2 key tiles of the longest range
+  const int round = (hd == 64 ? 3 : 2) * 256;
   int splits = 1;
-  // aim for >= 1024 workgroups while every split keeps >= 2 key tiles
-  while (wgs * splits < 1024 && maxpos / (AK * 2 * splits) >= 2 && splits < 16) splits *= 2;
+  while (wgs * (splits + 1) <= round && maxpos / (AK * (splits + 1)) >= 2 && splits < 16) ++splits;
   return splits;
 }
 
@@ -356,9 +366,11 @@ hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const K
                                             (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
                                             plan.seq_win_start, H, Hkv, kv.maxpos, B, scale_log2,
                                             kv_splits, ws_o, ws_ml, rows_cap);
-    if (kv_splits > 1)
-      k_attn_merge<<<rows_cap * H, 64, 0, st>>>(ws_o, ws_ml, kv_splits, plan.hdr, H, hd, rows_cap,
-                                                (bf16_t*)O, o_plane);
+    if (kv_splits > 1) {
+      const int items_per_block = 256 / (hd / 4);
+      k_attn_merge<<<(rows_cap * H + items_per_block - 1) / items_per_block, 256, 0, st>>>(
+          ws_o, ws_ml, kv_splits, plan.hdr, H, hd, rows_cap, (bf16_t*)O, o_plane);
+    }
   } else {
     if (hd != 64 && hd != 128) return hipErrorInvalidValue;
     const int items = rows_cap * H;
