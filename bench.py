@@ -35,26 +35,63 @@ PEAK_F32_TFLOPS = 157.3        # fp32 vector
 def algorithmic_work(w, stats):
     """FLOPs and HBM bytes per kernel class for the work recorded in ``stats``
     (counters summed over one decode).  Bytes count each weight once per
-    forward, the K/V read once per (sequence, kv head, layer) and the window
-    K/V written; FLOPs count only visible query-key pairs and masked LM rows."""
+    forward (for MoE layers, every expert: an upper bound, as nearly all of
+    the 64 experts receive rows at these batch sizes), the K/V read once per
+    (sequence, kv head, layer) and the window K/V written; FLOPs count only
+    visible query-key pairs and masked LM rows."""
     esz = 2 if w.dtype == "bf16" else 4     # weights
     asz = 4                                  # activations / KV: fp32 or a bf16 hi/lo pair
     d, H, Hkv, hd, F, V, L = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.ffn_dim, w.vocab, w.n_layers
     qkv = (H + 2 * Hkv) * hd
     rows, lm_rows, fw = stats["rows"], stats["lm_rows"], stats["forwards"]
-    gemm = {
-        "gemm_qkv": (qkv, d), "gemm_o": (d, H * hd), "gemm_gu": (2 * F, d), "gemm_down": (d, F),
-    }
+    gemm = {"gemm_qkv": (qkv, d), "gemm_o": (d, H * hd)}
+    if not w.n_experts:
+        gemm.update({"gemm_gu": (2 * F, d), "gemm_down": (d, F)})
     out = {}
     for k, (N, K) in gemm.items():
         flops = 2.0 * rows * N * K * L
         byts = (N * K * esz * fw + rows * K * asz + rows * N * 4) * L
         out[k] = (flops, byts)
+    if w.n_experts:
+        # routed experts: each row meets top_k experts; the shared experts see every row
+        Fe, Fs, E, k = w.expert_ffn, w.n_shared * w.expert_ffn, w.n_experts, w.top_k
+        out["gemm_gu"] = (2.0 * rows * (k * 2 * Fe + 2 * Fs) * d * L,
+                          ((E + w.n_shared) * 2 * Fe * d * esz * fw + rows * (k + 1) * d * asz) * L)
+        out["gemm_down"] = (2.0 * rows * (k * Fe + Fs) * d * L,
+                            ((E + w.n_shared) * Fe * d * esz * fw + rows * (k + 1) * (Fe * asz + d * 4)) * L)
     out["attn"] = (4.0 * hd * H * stats["pairs"] * L,
                    (stats["keys"] * Hkv * hd * 2 * asz + rows * H * hd * asz
                     + rows * H * hd * asz) * L)
     out["lm_head"] = (2.0 * lm_rows * V * d, V * d * esz * fw + lm_rows * d * asz)
     return out
+
+
+def source_tag(path):
+    """First 12 hex digits of the SHA-256 of a source file (to tell whether a
+    kernel changed since its counters were taken)."""
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:12]
+
+
+def measured_traffic(workload_name, kernel_class):
+    """HBM bytes per launch of ``kernel_class`` from the committed counter
+    summary of this workload (FETCH_SIZE and WRITE_SIZE passes, scaled by the
+    plain-copy calibration), or None when there is none or when the kernel
+    source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload_name}_{kernel_class}_hbm_counters.md")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("counters:"):
+                rec = dict(kv.split("=", 1) for kv in line.split()[1:])
+    if not rec or source_tag(os.path.join(ROOT, rec["source"])) != rec["source_sha256_12"]:
+        return None
+    return {"bytes_per_launch": float(rec["bytes_per_launch"]),
+            "algorithmic_bytes_per_launch": float(rec["algorithmic_bytes_per_launch"]),
+            "launches": rec["launches"]}
 
 
 def cpu_baseline(w, weights, prompts, tau, target_s=12.0):
@@ -203,7 +240,12 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": kernels[dom]["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    mt = measured_traffic(w.name, dom)
+    roof["traffic"] = mt["bytes_per_launch"] if mt else None
+    if mt:
+        roof["traffic_note"] = (f"HBM bytes per launch (FETCH_SIZE x2 + WRITE_SIZE x1) over {mt['launches'].replace('_', ' ')}; "
+                                f"algorithmic bytes per launch over the same launches: "
+                                f"{mt['algorithmic_bytes_per_launch']:.4g}")
     roof["kernel"] = dom
     roof["avg_launch_us"] = 1e3 * kernels[dom]["ms_per_decode"] / kernels[dom]["launches_per_decode"]
 
