@@ -182,3 +182,42 @@ def make_prompts(w: Workload, n: int | None = None, offset: int = 0) -> np.ndarr
     rng = np.random.default_rng(2000 + w.seed)
     allp = rng.integers(0, w.vocab - 1, size=(offset + n, w.prompt_len), dtype=np.int64)
     return allp[offset:offset + n].astype(np.int32)
+
+
+# ---- Redline harness inputs -------------------------------------------------
+# Random draws only: which prompts form a calibration half, the prompt-level
+# uniforms of a Monte Carlo trial, and planted correctness matrices.
+
+def split_masks(n: int, n_splits: int, cal_frac: float = 0.5, seed: int = 0) -> np.ndarray:
+    """[n_splits][n] uint8: 1 for the round(cal_frac * n) prompts of each
+    split's calibration half (a uniformly random subset), 0 for its test half."""
+    rng = np.random.default_rng([3000, seed])
+    k = int(round(cal_frac * n))
+    out = np.zeros((n_splits, n), dtype=np.uint8)
+    for s in range(n_splits):
+        out[s, rng.permutation(n)[:k]] = 1
+    return out
+
+
+def mc_uniforms(trials: int, k: int, n: int, seed: int = 0) -> np.ndarray:
+    """[trials][k][n] float64 uniforms on [0, 1)."""
+    return np.random.default_rng([4000, seed]).random((trials, k, n))
+
+
+def planted_correctness(n: int, risks, ref_index: int, ref_acc: float = 0.8, seed: int = 0,
+                        shared: bool = False) -> np.ndarray:
+    """[m][n] uint8 matrix: the reference is right on a random ref_acc share of
+    prompts; configuration j keeps each of those with probability 1 - risks[j]
+    (one uniform per prompt for every configuration when ``shared``) and is
+    right elsewhere with probability ref_acc."""
+    rng = np.random.default_rng([5000, seed])
+    m = len(risks)
+    ref = rng.random(n) < ref_acc
+    u_shared = rng.random(n)
+    out = np.zeros((m, n), dtype=np.uint8)
+    for j in range(m):
+        u = u_shared if shared else rng.random(n)
+        other = rng.random(n) < ref_acc
+        out[j] = np.where(ref, u >= risks[j], other)
+    out[ref_index] = ref
+    return out
