@@ -6,7 +6,10 @@
 //
 // bf16 kernel (Q, K and V are bf16 hi/lo pairs in two planes; V is kept
 // transposed in the cache, in tiles of 64 keys [dim][64]): one workgroup =
-// 64 query rows of one head (4 wave64s x 16 queries).  Key tiles of 64
+// 16 NW queries of one (sequence, kv head) -- window rows x the q-heads that
+// share the kv head -- as NW wave64s x 16 queries (NW = 2 when a window
+// holds at most 32 such queries, else 4); a wave with no query of its own
+// only helps stage the tiles.  Key tiles of 64
 // positions stream from HBM through LDS with 16-byte coalesced loads (K rows
 // and V^T tile rows, each tile a contiguous block), and the wave computes
 // S^T = K Q^T and O^T += V^T P^T with MFMA 16x16x32 bf16 (three products
@@ -29,11 +32,10 @@ __device__ __forceinline__ bf16_t f2bf_a(float f) {
   return (bf16_t)(u >> 16);
 }
 
-constexpr int AQ = 64;    // query rows per workgroup
 constexpr int AK = 64;    // keys per tile
 
-template <int HD>
-__global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q, size_t q_plane,
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict__ Q, size_t q_plane,
                                                    const bf16_t* __restrict__ Kc, size_t k_plane,
                                                    const bf16_t* __restrict__ Vt, size_t v_plane,
                                                    int vstride, bf16_t* __restrict__ O,
@@ -43,38 +45,52 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
                                                    const int32_t* __restrict__ seq_win_start, int H,
                                                    int Hkv, int maxpos, int B, float scale_log2,
                                                    int kv_splits, float* __restrict__ ws_o,
-                                                   float* __restrict__ ws_ml, int rows_cap) {
+                                                   float* __restrict__ ws_ml, int rows_cap,
+                                                   int b, int nqt) {
   constexpr int KP = HD + 8;        // padded K row (elements)
   constexpr int VP = AK + 8;        // padded transposed-V row
   constexpr int CH = AK * HD / 8;   // 16-byte chunks per K (or V) tile and plane
-  constexpr int NCH = CH / 256;     // chunks per thread
+  constexpr int NT = 64 * NW;       // threads
+  constexpr int AQ = 16 * NW;       // queries per workgroup
+  constexpr int NCH = CH / NT;      // chunks per thread
   __shared__ __attribute__((aligned(16))) bf16_t sKh[AK * KP];
   __shared__ __attribute__((aligned(16))) bf16_t sKl[AK * KP];
   __shared__ __attribute__((aligned(16))) bf16_t sVh[HD * VP];
   __shared__ __attribute__((aligned(16))) bf16_t sVl[HD * VP];
 
-  const int s = blockIdx.z / kv_splits, split = blockIdx.z % kv_splits;
-  const int h = blockIdx.y, qt = blockIdx.x;
+  // The queries of one (sequence s, kv head kv) are numbered qi = r * G + j
+  // for window row r and q-head kv * G + j (G = H / Hkv heads share the kv
+  // head); a workgroup takes AQ consecutive qi, so every K/V tile it stages
+  // serves all G heads of the rows it covers.
+  // Items u = ((s * Hkv + kv) * kv_splits + split) * nqt + qt: the nqt query
+  // tiles that read the same keys are neighbours, so they share one XCD's L2.
+  const int G = H / Hkv;
+  const int items = b * Hkv * kv_splits * nqt;
+  const int u = xcd_item(blockIdx.x, items);
+  if (u >= items) return;
+  const int qt = u % nqt, split = (u / nqt) % kv_splits;
+  const int kv = (u / (nqt * kv_splits)) % Hkv, s = u / (nqt * kv_splits * Hkv);
   const int W = seq_win_len[s];
-  if (qt * AQ >= W) return;
-  const int row0 = seq_row_start[s] + qt * AQ;
-  const int nrows = min(AQ, W - qt * AQ);
-  const int pos0 = seq_win_start[s] + qt * AQ;
-  const int kend = ((pos0 + nrows - 1) / B + 1) * B;        // keys [0, kend)
+  const int QG = G * W;
+  if (qt * AQ >= QG) return;
+  const int row_start = seq_row_start[s], win_start = seq_win_start[s];
+  const int qlast = min(qt * AQ + AQ, QG) - 1;
+  const int kend = ((win_start + qlast / G) / B + 1) * B;   // keys [0, kend): the last row's bound
   // this split's key tiles: a contiguous, tile-aligned share of [0, kend)
   const int ntiles_all = (kend + AK - 1) / AK;
   const int per = (ntiles_all + kv_splits - 1) / kv_splits;
   const int t_lo = split * per, t_hi = min(ntiles_all, t_lo + per);
-  const int kv = h / (H / Hkv);
   const bf16_t* Kp = Kc + ((size_t)s * Hkv + kv) * (size_t)maxpos * HD;
   const bf16_t* Vp = Vt + ((size_t)s * Hkv + kv) * (size_t)HD * vstride;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int q = wave * 16 + c;                                // query row in tile
-  const bool qvalid = q < nrows;
-  const int qpos = pos0 + q;
-  const int qend = ((qpos / B) + 1) * B;                      // this query's key bound
+  const int qi = qt * AQ + wave * 16 + c;                    // this lane's query
+  const bool qvalid = qi < QG;
+  const bool wave_on = qt * AQ + wave * 16 < QG;             // the wave holds a query
+  const int qrow = row_start + (qvalid ? qi / G : 0);        // its row in the step
+  const int h = kv * G + (qvalid ? qi % G : 0);              // its q-head
+  const int qend = ((win_start + (qvalid ? qi / G : 0)) / B + 1) * B;   // its key bound
 
   // Q^T fragments (B operand of S^T = K Q^T): dims [32 kc + 8 g, +8) of query c,
   // hi and lo halves.
@@ -82,7 +98,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
 #pragma unroll
   for (int kc = 0; kc < HD / 32; ++kc) {
     if (qvalid) {
-      const bf16_t* qp = Q + ((size_t)(row0 + q) * H + h) * HD + kc * 32 + g * 8;
+      const bf16_t* qp = Q + ((size_t)qrow * H + h) * HD + kc * 32 + g * 8;
       qh[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)qp);
       ql[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + q_plane));
     } else {
@@ -104,7 +120,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
 #define BD_FETCH(K0)                                                            \
   do {                                                                          \
     _Pragma("unroll") for (int it = 0; it < NCH; ++it) {                        \
-      const int ci = tid + 256 * it;                                            \
+      const int ci = tid + NT * it;                                             \
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;                  \
       pkh[it] = pkl[it] = u32x4{0u, 0u, 0u, 0u};                                \
       if ((K0) + key < kend) {                                                  \
@@ -124,7 +140,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
     // stage K (row-major) and V^T
 #pragma unroll
     for (int it = 0; it < NCH; ++it) {
-      const int ci = tid + 256 * it;
+      const int ci = tid + NT * it;
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;
       *(u32x4*)(sKh + key * KP + dc) = pkh[it];
       *(u32x4*)(sKl + key * KP + dc) = pkl[it];
@@ -134,6 +150,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
     }
     __syncthreads();
     if (kt + 1 < t_hi) BD_FETCH(k0 + AK);
+    if (wave_on) {
 
     // S^T sub-tiles (keys st*16 + 4g + r, query c): Kh.Qh + Kh.Ql + Kl.Qh
     float sv[4][4];
@@ -213,6 +230,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
         oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl, ph[kc], oacc[t], 0, 0, 0);
       }
     }
+    }  // wave_on
     __syncthreads();
   }
 #undef BD_FETCH
@@ -222,7 +240,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
   if (!qvalid) return;
   if (kv_splits == 1) {
     const float inv = 1.0f / l;
-    bf16_t* orow = O + (size_t)(row0 + q) * H * HD + h * HD;
+    bf16_t* orow = O + (size_t)qrow * H * HD + h * HD;
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t) {
       // O^T tile t: lane holds dims t*16 + 4g + r of query c; stored as the
@@ -241,7 +259,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const bf16_t* __restrict__ Q,
     }
   } else {
     // unnormalised partial of this key split, merged by k_attn_merge
-    const size_t base = ((size_t)split * rows_cap + row0 + q) * H + h;
+    const size_t base = ((size_t)split * rows_cap + qrow) * H + h;
     float* orow = ws_o + base * HD;
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t)
@@ -332,12 +350,17 @@ __global__ __launch_bounds__(256) void k_attn_f32(const float* __restrict__ Q,
   for (int e = 0; e < per; ++e) o[lane * per + e] = acc[e] / l;
 }
 
-int attention_splits(int b, int win_cap, int H, int hd, int maxpos) {
-  const int wgs = ((win_cap + AQ - 1) / AQ) * H * b;
-  // the query-tile kernel keeps 3 (hd 64) or 2 (hd 128) workgroups per CU
-  // resident: split the key range until the grid fills one resident round of
-  // 256 CUs, while every split keeps >= 2 key tiles of the longest range
-  const int round = (hd == 64 ? 3 : 2) * 256;
+// waves per workgroup for a window of win_cap rows (see k_attn_bf16)
+static int attention_waves(int win_cap, int H, int Hkv) { return (H / Hkv) * win_cap <= 32 ? 2 : 4; }
+
+int attention_splits(int b, int win_cap, int H, int Hkv, int hd, int maxpos) {
+  const int nw = attention_waves(win_cap, H, Hkv);
+  const int wgs = (((H / Hkv) * win_cap + 16 * nw - 1) / (16 * nw)) * Hkv * b;
+  // workgroups resident per CU (LDS-bound: 37 KB per workgroup at hd 64,
+  // 72 KB at hd 128; 3 of the 4-wave hd-64 kind): split the key range until
+  // the grid fills one resident round of 256 CUs, while every split keeps
+  // >= 2 key tiles of the longest range
+  const int round = (hd == 64 ? (nw == 2 ? 4 : 3) : 2) * 256;
   int splits = 1;
   while (wgs * (splits + 1) <= round && maxpos / (AK * (splits + 1)) >= 2 && splits < 16) ++splits;
   return splits;
@@ -355,17 +378,20 @@ hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const K
     const bf16_t* k = (const bf16_t*)kv.K;
     const bf16_t* v = (const bf16_t*)kv.V;
     if (kv_splits < 1 || (kv_splits > 1 && (!ws_o || !ws_ml))) return hipErrorInvalidValue;
-    dim3 grid((win_cap + AQ - 1) / AQ, H, b * kv_splits);
-    if (hd == 128)
-      k_attn_bf16<128><<<grid, 256, 0, st>>>(q, q_plane, k, kv.k_plane, v, kv.v_plane, kv.vstride,
-                                             (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
-                                             plan.seq_win_start, H, Hkv, kv.maxpos, B, scale_log2,
-                                             kv_splits, ws_o, ws_ml, rows_cap);
-    else
-      k_attn_bf16<64><<<grid, 256, 0, st>>>(q, q_plane, k, kv.k_plane, v, kv.v_plane, kv.vstride,
-                                            (bf16_t*)O, o_plane, plan.seq_row_start, plan.seq_win_len,
-                                            plan.seq_win_start, H, Hkv, kv.maxpos, B, scale_log2,
-                                            kv_splits, ws_o, ws_ml, rows_cap);
+    const int nw = attention_waves(win_cap, H, Hkv);
+    const int nqt = ((H / Hkv) * win_cap + 16 * nw - 1) / (16 * nw);
+    const int grid = b * Hkv * kv_splits * nqt + 7;
+#define BD_ATTN(HD_, NW_)                                                                     \
+  k_attn_bf16<HD_, NW_><<<grid, 64 * NW_, 0, st>>>(                                           \
+      q, q_plane, k, kv.k_plane, v, kv.v_plane, kv.vstride, (bf16_t*)O, o_plane,              \
+      plan.seq_row_start, plan.seq_win_len, plan.seq_win_start, H, Hkv, kv.maxpos, B,         \
+      scale_log2, kv_splits, ws_o, ws_ml, rows_cap, b, nqt)
+    if (hd == 128) {
+      if (nw == 2) BD_ATTN(128, 2); else BD_ATTN(128, 4);
+    } else {
+      if (nw == 2) BD_ATTN(64, 2); else BD_ATTN(64, 4);
+    }
+#undef BD_ATTN
     if (kv_splits > 1) {
       const int items_per_block = 256 / (hd / 4);
       k_attn_merge<<<(rows_cap * H + items_per_block - 1) / items_per_block, 256, 0, st>>>(

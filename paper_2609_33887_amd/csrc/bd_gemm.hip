@@ -56,17 +56,6 @@ constexpr int SK = 32;       // K per pipeline stage (KALIGN = 4 stages)
 
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
 
-// Work item of a GEMM workgroup.  Launches are 1-D with at least items + 7
-// workgroups; the dispatcher deals consecutive workgroups to the 8 XCDs in
-// turn, and item u = (id % 8) * ceil(items / 8) + id / 8 gives each XCD a
-// contiguous range of items (items are numbered so that neighbours share
-// operand tiles), which then stay in that XCD's L2.  Workgroups with
-// id >= 8 ceil(items / 8), and those whose u >= items, get u = items (none).
-__device__ __forceinline__ int xcd_item(int id, int items) {
-  const int per = (items + 7) / 8;
-  return id < 8 * per ? (id % 8) * per + id / 8 : items;
-}
-
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 template <int BM, int BN>

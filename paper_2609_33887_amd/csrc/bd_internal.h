@@ -170,6 +170,17 @@ hipError_t launch_lm_logits(bool is_bf16, const void* A, int d, size_t a_plane, 
                             int mask_id, float scale, const int32_t* M_dev, int rows_cap,
                             float* logits, hipStream_t st);
 
+// Work item of a workgroup in an XCD-aware launch.  Launches are 1-D with at
+// least items + 7 workgroups; the dispatcher deals consecutive workgroups to
+// the 8 XCDs in turn, and item u = (id % 8) * ceil(items / 8) + id / 8 gives
+// each XCD a contiguous range of items (items are numbered so that neighbours
+// share operand tiles), which then stay in that XCD's L2.  Workgroups with
+// id >= 8 ceil(items / 8), and those whose u >= items, get u = items (none).
+__device__ __forceinline__ int xcd_item(int id, int items) {
+  const int per = (items + 7) / 8;
+  return id < 8 * per ? (id % 8) * per + id / 8 : items;
+}
+
 // One layer's KV cache.  K: [seq][kv head][pos][hd].  V: bf16 models keep
 // it transposed in tiles of 64 keys, [seq][kv head][pos / 64][hd][64]: a
 // tile is one contiguous block per plane (DRAM page locality when streamed)
@@ -190,8 +201,9 @@ struct KvView {
   int maxpos, vstride;
 };
 
-// Attention of the rows of `plan` over the cache.  bf16 models: 64-query
-// tiles of one head, 64-key tiles staged in LDS; kv_splits > 1 splits every
+// Attention of the rows of `plan` over the cache.  bf16 models: tiles of 64
+// queries of one (sequence, kv head) (window rows x the q-heads sharing the kv
+// head), 64-key tiles staged in LDS; kv_splits > 1 splits every
 // query tile's key range into that many workgroups (partials in ws_o
 // [splits][rows_cap][H][hd], ws_ml [splits][rows_cap][H][2]) merged in split
 // order.  O: bf16 plane pair (lo at O + o_plane elements) for bf16 models,
@@ -200,7 +212,7 @@ hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const K
                             size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
                             int hd, int B, int kv_splits, float* ws_o, float* ws_ml, int rows_cap,
                             hipStream_t st);
-int attention_splits(int b, int win_cap, int H, int hd, int maxpos);
+int attention_splits(int b, int win_cap, int H, int Hkv, int hd, int maxpos);
 
 hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
                         int vocab, PlanView plan, int rows_cap, float* X, int32_t* err_flag,
