@@ -226,6 +226,96 @@ bd_status rl_risk_select(int32_t n, int32_t m, int32_t ref_index, const uint8_t*
                          double* p_out, uint8_t* valid_out, int32_t* selected_out,
                          int32_t* near_ties_out);
 
+/*
+ * Multiple-testing procedures (App. A.3 and the baselines of App. D); valid
+ * means the null R(lambda) > alpha is rejected.
+ *  RL_HOLM            Holm step-down at family-wise level delta (primary).
+ *  RL_BONFERRONI      p <= delta / m.
+ *  RL_FIXED_SEQUENCE  walk a caller-given, data-independent order, testing
+ *                     each configuration at full delta until the first failure.
+ *  RL_UNCORRECTED     p <= delta for each configuration (no multiplicity
+ *                     correction).
+ *  RL_PLUGIN          V / n <= alpha, formed and compared in double precision
+ *                     (no finite-sample margin).
+ */
+#define RL_HOLM 0
+#define RL_BONFERRONI 1
+#define RL_FIXED_SEQUENCE 2
+#define RL_UNCORRECTED 3
+#define RL_PLUGIN 4
+
+/*
+ * rl_select -- rl_risk_select with a choice of procedure and of prompts.
+ *  method: one of RL_*.  order: [m], a permutation of 0..m-1, read only for
+ *  RL_FIXED_SEQUENCE (may be NULL otherwise).  prompt_mask: [n] uint8 or
+ *  NULL; when given, only the prompts with a non-zero entry are counted and
+ *  the p-values use their number n_cal in place of n.  Other arguments and
+ *  outputs as rl_risk_select (V_out, p_out, valid_out may be NULL).
+ *  Host-only.  Errors: BD_EINVAL for the argument errors of rl_risk_select,
+ *  an unknown method, a missing or non-permutation order under
+ *  RL_FIXED_SEQUENCE, or a mask that selects no prompt.
+ */
+bd_status rl_select(int32_t n, int32_t m, int32_t ref_index, const uint8_t* correct,
+                    const uint8_t* prompt_mask, const double* cost, double alpha, double delta,
+                    int32_t method, const int32_t* order, int32_t* V_out, double* p_out,
+                    uint8_t* valid_out, int32_t* selected_out);
+
+/*
+ * rl_alpha_sweep -- selection at each budget of a grid (App. A.6).
+ *  alphas: [n_alpha] budgets, each in (0, 1), any order.  selected_out
+ *  [n_alpha] receives the deployed index at alphas[k]; n_valid_out [n_alpha]
+ *  (may be NULL) the number of valid configurations there.  alpha_hat_out
+ *  (may be NULL): the smallest budget of the grid at which some valid
+ *  configuration has cost > cost[ref_index] (alpha_hat), NaN if none has.
+ *  Host-only.  Errors: BD_EINVAL as rl_select for any budget, n_alpha < 1 or
+ *  NULL alphas / selected_out.
+ */
+bd_status rl_alpha_sweep(int32_t n, int32_t m, int32_t ref_index, const uint8_t* correct,
+                         const double* cost, const double* alphas, int32_t n_alpha, double delta,
+                         int32_t method, const int32_t* order, int32_t* selected_out,
+                         int32_t* n_valid_out, double* alpha_hat_out);
+
+/*
+ * rl_split_exceedance -- held-out validity over calibration/test splits
+ * (§5 "Redline and the mean-accuracy rule", App. D).
+ *  cal_masks: [n_splits][n] uint8, non-zero = calibration prompt of that
+ *  split; every split needs at least one prompt on each side.  For split s
+ *  the procedure selects on the calibration prompts; risks are then
+ *  R_test(j) = V_j(test prompts) / n_test and R_pool(j) = V_j(all) / n, in
+ *  double precision.  deployed_out [n_splits] (may be NULL): the deployed
+ *  index; test_viol_out [n_splits] (may be NULL): its violations on the test
+ *  prompts.  counts_out [4] (may be NULL): the number of splits whose
+ *  deployed configuration has R_test > alpha, has R_pool > alpha, whose
+ *  valid set holds a configuration with R_test > alpha, with R_pool > alpha.
+ *  gain_sum_out (may be NULL): the sum over splits, in split order, of
+ *  cost[deployed] / cost[ref_index] - 1.  Splits run on host threads; the
+ *  results do not depend on their number.  Host-only.  Errors: BD_EINVAL as
+ *  rl_select, n_splits < 1, NULL cal_masks or a one-sided split.
+ */
+bd_status rl_split_exceedance(int32_t n, int32_t m, int32_t ref_index, const uint8_t* correct,
+                              const double* cost, double alpha, double delta, int32_t method,
+                              const int32_t* order, int32_t n_splits, const uint8_t* cal_masks,
+                              int32_t* deployed_out, int32_t* test_viol_out, int32_t* counts_out,
+                              double* gain_sum_out);
+
+/*
+ * rl_monte_carlo -- the synthetic check with known risks (App. A.7).
+ *  true_risk: [m].  u: [trials][k][n] float64 uniforms, k = 1 (one uniform
+ *  per prompt shared by every configuration) or k = m (independent draws).
+ *  In trial t configuration j loses prompt i when
+ *  u[t][k == 1 ? 0 : j][i] < true_risk[j], and V_j is its number of losses;
+ *  the p-values and the procedure are those of rl_select.
+ *  false_trials_out: the trials in which some configuration with
+ *  true_risk > alpha is valid (family-wise errors).  valid_counts_out [m]
+ *  (may be NULL): per configuration, the trials in which it is valid.
+ *  Trials run on host threads.  Host-only.  Errors: BD_EINVAL for n, m < 1,
+ *  trials < 1, k not 1 or m, NULL inputs, or alpha, delta, method, order as
+ *  rl_select.
+ */
+bd_status rl_monte_carlo(int32_t n, int32_t m, const double* true_risk, double alpha, double delta,
+                         int32_t method, const int32_t* order, int32_t trials, int32_t k,
+                         const double* u, int32_t* false_trials_out, int32_t* valid_counts_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,7 +20,9 @@ BD_F32, BD_BF16 = 0, 1
 
 EXPORTED = ["bd_init_model", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
             "bd_decode", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
-            "bd_profile_read", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select"]
+            "bd_profile_read", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select",
+            "rl_select", "rl_alpha_sweep", "rl_split_exceedance", "rl_monte_carlo"]
+RL_METHODS = {"holm": 0, "bonferroni": 1, "fixed_sequence": 2, "uncorrected": 3, "plugin": 4}
 PROF_KINDS = ["embed", "norm", "gemm_qkv", "rope", "attn", "gemm_o", "gemm_gu", "gemm_down", "lm_head",
               "commit", "moe_route"]
 
@@ -67,6 +69,16 @@ def _load():
         "bd_model_free": [VP],
         "rl_risk_select": [I32, I32, I32, P(ctypes.c_uint8), P(ctypes.c_double), ctypes.c_double,
                            ctypes.c_double, P(I32), P(ctypes.c_double), P(ctypes.c_uint8), P(I32), P(I32)],
+        "rl_select": [I32, I32, I32, P(ctypes.c_uint8), P(ctypes.c_uint8), P(ctypes.c_double),
+                      ctypes.c_double, ctypes.c_double, I32, P(I32), P(I32), P(ctypes.c_double),
+                      P(ctypes.c_uint8), P(I32)],
+        "rl_alpha_sweep": [I32, I32, I32, P(ctypes.c_uint8), P(ctypes.c_double), P(ctypes.c_double), I32,
+                           ctypes.c_double, I32, P(I32), P(I32), P(I32), P(ctypes.c_double)],
+        "rl_split_exceedance": [I32, I32, I32, P(ctypes.c_uint8), P(ctypes.c_double), ctypes.c_double,
+                                ctypes.c_double, I32, P(I32), I32, P(ctypes.c_uint8), P(I32), P(I32),
+                                P(I32), P(ctypes.c_double)],
+        "rl_monte_carlo": [I32, I32, P(ctypes.c_double), ctypes.c_double, ctypes.c_double, I32, P(I32),
+                           I32, I32, P(ctypes.c_double), P(I32), P(I32)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -178,6 +190,95 @@ def rl_risk_select(correct, cost, ref_index: int, alpha: float, delta: float):
                               V.ctypes.data_as(i32), p.ctypes.data_as(f64), valid.ctypes.data_as(u8),
                               ctypes.byref(sel), ctypes.byref(near)))
     return V, p, valid.astype(bool), sel.value, near.value
+
+
+_u8, _f64, _i32 = ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)
+
+
+def _method_order(method: str, order, m: int):
+    import numpy as np
+    code = RL_METHODS[method]
+    o = None if order is None else np.ascontiguousarray(order, dtype=np.int32)
+    if o is not None and o.shape != (m,):
+        raise ValueError("order must hold m entries")
+    return code, o, (None if o is None else o.ctypes.data_as(_i32))
+
+
+def rl_select(correct, cost, ref_index: int, alpha: float, delta: float, method: str = "holm",
+              order=None, mask=None):
+    """Returns (V int32[m], p float64[m], valid bool[m], selected)."""
+    import numpy as np
+    c = np.ascontiguousarray(correct, dtype=np.uint8)
+    m, n = c.shape
+    k = np.ascontiguousarray(cost, dtype=np.float64)
+    code, o, op = _method_order(method, order, m)
+    mk = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    V = np.zeros(m, dtype=np.int32)
+    p = np.zeros(m, dtype=np.float64)
+    valid = np.zeros(m, dtype=np.uint8)
+    sel = ctypes.c_int32(-1)
+    _check(lib.rl_select(n, m, ref_index, c.ctypes.data_as(_u8), None if mk is None else mk.ctypes.data_as(_u8),
+                         k.ctypes.data_as(_f64), alpha, delta, code, op, V.ctypes.data_as(_i32),
+                         p.ctypes.data_as(_f64), valid.ctypes.data_as(_u8), ctypes.byref(sel)))
+    return V, p, valid.astype(bool), sel.value
+
+
+def rl_alpha_sweep(correct, cost, ref_index: int, alphas, delta: float, method: str = "holm", order=None):
+    """Returns (selected int32[n_alpha], n_valid int32[n_alpha], alpha_hat or None)."""
+    import math
+    import numpy as np
+    c = np.ascontiguousarray(correct, dtype=np.uint8)
+    m, n = c.shape
+    k = np.ascontiguousarray(cost, dtype=np.float64)
+    a = np.ascontiguousarray(alphas, dtype=np.float64)
+    code, o, op = _method_order(method, order, m)
+    sel = np.zeros(len(a), dtype=np.int32)
+    nval = np.zeros(len(a), dtype=np.int32)
+    hat = ctypes.c_double(0.0)
+    _check(lib.rl_alpha_sweep(n, m, ref_index, c.ctypes.data_as(_u8), k.ctypes.data_as(_f64),
+                              a.ctypes.data_as(_f64), len(a), delta, code, op, sel.ctypes.data_as(_i32),
+                              nval.ctypes.data_as(_i32), ctypes.byref(hat)))
+    return sel, nval, (None if math.isnan(hat.value) else hat.value)
+
+
+def rl_split_exceedance(correct, cost, ref_index: int, alpha: float, delta: float, cal_masks,
+                        method: str = "holm", order=None):
+    """Returns (deployed int32[S], test_violations int32[S], counts int32[4], gain_sum);
+    counts = (exceed_test, exceed_pooled, fwer_test, fwer_pooled)."""
+    import numpy as np
+    c = np.ascontiguousarray(correct, dtype=np.uint8)
+    m, n = c.shape
+    k = np.ascontiguousarray(cost, dtype=np.float64)
+    masks = np.ascontiguousarray(cal_masks, dtype=np.uint8)
+    if masks.ndim != 2 or masks.shape[1] != n:
+        raise ValueError("cal_masks must be [n_splits][n]")
+    S = masks.shape[0]
+    code, o, op = _method_order(method, order, m)
+    dep = np.zeros(S, dtype=np.int32)
+    tv = np.zeros(S, dtype=np.int32)
+    counts = np.zeros(4, dtype=np.int32)
+    gain = ctypes.c_double(0.0)
+    _check(lib.rl_split_exceedance(n, m, ref_index, c.ctypes.data_as(_u8), k.ctypes.data_as(_f64), alpha,
+                                   delta, code, op, S, masks.ctypes.data_as(_u8), dep.ctypes.data_as(_i32),
+                                   tv.ctypes.data_as(_i32), counts.ctypes.data_as(_i32), ctypes.byref(gain)))
+    return dep, tv, counts, gain.value
+
+
+def rl_monte_carlo(true_risk, alpha: float, delta: float, u, method: str = "holm", order=None):
+    """u: float64 [trials][1 or m][n].  Returns (false_trials, valid_counts int32[m])."""
+    import numpy as np
+    r = np.ascontiguousarray(true_risk, dtype=np.float64)
+    m = r.shape[0]
+    uu = np.ascontiguousarray(u, dtype=np.float64)
+    if uu.ndim != 3:
+        raise ValueError("u must be [trials][k][n]")
+    trials, kk, n = uu.shape
+    code, o, op = _method_order(method, order, m)
+    ft = ctypes.c_int32(0)
+    counts = np.zeros(m, dtype=np.int32)
+    _check(lib.rl_monte_carlo(n, m, r.ctypes.data_as(_f64), alpha, delta, code, op, trials, kk,
+                              uu.ctypes.data_as(_f64), ctypes.byref(ft), counts.ctypes.data_as(_i32)))
+    return ft.value, counts
 
 
 # ---------------------------------------------------------------- torch helpers

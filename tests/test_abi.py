@@ -95,3 +95,130 @@ def test_redline_nothing_valid_deploys_reference():
     correct[0] = 0                       # reference wrong everywhere: no violations anywhere
     V, p, valid, sel, _ = bd.rl_risk_select(correct, [1.0, 5.0, 9.0], 0, 0.1, 0.1)
     assert V.tolist() == [0, 0, 0] and sel == 2
+
+
+# ---- Redline variants and validity harness: library against the oracle ----
+
+def _no_near_ties(p_oracle, delta, m):
+    """True when no oracle p-value sits within 1e-9 (relative) of any
+    threshold a procedure can compare it with."""
+    thr = [delta / k for k in range(1, m + 1)]
+    return all(abs(float(p) / t - 1.0) >= 1e-9 for p in p_oracle for t in thr)
+
+
+def _planted_cases(seed, count):
+    import bd_synth
+    rng = np.random.default_rng(seed)
+    for case in range(count):
+        m = int(rng.integers(1, 12))
+        n = int(rng.integers(30, 700))
+        ref = int(rng.integers(0, m))
+        risks = list(rng.uniform(0.0, 0.25, size=m))
+        c = bd_synth.planted_correctness(n, risks, ref, seed=seed * 1000 + case, shared=bool(case % 2))
+        cost = list(rng.choice([1.0, 2.0, 3.0, 4.5], size=m))
+        order = list(rng.permutation(m))
+        yield m, n, ref, c, cost, order, rng
+
+
+@pytest.mark.parametrize("method", ["holm", "bonferroni", "fixed_sequence", "uncorrected", "plugin"])
+def test_rl_select_matches_oracle(method):
+    from paper_2609_33887_amd import bd
+    from oracle import redline as rl
+    for m, n, ref, c, cost, order, rng in _planted_cases(21, 40):
+        alpha = float(rng.choice([0.05, 0.1, 0.15, 0.2]))
+        delta = float(rng.choice([0.05, 0.1]))
+        mask = (rng.random(n) < 0.6).astype(np.uint8) if rng.random() < 0.5 else None
+        if mask is not None and mask.sum() == 0:
+            mask[0] = 1
+        V, p, valid, sel = bd.rl_select(c, cost, ref, alpha, delta, method, order, mask)
+        o = rl.select(c, cost, ref, alpha, delta, method, order, mask)
+        assert V.tolist() == o.V.tolist()
+        for a, b in zip(p, o.p):
+            assert abs(a - float(b)) <= 1e-11 * float(b) + 1e-300
+        if method == "plugin" or _no_near_ties(o.p, delta, m):
+            assert valid.tolist() == o.valid.tolist() and sel == o.selected
+
+
+def test_rl_select_holm_equals_rl_risk_select():
+    from paper_2609_33887_amd import bd
+    for m, n, ref, c, cost, order, rng in _planted_cases(22, 20):
+        a = bd.rl_risk_select(c, cost, ref, 0.1, 0.1)
+        b = bd.rl_select(c, cost, ref, 0.1, 0.1, "holm")
+        assert a[0].tolist() == b[0].tolist() and a[1].tolist() == b[1].tolist()
+        assert a[2].tolist() == b[2].tolist() and a[3] == b[3]
+
+
+def test_rl_alpha_sweep_matches_oracle_and_unlock_table():
+    from paper_2609_33887_amd import bd
+    from oracle import redline as rl
+    from tests.test_oracle_redline import load, ref_index
+    alphas = [i / 100 for i in range(1, 31)]
+    for u in load("unlock"):
+        rows = load(u["grid"])
+        n = int(rows[0]["n"])
+        c = np.ones((len(rows), n), dtype=np.uint8)
+        for j, r in enumerate(rows):
+            c[j, :int(r["k"])] = 0
+        tpf = [float(r["tpf"]) for r in rows]
+        for method in ("holm", "bonferroni"):
+            sel, nval, hat = bd.rl_alpha_sweep(c, tpf, ref_index(rows), alphas[::-1], 0.10, method)
+            osel, onval, ohat = rl.alpha_sweep(c, tpf, ref_index(rows), alphas[::-1], 0.10, method)
+            assert sel.tolist() == osel and nval.tolist() == onval and hat == ohat
+        _, _, hat = bd.rl_alpha_sweep(c, tpf, ref_index(rows), alphas, 0.10)
+        assert hat == pytest.approx(float(u["alpha_min"]))
+    # no configuration faster than the reference: alpha_hat is undefined
+    c = np.ones((2, 50), dtype=np.uint8)
+    _, _, hat = bd.rl_alpha_sweep(c, [3.0, 1.0], 0, alphas, 0.10)
+    assert hat is None
+
+
+@pytest.mark.parametrize("method", ["holm", "bonferroni", "fixed_sequence", "uncorrected", "plugin"])
+def test_rl_split_exceedance_matches_oracle(method):
+    import bd_synth
+    from paper_2609_33887_amd import bd
+    from oracle import redline as rl
+    for case, (m, n, ref, c, cost, order, rng) in enumerate(_planted_cases(23, 6)):
+        masks = bd_synth.split_masks(n, 150, cal_frac=float(rng.choice([0.3, 0.5, 0.7])), seed=case)
+        alpha = float(rng.choice([0.05, 0.1, 0.15]))
+        dep, tv, counts, gain = bd.rl_split_exceedance(c, cost, ref, alpha, 0.1, masks, method, order)
+        o = rl.split_exceedance(c, cost, ref, alpha, 0.1, masks, method, order)
+        assert dep.tolist() == o.deployed and tv.tolist() == o.test_violations
+        assert counts.tolist() == [o.exceed_test, o.exceed_pooled, o.fwer_test, o.fwer_pooled]
+        assert gain == o.gain_sum
+
+
+@pytest.mark.parametrize("shared", [True, False])
+@pytest.mark.parametrize("method", ["holm", "bonferroni", "fixed_sequence", "uncorrected", "plugin"])
+def test_rl_monte_carlo_matches_oracle(method, shared):
+    import bd_synth
+    from paper_2609_33887_amd import bd
+    from oracle import redline as rl
+    risks = [0.01, 0.02, 0.07, 0.07, 0.07]             # App. A.7's configurations
+    u = bd_synth.mc_uniforms(300, 1 if shared else len(risks), 800, seed=8)
+    order = [0, 1, 2, 3, 4]
+    ft, counts = bd.rl_monte_carlo(risks, 0.05, 0.10, u, method, order)
+    oft, ocounts = rl.monte_carlo(risks, 0.05, 0.10, u, method, order)
+    assert ft == oft and counts.tolist() == ocounts.tolist()
+
+
+def test_redline_variants_reject_bad_arguments():
+    from paper_2609_33887_amd import bd
+    c = np.ones((3, 20), dtype=np.uint8)
+    cost = [1.0, 2.0, 3.0]
+    bad = [
+        lambda: bd.rl_select(c, cost, 0, 0.1, 0.1, "fixed_sequence", None),          # no order
+        lambda: bd.rl_select(c, cost, 0, 0.1, 0.1, "fixed_sequence", [0, 0, 1]),     # not a permutation
+        lambda: bd.rl_select(c, cost, 0, 0.1, 0.1, "holm", None, np.zeros(20)),      # empty prompt set
+        lambda: bd.rl_alpha_sweep(c, cost, 0, [0.1, 1.0], 0.1),                      # budget out of range
+        lambda: bd.rl_split_exceedance(c, cost, 0, 0.1, 0.1, np.ones((2, 20))),      # no test prompts
+        lambda: bd.rl_monte_carlo([0.1, 0.2, 0.3], 0.1, 0.1, np.zeros((4, 2, 20))),  # k neither 1 nor m
+    ]
+    for f in bad:
+        with pytest.raises(bd.BDError) as e:
+            f()
+        assert e.value.status == bd.BD_EINVAL
+        assert bd.bd_last_error().startswith("rl_")
+    code = bd.lib.rl_select(20, 3, 0, c.ctypes.data_as(bd._u8), None,
+                            np.asarray(cost).ctypes.data_as(bd._f64), 0.1, 0.1, 7, None, None, None, None,
+                            bd.ctypes.byref(bd.ctypes.c_int32()))
+    assert code == bd.BD_EINVAL and "unknown procedure" in bd.bd_last_error()
