@@ -17,8 +17,23 @@ the engine description of the paper:
 * One-step cache write (App. G.2): a committed block's K/V are recomputed
   from its clean tokens in the next forward, where its rows ride along in
   front of the active blocks; after that forward it is cached.
-* Admission: with no admission threshold, freed slots are refilled at the end
-  of the step until ``n_inflight`` blocks are active (reading of App. G).
+* Admission (App. G: the admission threshold turns a placeholder into an
+  active block): at the end of a step, and after the prefill, placeholders
+  are admitted in order while fewer than ``n_inflight`` blocks are active and
+  either no block is active or the youngest active block has resolved a
+  fraction >= ``tau_add`` of its positions.  ``tau_add <= 0`` refills every
+  free slot at once.
+* Semi-completion (App. G: the accept and semi-completion thresholds decide
+  which positions an active block resolves): with ``tau_semi`` given, an
+  active block whose predecessor is still active and has resolved a fraction
+  < ``tau_semi`` of its positions is semi-activated and commits only positions
+  with confidence >= ``tau``; every other active block is fully activated and,
+  when none of its masked positions clears ``tau``, commits its single most
+  confident one.  Later blocks thus start committing at the engine's pace once
+  the predecessor's top-1 context is mostly in place, before it is cached.
+  Without ``tau_semi`` the forced commit is one per sequence, over all active
+  blocks (the base rule above).  Resolved fractions are float32 ratios
+  compared with float32 thresholds.
 * TPF (§2.1): tokens committed per model forward; a forward is a step in
   which the sequence has at least one active block.  Prefill is not counted
   (App. G.1).
@@ -34,7 +49,32 @@ from .model import OracleModel, lm_stats
 
 PLACEHOLDER, ACTIVE, PENDING, CACHED = 0, 1, 2, 3
 
-__all__ = ["SeqDecoder", "commit_set", "decode_batch", "PLACEHOLDER", "ACTIVE", "PENDING", "CACHED"]
+__all__ = ["SeqDecoder", "commit_set", "commit_set_semi", "frac_at_least", "decode_batch", "PLACEHOLDER", "ACTIVE", "PENDING", "CACHED"]
+
+
+def frac_at_least(resolved: int, B: int, thr: float) -> bool:
+    """resolved / B >= thr, as a float32 division and comparison."""
+    return bool(np.float32(resolved) / np.float32(B) >= np.float32(thr))
+
+
+def commit_set_semi(conf: np.ndarray, block: np.ndarray, resolved, B: int, tau: float,
+                    tau_semi: float):
+    """Semi-completion commit rule.  ``block[i]`` is the index (0 = oldest
+    active) of the block holding masked position i; ``resolved[k]`` is active
+    block k's resolved count before this step.  Returns (commit mask, list of
+    the index arrays of the blocks that took a forced commit)."""
+    t = float(np.float32(tau))
+    s = conf >= t
+    forced = []
+    for k in range(len(resolved)):
+        idx = np.nonzero(block == k)[0]
+        if idx.size == 0:
+            continue
+        full = k == 0 or frac_at_least(int(resolved[k - 1]), B, tau_semi)
+        if full and not s[idx].any():
+            s[idx[int(np.argmax(conf[idx]))]] = True   # first maximum = lowest position
+            forced.append(idx)
+    return s, forced
 
 
 def commit_set(conf: np.ndarray, tau: float) -> np.ndarray:
@@ -63,11 +103,12 @@ class SeqDecoder:
     positions in ``G // B`` blocks, at most ``n_inflight`` active blocks."""
 
     def __init__(self, model: OracleModel, prompt: np.ndarray, G: int, B: int, n_inflight: int,
-                 tau: float):
+                 tau: float, tau_semi: Optional[float] = None, tau_add: float = 0.0):
         P = len(prompt)
         if B < 1 or n_inflight < 1 or P % B or G % B:
             raise ValueError("need B >= 1, n_inflight >= 1, P % B == 0 and G % B == 0")
         self.model, self.P, self.G, self.B, self.nb, self.tau = model, P, G, B, n_inflight, tau
+        self.tau_semi, self.tau_add = tau_semi, tau_add
         self.mask_id = model.mask_id
         self.tokens = np.concatenate([np.asarray(prompt, dtype=np.int64),
                                       np.full(G, self.mask_id, dtype=np.int64)])
@@ -80,10 +121,18 @@ class SeqDecoder:
         self.keep_records = False
 
     # -- slots --------------------------------------------------------------
+    def resolved(self, b: int) -> int:
+        """Unmasked positions of generation block b."""
+        lo = self.P + b * self.B
+        return int(np.count_nonzero(self.tokens[lo:lo + self.B] != self.mask_id))
+
     def _admit(self):
         while np.count_nonzero(self.status == ACTIVE) < self.nb:
             free = np.nonzero(self.status == PLACEHOLDER)[0]
             if free.size == 0:
+                break
+            act = np.nonzero(self.status == ACTIVE)[0]
+            if act.size and not frac_at_least(self.resolved(int(act[-1])), self.B, self.tau_add):
                 break
             self.status[free[0]] = ACTIVE
 
@@ -139,9 +188,22 @@ class SeqDecoder:
         self._admit()
         self.forwards += 1
 
+    def decision(self, masked: np.ndarray, conf: np.ndarray):
+        """This step's own commit mask over ``masked`` and the index arrays of
+        the groups that took a forced commit (the whole set under the base
+        rule, single blocks under semi-completion)."""
+        if self.tau_semi is None:
+            own = commit_set(conf, self.tau)
+            forced = [] if (conf >= np.float32(self.tau)).any() else [np.arange(len(conf))]
+            return own, forced
+        act = np.nonzero(self.status == ACTIVE)[0]
+        block = (masked - self.P) // self.B - int(act[0])
+        resolved = [self.resolved(int(b)) for b in act]
+        return commit_set_semi(conf, block, resolved, self.B, self.tau, self.tau_semi)
+
     def step(self, step: int, decide: Optional[Callable] = None):
         masked, conf, tok, p2 = self.forward_step()
-        own = commit_set(conf, self.tau)
+        own, _ = self.decision(masked, conf)
         if decide is None:
             sel = own
             toks = tok[sel]
@@ -169,7 +231,8 @@ class BatchResult:
 
 def decode_batch(model: OracleModel, prompts: np.ndarray, G: int, B: int, n_inflight: int,
                  tau: float, decide: Optional[Callable] = None, max_steps: int | None = None,
-                 keep_records: bool = False) -> BatchResult:
+                 keep_records: bool = False, tau_semi: Optional[float] = None,
+                 tau_add: float = 0.0) -> BatchResult:
     """Decode independent sequences; batch rows never interact, so each runs
     its own state machine and the global step index equals its forward index
     while it is active."""
@@ -179,7 +242,7 @@ def decode_batch(model: OracleModel, prompts: np.ndarray, G: int, B: int, n_infl
     fw = np.zeros(b, dtype=np.int64)
     steps = 0
     for i in range(b):
-        d = SeqDecoder(model, prompts[i], G, B, n_inflight, tau)
+        d = SeqDecoder(model, prompts[i], G, B, n_inflight, tau, tau_semi, tau_add)
         d.keep_records = keep_records
         d.seq_index = i
         d.prefill()

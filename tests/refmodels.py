@@ -187,17 +187,35 @@ def torch_causal_logits(cfg, ws, tokens):
 
 
 # ---------------------------------------------------------------- brute decode
-def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward):
+def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward, tau_semi=None, tau_add=0.0):
     """Decode by recomputing the whole sequence every step.
 
     Block k of the generation is committed once it and all blocks before it
     hold no mask; blocks in [committed, admitted) are active; at most ``nb``
     blocks are active; a step commits every masked position of an active block
-    with confidence >= tau, or the single most confident one."""
+    with confidence >= tau, or the single most confident one.  With
+    ``tau_semi``: the single most confident position is taken per block, in
+    every active block with none above tau whose previous block is committed
+    or had at least the fraction tau_semi of its positions unmasked when the
+    step began.  A further block is admitted while fewer than nb are active
+    and either none is active or the last admitted one has at least the
+    fraction tau_add of its positions unmasked (fractions in float32)."""
     P = len(prompt)
     tokens = list(prompt) + [cfg.mask_id] * G
     nblk = G // B
-    committed, admitted = 0, min(nb, nblk)
+    f32 = np.float32
+
+    def unmasked(k):
+        return sum(1 for p in range(P + k * B, P + (k + 1) * B) if tokens[p] != cfg.mask_id)
+
+    def admit(committed, admitted):
+        while admitted < nblk and admitted - committed < nb and \
+                (admitted == committed or f32(unmasked(admitted - 1)) / f32(B) >= f32(tau_add)):
+            admitted += 1
+        return admitted
+
+    committed = 0
+    admitted = admit(0, 0)
     commit_step = [-1] * G
     steps = 0
     tau32 = float(np.float32(tau))
@@ -213,14 +231,24 @@ def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward):
             tok = min(i for i, v in enumerate(row) if v == mx)
             stats.append((1.0 / tot, tok))
         chosen = [i for i, (c, _) in enumerate(stats) if c >= tau32]
-        if not chosen:
-            best = max(c for c, _ in stats)
-            chosen = [min(i for i, (c, _) in enumerate(stats) if c == best)]
+        if tau_semi is None:
+            if not chosen:
+                best = max(c for c, _ in stats)
+                chosen = [min(i for i, (c, _) in enumerate(stats) if c == best)]
+        else:
+            done_before = {k: unmasked(k) for k in range(committed, admitted)}
+            for k in range(committed, admitted):
+                mine = [i for i, p in enumerate(cand) if (p - P) // B == k]
+                if not mine or any(i in chosen for i in mine):
+                    continue
+                if k == committed or f32(done_before[k - 1]) / f32(B) >= f32(tau_semi):
+                    best = max(stats[i][0] for i in mine)
+                    chosen.append(min(i for i in mine if stats[i][0] == best))
         for i in chosen:
             tokens[cand[i]] = stats[i][1]
             commit_step[cand[i] - P] = steps
         while committed < admitted and cfg.mask_id not in tokens[P + committed * B:P + (committed + 1) * B]:
             committed += 1
-        admitted = min(nblk, committed + nb)
+        admitted = admit(committed, admitted)
         steps += 1
     return np.array(tokens[P:]), np.array(commit_step), steps

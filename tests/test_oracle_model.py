@@ -167,6 +167,66 @@ def test_decode_matches_brute_force(P, B, nb, tau):
     assert r.forwards[0] == bsteps
 
 
+SEMI_CASES = [(P, B, nb, tau, ts, ta) for B in (2, 4) for P in range(0, 8 - B, B) for nb in (2, 3)
+              for tau in (0.5, 0.9, 2.0) for ts, ta in ((0.5, 0.0), (0.5, 0.5), (1.0, 0.25), (0.0, 1.0))]
+
+
+@pytest.mark.parametrize("P,B,nb,tau,tau_semi,tau_add", SEMI_CASES)
+def test_decode_with_semi_and_add_matches_brute_force(P, B, nb, tau, tau_semi, tau_add):
+    """The semi-completion and admission thresholds (App. G): cached oracle
+    decode = full recomputation with the rules restated independently."""
+    G = 8 - P
+    cfg, ws, m = _model(TinyCfg())
+    prompt = np.random.default_rng(P * 100 + B + 7).integers(0, cfg.vocab - 1, P)
+    bt, bs, bsteps = brute_decode(cfg, ws, list(prompt), G, B, nb, tau, tau_semi=tau_semi, tau_add=tau_add)
+    r = decode_batch(m, prompt[None, :], G, B, nb, tau, tau_semi=tau_semi, tau_add=tau_add)
+    np.testing.assert_array_equal(r.tokens[0], bt)
+    np.testing.assert_array_equal(r.commit_step[0], bs)
+    assert r.forwards[0] == bsteps
+
+
+@pytest.mark.parametrize("nb", [2, 3])
+def test_semi_zero_forces_one_token_per_block(nb):
+    """tau > 1 and tau_semi = 0: every active block is fully activated and
+    resolves one position per step, so nb blocks finish together every B
+    steps: forwards = G / nb, TPF = nb (G / B a multiple of nb)."""
+    cfg, ws, m = _model(TinyCfg(vocab=29))
+    P, B = 4, 4
+    G = B * nb * 2
+    prompts = np.random.default_rng(16).integers(0, cfg.vocab - 1, (2, P))
+    r = decode_batch(m, prompts, G, B, nb, 2.0, tau_semi=0.0, tau_add=0.0)
+    assert r.forwards.tolist() == [G // nb] * 2 and r.tpf == nb
+    np.testing.assert_array_equal(np.sort(r.commit_step[0]), np.repeat(np.arange(G // nb), nb))
+
+
+@pytest.mark.parametrize("nb", [2, 3])
+def test_semi_above_one_forces_only_the_oldest_block(nb):
+    """tau > 1 and tau_semi > 1: only the oldest active block (whose
+    predecessor is committed) may force a commit: one token per step."""
+    cfg, ws, m = _model(TinyCfg(vocab=29))
+    P, G, B = 4, 24, 4
+    prompts = np.random.default_rng(17).integers(0, cfg.vocab - 1, (2, P))
+    r = decode_batch(m, prompts, G, B, nb, 2.0, tau_semi=1.5)
+    assert r.forwards.tolist() == [G, G] and r.tpf == 1.0
+
+
+@pytest.mark.parametrize("tau", [0.4, 0.8])
+def test_add_one_or_single_block_reduces_to_one_block_decoding(tau):
+    """tau_add = 1 admits a block only when no other is in flight, and with
+    one block in flight the semi-completion rule is the base rule: both give
+    the n_inflight = 1 trace."""
+    cfg, ws, m = _model(TinyCfg(vocab=31), seed=5, std=0.4)
+    P, G, B = 4, 32, 4
+    prompts = np.random.default_rng(18).integers(0, cfg.vocab - 1, (2, P))
+    base = decode_batch(m, prompts, G, B, 1, tau)
+    for nb, ts in ((3, 0.7), (2, None), (3, 0.0)):
+        r = decode_batch(m, prompts, G, B, nb, tau, tau_semi=ts, tau_add=1.0)
+        np.testing.assert_array_equal(r.commit_step, base.commit_step)
+        np.testing.assert_array_equal(r.tokens, base.tokens)
+    r = decode_batch(m, prompts, G, B, 1, tau, tau_semi=0.9, tau_add=0.3)
+    np.testing.assert_array_equal(r.commit_step, base.commit_step)
+
+
 # ---------------------------------------------------------------- P2: causal decoding
 def test_block_size_one_is_greedy_causal_decoding():
     cfg, ws, m = _model(TinyCfg(vocab=23, n_kv_heads=2), seed=3)
