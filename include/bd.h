@@ -56,13 +56,32 @@ typedef struct {
     int32_t dtype;         /* bd_dtype of matrices, activations and KV cache */
 } bd_model_cfg;
 
-/* One serving configuration: the paper's operating point lambda (§2.1 and
- * the notation table): accept threshold, in-flight block count, block size. */
+/* One serving configuration: the paper's operating point lambda (§2.1, the
+ * notation table and App. G): accept threshold, in-flight block count, block
+ * size, semi-completion and admission thresholds.  "Resolved fraction" below
+ * is (unmasked positions of a block) / B as a float32 ratio, compared with
+ * the threshold as float32. */
 typedef struct {
-    float tau;             /* commit positions with confidence >= tau (float32
-                              compare); tau > 1 commits one token per step */
+    float tau;             /* accept: commit positions with confidence >= tau
+                              (float32 compare); tau > 1 commits only forced
+                              positions */
     int32_t n_inflight;    /* maximum number of active blocks, >= 1 */
     int32_t block_size;    /* B >= 1 */
+    float tau_semi;        /* semi-completion, < 0 = off.  Off: when no active
+                              position of a sequence clears tau, its single most
+                              confident one is committed.  On: an active block
+                              whose predecessor is committed, or active with a
+                              resolved fraction >= tau_semi at the start of the
+                              step, is fully activated and commits its own most
+                              confident position when none of its positions
+                              clears tau; other active blocks commit only
+                              positions >= tau. */
+    float tau_add;         /* admission: after the prefill and after every
+                              commit, placeholders are admitted in order while
+                              fewer than n_inflight blocks are active and either
+                              none is active or the youngest active block's
+                              resolved fraction is >= tau_add; <= 0 refills
+                              every free slot at once */
 } bd_decode_cfg;
 
 typedef struct bd_model bd_model;

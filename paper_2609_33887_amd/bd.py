@@ -36,7 +36,14 @@ class bd_model_cfg(ctypes.Structure):
 
 
 class bd_decode_cfg(ctypes.Structure):
-    _fields_ = [("tau", ctypes.c_float), ("n_inflight", ctypes.c_int32), ("block_size", ctypes.c_int32)]
+    _fields_ = [("tau", ctypes.c_float), ("n_inflight", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("tau_semi", ctypes.c_float), ("tau_add", ctypes.c_float)]
+
+
+def decode_cfg(tau: float, n_inflight: int, block_size: int, tau_semi=None, tau_add: float = 0.0):
+    """The C configuration; ``tau_semi=None`` switches semi-completion off."""
+    return bd_decode_cfg(tau=tau, n_inflight=n_inflight, block_size=block_size,
+                         tau_semi=-1.0 if tau_semi is None else tau_semi, tau_add=tau_add)
 
 
 class BDError(RuntimeError):
@@ -328,13 +335,14 @@ class Model:
 class State:
     """A decode state of ``b`` sequences (prefill done on creation)."""
 
-    def __init__(self, model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int):
+    def __init__(self, model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int,
+                 tau_semi=None, tau_add: float = 0.0):
         torch = model.torch
         self.m = model
         self.prompts = torch.as_tensor(prompts, dtype=torch.int32).to(model.device).contiguous()
         self.b, self.P = self.prompts.shape
         self.G = G
-        self.cfg = bd_decode_cfg(tau=tau, n_inflight=n_inflight, block_size=block_size)
+        self.cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add)
         self.handle = bd_prefill(model.handle, self.prompts.data_ptr(), self.b, self.P, G, self.cfg)
 
     def step(self, conf=None, tok=None, logits=None):
@@ -374,7 +382,8 @@ class State:
             pass
 
 
-def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int):
+def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int, tau_semi=None,
+           tau_add: float = 0.0):
     """Whole decode through ``bd_decode``; returns numpy (tokens, commit_step, forwards)."""
     torch = model.torch
     pr = torch.as_tensor(prompts, dtype=torch.int32).to(model.device).contiguous()
@@ -382,6 +391,6 @@ def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_siz
     t = torch.empty((b, G), dtype=torch.int32, device=model.device)
     c = torch.empty((b, G), dtype=torch.int32, device=model.device)
     f = torch.empty((b,), dtype=torch.int32, device=model.device)
-    cfg = bd_decode_cfg(tau=tau, n_inflight=n_inflight, block_size=block_size)
+    cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add)
     bd_decode(model.handle, pr.data_ptr(), b, P, G, cfg, t.data_ptr(), c.data_ptr(), f.data_ptr())
     return t.cpu().numpy(), c.cpu().numpy(), f.cpu().numpy()

@@ -113,6 +113,7 @@ struct ProfScope {
 struct bd_state {
   int b, P, G, B, nb;
   float tau;
+  int semi_min, add_min;   // thresholds as resolved counts (see min_resolved)
   int maxpos, rows_step, rows_pre, rows_cap, lm_cap, win_step;
   int32_t *tokens, *commit_step, *seq_state, *commit_flag;
   int32_t* plan_buf[3];
@@ -458,6 +459,14 @@ static bd_status check_err_flag(bd_model* m) {
   return BD_OK;
 }
 
+// Smallest resolved count r in [0, B] whose float32 fraction r / B reaches
+// thr (float32 compare), or B + 1 when none does.
+static int min_resolved(float thr, int B) {
+  for (int r = 0; r <= B; ++r)
+    if ((float)r / (float)B >= thr) return r;
+  return B + 1;
+}
+
 extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
                                 const bd_decode_cfg* cfg, bd_state** out) {
   if (!m || !cfg || !out) return fail(BD_EINVAL, "NULL argument");
@@ -465,7 +474,8 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   const int B = cfg->block_size, nb = cfg->n_inflight;
   if (b < 1 || P < 0 || G < 1 || B < 1 || nb < 1) return fail(BD_EINVAL, "need b, G, B, n_inflight >= 1 and P >= 0");
   if (P % B || G % B) return fail(BD_EINVAL, "P and G must be multiples of the block size");
-  if (isnan(cfg->tau)) return fail(BD_EINVAL, "tau is NaN");
+  if (isnan(cfg->tau) || isnan(cfg->tau_semi) || isnan(cfg->tau_add))
+    return fail(BD_EINVAL, "tau, tau_semi or tau_add is NaN");
   if (P > 0 && !prompt) return fail(BD_EINVAL, "NULL prompt");
   if (b > 256) return fail(BD_EUNSUPPORTED, "at most 256 sequences per state");
   if (nb > 8) return fail(BD_EUNSUPPORTED, "at most 8 in-flight blocks");
@@ -473,6 +483,8 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
 
   bd_state* s = new bd_state();
   s->b = b; s->P = P; s->G = G; s->B = B; s->nb = nb; s->tau = cfg->tau;
+  s->semi_min = cfg->tau_semi < 0.0f ? -1 : min_resolved(cfg->tau_semi, B);
+  s->add_min = min_resolved(cfg->tau_add, B);
   s->maxpos = P + G;
   s->win_step = 2 * nb * B;
   s->rows_step = round_up(b * s->win_step, 256);
@@ -591,6 +603,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ia.commit_step = s->commit_step;
   ia.seq_state = s->seq_state;
   ia.b = b; ia.P = P; ia.G = G; ia.B = B; ia.nb = nb; ia.mask_id = c.mask_id; ia.vocab = c.vocab;
+  ia.add_min = s->add_min;
   ia.err_flag = m->err_flag;
   ia.stats = s->stats;
   e = launch_init_decode(ia, m->stream);
@@ -620,7 +633,7 @@ extern "C" bd_status bd_state_reset(bd_model* m, bd_state* s) {
   ia.prompt = nullptr;
   ia.commit_step = s->commit_step;
   ia.seq_state = s->seq_state;
-  ia.b = s->b; ia.P = s->P; ia.G = s->G; ia.B = s->B; ia.nb = s->nb;
+  ia.b = s->b; ia.P = s->P; ia.G = s->G; ia.B = s->B; ia.nb = s->nb; ia.add_min = s->add_min;
   ia.mask_id = m->cfg.mask_id; ia.vocab = m->cfg.vocab; ia.err_flag = m->err_flag;
   ia.stats = s->stats;
   HIPCHK(launch_init_decode(ia, m->stream));
@@ -677,6 +690,8 @@ extern "C" bd_status bd_commit(bd_model* m, bd_state* s, int32_t* all_done_host)
   a.mask_id = m->cfg.mask_id;
   a.step = s->steps;
   a.tau = s->tau;
+  a.semi_min = s->semi_min;
+  a.add_min = s->add_min;
   a.stats = s->stats;
   LAUNCH(BD_PROF_COMMIT, launch_commit(a, m->stream));
   s->cur ^= 1;

@@ -241,6 +241,8 @@ struct CommitArgs {
   long long* stats;         // [8] work counters of the executed steps
   int b, P, G, B, nb, mask_id, step;
   float tau;
+  int semi_min;             // semi-completion: resolved count that fully activates the next block; -1 = off
+  int add_min;              // admission: resolved count of the youngest active block that admits the next
 };
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 
@@ -252,6 +254,7 @@ struct InitArgs {
   int32_t* commit_step;
   int32_t* seq_state;
   int b, P, G, B, nb, mask_id, vocab;
+  int add_min;              // as in CommitArgs
   int32_t* err_flag;
   long long* stats;         // [8], cleared
 };

@@ -279,30 +279,80 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       s_pairs[s] = (long long)B * (nbw * start + (long long)B * nbw * (nbw + 1) / 2);
       s_keys[s] = start + (long long)a.in.seq_win_len[s];
     }
-    // pass 1: does any position clear tau, and the most confident position
-    bool any = false;
-    float best = -INFINITY;
-    int bestpos = 0x7fffffff;
+    // pass 1, per active block k: masked positions, whether one clears tau,
+    // and the most confident one (lowest position among equals)
+    int blk_masked[MAXNB], blk_commit[MAXNB], blk_best_pos[MAXNB];
+    float blk_best[MAXNB];
+    bool blk_any[MAXNB];
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k) {
+      blk_masked[k] = 0; blk_commit[k] = 0; blk_best[k] = -INFINITY; blk_best_pos[k] = 0x7fffffff;
+      blk_any[k] = false;
+    }
     for (int base = 0; base < lmn; base += 64) {
       const int i = base + lane;
-      if (i < lmn) {
-        const float cf = a.conf[lm0 + i];
-        const int pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
-        any |= (cf >= a.tau);
-        if (cf > best || (cf == best && pos < bestpos)) { best = cf; bestpos = pos; }
+      const bool valid = i < lmn;
+      float cf = -INFINITY;
+      int pos = 0x7fffffff, kb = -1;
+      if (valid) {
+        cf = a.conf[lm0 + i];
+        pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
+        kb = (pos - P) / B - first_act;
+      }
+#pragma unroll
+      for (int k = 0; k < MAXNB; ++k) {
+        const bool mine = valid && kb == k;
+        blk_masked[k] += wave_popc(mine);
+        blk_any[k] |= mine && cf >= a.tau;
+        if (mine && (cf > blk_best[k] || (cf == blk_best[k] && pos < blk_best_pos[k]))) {
+          blk_best[k] = cf;
+          blk_best_pos[k] = pos;
+        }
       }
     }
-    any = __ballot(any) != 0;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const float ob = __shfl_xor(best, off);
-      const int op = __shfl_xor(bestpos, off);
-      if (ob > best || (ob == best && op < bestpos)) { best = ob; bestpos = op; }
+    for (int k = 0; k < MAXNB; ++k) {
+      blk_any[k] = __ballot(blk_any[k]) != 0;
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ob = __shfl_xor(blk_best[k], off);
+        const int op = __shfl_xor(blk_best_pos[k], off);
+        if (ob > blk_best[k] || (ob == blk_best[k] && op < blk_best_pos[k])) {
+          blk_best[k] = ob;
+          blk_best_pos[k] = op;
+        }
+      }
     }
-    // pass 2: commit, and count masked / committed positions per active block
-    int blk_masked[MAXNB], blk_commit[MAXNB];
+    // forced commits.  Semi-completion off: one per sequence when no position
+    // clears tau, the most confident over all blocks (blocks are in position
+    // order, so the first block holding the maximum has its lowest position).
+    // On: one per fully activated block with masked positions of which none
+    // clears tau; block k > 0 is fully activated when block k - 1 had
+    // resolved >= semi_min positions at the start of the step.
+    int forced_pos[MAXNB];
 #pragma unroll
-    for (int k = 0; k < MAXNB; ++k) { blk_masked[k] = 0; blk_commit[k] = 0; }
+    for (int k = 0; k < MAXNB; ++k) forced_pos[k] = -1;
+    if (a.semi_min < 0) {
+      bool any = false;
+      float best = -INFINITY;
+      int bp = -1;
+#pragma unroll
+      for (int k = 0; k < MAXNB; ++k) {
+        any |= blk_any[k];
+        if (k < n_act && blk_masked[k] > 0 && (bp < 0 || blk_best[k] > best)) {
+          best = blk_best[k];
+          bp = blk_best_pos[k];
+        }
+      }
+      if (!any) forced_pos[0] = bp;
+    } else {
+#pragma unroll
+      for (int k = 0; k < MAXNB; ++k) {
+        const bool full = k == 0 || (B - blk_masked[k > 0 ? k - 1 : 0]) >= a.semi_min;
+        if (k < n_act && blk_masked[k] > 0 && full && !blk_any[k]) forced_pos[k] = blk_best_pos[k];
+      }
+    }
+    // pass 2: commit, and count committed positions per active block
     for (int base = 0; base < lmn; base += 64) {
       const int i = base + lane;
       const bool valid = i < lmn;
@@ -311,7 +361,9 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       if (valid) {
         const float cf = a.conf[lm0 + i];
         const int pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
-        c = any ? (cf >= a.tau) : (pos == bestpos);
+        c = cf >= a.tau;
+#pragma unroll
+        for (int k = 0; k < MAXNB; ++k) c |= pos == forced_pos[k];
         kb = (pos - P) / B - first_act;
         if (c) {
           a.tokens[(size_t)s * a.tok_stride + pos] = a.tok[lm0 + i];
@@ -320,10 +372,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
         a.commit_flag[lm0 + i] = c ? 1 : 0;
       }
 #pragma unroll
-      for (int k = 0; k < MAXNB; ++k) {
-        blk_masked[k] += wave_popc(valid && kb == k);
-        blk_commit[k] += wave_popc(valid && kb == k && c);
-      }
+      for (int k = 0; k < MAXNB; ++k) blk_commit[k] += wave_popc(valid && kb == k && c);
     }
     int ncommit = 0;
 #pragma unroll
@@ -343,8 +392,17 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
     first_act += sw;
     n_act -= sw;
     const int nblk = G / B;
+    // admission: the youngest active block after the sweep is pre-sweep
+    // block sw + n_act - 1; a newly admitted block has nothing resolved
+    int young = 0;
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k)
+      if (k == sw + n_act - 1) young = B - (blk_masked[k] - blk_commit[k]);
     int adm = 0;
-    while (n_act < a.nb && next_blk < nblk) { ++n_act; ++next_blk; ++adm; }
+    while (n_act < a.nb && next_blk < nblk && (n_act == 0 || young >= a.add_min)) {
+      ++n_act; ++next_blk; ++adm;
+      young = 0;
+    }
     const int now_done = (n_act == 0);
     if (lane == 0) {
       ss[SS_CACHE_LEN] = cache_len;
@@ -423,7 +481,10 @@ __global__ __launch_bounds__(1024) void k_init_decode(InitArgs a) {
   __shared__ int s_win[MAXB], s_rs[MAXB];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
   const int stride = a.P + a.G, nblk = a.G / a.B;
-  const int nact = min(a.nb, nblk);
+  // admission as after a commit: the first block unconditionally, further
+  // ones while the youngest (nothing resolved yet) reaches add_min
+  int nact = min(1, nblk);
+  while (nact < a.nb && nact < nblk && 0 >= a.add_min) ++nact;
   for (int s = wave; s < a.b; s += nw) {
     int32_t* t = a.tokens + (size_t)s * stride;
     if (a.prompt) {

@@ -9,7 +9,8 @@ excused only when the oracle's numbers make it a near-tie:
 
   T1  |conf - tau| <= 1e-3 at a position committed by one side only;
   T2  the two most probable tokens are within 1e-3 of probability;
-  T3  the forced single commit where the two best confidences are within 1e-3;
+  T3  a forced commit (of the sequence, or of one block under semi-completion)
+      whose two best confidences are within 1e-3;
   T4  (MoE) a step whose forward, in the oracle, routed some row with a gap of
       at most 1e-5 between its k-th and (k+1)-th router logits: expert choice
       there can differ, so that step's statistics and decisions are excused.
@@ -36,10 +37,10 @@ class GpuTrace:
 
 
 def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=None, logit_steps=None,
-                      progress=None):
+                      progress=None, tau_semi=None, tau_add=0.0):
     import torch
     from paper_2609_33887_amd import bd
-    st = bd.State(model, prompts, G, tau, nb, B)
+    st = bd.State(model, prompts, G, tau, nb, B, tau_semi, tau_add)
     b = st.b
     dev = model.device
     V = model.w.vocab
@@ -87,14 +88,14 @@ class Report:
 
 
 def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, conf_tol, logit_tol,
-             max_steps=None, progress=None):
+             max_steps=None, progress=None, tau_semi=None, tau_add=0.0):
     """Replay the chosen sequences in the oracle against ``trace`` (the first
     ``max_steps`` steps of each when given)."""
     from oracle.decode import SeqDecoder
     rep = Report()
     tau32 = float(np.float32(tau))
     for i in seq_ids:
-        d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau)
+        d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau, tau_semi, tau_add)
         if progress:
             progress(f"  oracle prefill of sequence {i}")
         d.prefill()
@@ -129,18 +130,21 @@ def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, con
             if np.any(np.abs(conf - gconf) > conf_tol):
                 rep.failures.append((i, step, f"confidence differs by {np.max(np.abs(conf - gconf)):.3g}"))
             # decisions
-            own = np.zeros(len(masked), dtype=bool)
-            own_sel = conf >= tau32
-            if own_sel.any():
-                own = own_sel
-            else:
-                own[int(np.argmax(conf))] = True
+            own, forced = d.decision(masked, conf)
             gsel = trace.commit_step[i, masked - P] == step
+
+            def forced_near(k):
+                for grp in forced:
+                    if k in grp and len(grp) > 1:
+                        c2 = np.sort(conf[grp])
+                        if c2[-1] - c2[-2] <= NEAR:
+                            return True
+                return False
+
             for k in np.nonzero(own != gsel)[0]:
                 if abs(conf[k] - tau32) <= NEAR:
                     rep.t1 += 1
-                elif not own_sel.any() and len(conf) > 1 and \
-                        np.sort(conf)[-1] - np.sort(conf)[-2] <= NEAR:
+                elif forced_near(k):
                     rep.t3 += 1
                 else:
                     rep.failures.append((i, step, f"commit decision differs at position {masked[k] - P} "

@@ -73,20 +73,22 @@ def get_model(w):
     return _models[key]
 
 
-def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None):
+def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None, tau_semi=None,
+               tau_add=0.0):
     from oracle.model import OracleModel
     from tests.gpu_harness import capture_gpu_trace, lockstep
     _need_gpu()
     _say(f"[parity] {w.name} tau={tau} b={w.batch} P={w.prompt_len} G={w.gen_len} B={w.block_size} "
-         f"nb={w.n_inflight}")
+         f"nb={w.n_inflight} tau_semi={tau_semi} tau_add={tau_add}")
     model, ws = get_model(w)
     prompts = make_prompts(w)
     ids = list(range(w.batch)) if seq_ids is None else list(seq_ids)
     tr = capture_gpu_trace(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size,
-                           logits_for=set(ids) if logits else (), logit_steps=logit_steps, progress=_say)
+                           logits_for=set(ids) if logits else (), logit_steps=logit_steps, progress=_say,
+                           tau_semi=tau_semi, tau_add=tau_add)
     om = OracleModel(w, ws, "f64" if w.dtype == "f32" else "bf16")
     rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, w.n_inflight, w.block_size, *TOL[w.dtype],
-                   max_steps=max_steps, progress=_say)
+                   max_steps=max_steps, progress=_say, tau_semi=tau_semi, tau_add=tau_add)
     ctol, ltol = TOL[w.dtype]
     _say(f"  positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} max|dlogit|={rep.max_logit_diff:.3g} "
          f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} T4(steps)={rep.t4} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
@@ -113,6 +115,27 @@ def test_degenerate_thresholds(tau):
         assert (tr.forwards == -(-nblk // w.n_inflight)).all()
     else:
         assert (tr.forwards == w.gen_len).all()
+
+
+# semi-completion / admission thresholds (App. G): acc x semi x add points
+# like the paper's grids, on multi-block small models
+ENGINE_POINTS = [(0.9, 0.7, 0.1), (0.85, 0.9, 0.3), (0.95, 0.5, 0.0), (2.0, 0.0, 0.0)]
+
+
+@pytest.mark.parametrize("name", ["mha64", "gqa128_ragged", "moe", "f32_gqa"])
+@pytest.mark.parametrize("tau,tau_semi,tau_add", ENGINE_POINTS)
+def test_small_models_semi_add(name, tau, tau_semi, tau_add):
+    w = SMALL[name]
+    tr, rep = run_parity(w, tau, logits=False, tau_semi=tau_semi, tau_add=tau_add)
+    if tau > 1.0 and tau_semi == 0.0 and (w.gen_len // w.block_size) % w.n_inflight == 0:
+        # every active block forces one position per step: TPF = n_inflight
+        assert (tr.forwards == w.gen_len // w.n_inflight).all()
+
+
+def test_config2_multiblock_semi_add():
+    """Config 2 (3 blocks in flight) at acc 0.9 / semi 0.7 / add 0.1: the
+    whole batch on the GPU, the oracle replays sequence 5 for 16 steps."""
+    run_parity(workload(2), 0.9, seq_ids=[5], max_steps=16, logit_steps=2, tau_semi=0.7, tau_add=0.1)
 
 
 def test_config0_tiny_f32():
