@@ -570,7 +570,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
       return fail(BD_EHIP, "hipMemsetAsync: %s", hipGetErrorString(e2));
     }
   }
-  s->attn_splits = m->bf16 ? attention_splits(b, s->win_step, H, Hkv, hd, s->maxpos) : 1;
+  s->attn_splits = m->bf16 ? attention_splits(b, s->win_step, nb * B, H, Hkv, hd, s->maxpos) : 1;
   if (s->attn_splits > 1) {
     ALLOC(s->attn_ws_o, (size_t)s->attn_splits * s->rows_step * H * hd * 4);
     ALLOC(s->attn_ws_ml, (size_t)s->attn_splits * s->rows_step * H * 2 * 4);

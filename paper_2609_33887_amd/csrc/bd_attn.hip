@@ -353,9 +353,11 @@ __global__ __launch_bounds__(256) void k_attn_f32(const float* __restrict__ Q,
 // waves per workgroup for a window of win_cap rows (see k_attn_bf16)
 static int attention_waves(int win_cap, int H, int Hkv) { return (H / Hkv) * win_cap <= 32 ? 2 : 4; }
 
-int attention_splits(int b, int win_cap, int H, int Hkv, int hd, int maxpos) {
+int attention_splits(int b, int win_cap, int rows_est, int H, int Hkv, int hd, int maxpos) {
+  // the launch shape follows win_cap (the largest window); the work estimate
+  // follows rows_est, the rows a window usually holds
   const int nw = attention_waves(win_cap, H, Hkv);
-  const int wgs = (((H / Hkv) * win_cap + 16 * nw - 1) / (16 * nw)) * Hkv * b;
+  const int wgs = (((H / Hkv) * rows_est + 16 * nw - 1) / (16 * nw)) * Hkv * b;
   // workgroups resident per CU (LDS-bound: 37 KB per workgroup at hd 64,
   // 72 KB at hd 128; 3 of the 4-wave hd-64 kind): split the key range until
   // the grid fills one resident round of 256 CUs, while every split keeps

@@ -212,7 +212,7 @@ hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const K
                             size_t o_plane, PlanView plan, int b, int win_cap, int H, int Hkv,
                             int hd, int B, int kv_splits, float* ws_o, float* ws_ml, int rows_cap,
                             hipStream_t st);
-int attention_splits(int b, int win_cap, int H, int Hkv, int hd, int maxpos);
+int attention_splits(int b, int win_cap, int rows_est, int H, int Hkv, int hd, int maxpos);
 
 hipError_t launch_embed(bool is_bf16, const int32_t* tokens, int tok_stride, const void* E, int d,
                         int vocab, PlanView plan, int rows_cap, float* X, int32_t* err_flag,

@@ -301,6 +301,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < MAXNB; ++k) {
+        if (k >= n_act) break;                 // wave-uniform
         const bool mine = valid && kb == k;
         blk_masked[k] += wave_popc(mine);
         blk_any[k] |= mine && cf >= a.tau;
@@ -312,6 +313,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < MAXNB; ++k) {
+      if (k >= n_act) break;
       blk_any[k] = __ballot(blk_any[k]) != 0;
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
@@ -372,7 +374,10 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
         a.commit_flag[lm0 + i] = c ? 1 : 0;
       }
 #pragma unroll
-      for (int k = 0; k < MAXNB; ++k) blk_commit[k] += wave_popc(valid && kb == k && c);
+      for (int k = 0; k < MAXNB; ++k) {
+        if (k >= n_act) break;
+        blk_commit[k] += wave_popc(valid && kb == k && c);
+      }
     }
     int ncommit = 0;
 #pragma unroll

@@ -1,13 +1,21 @@
 """Redline selection sweep over serving configurations (§4.2, App. A).
 
-Every configuration lambda = (tau, n_inflight) decodes the same calibration
-prompts through ``bd_decode``; a decode is *correct* when its final ``tail``
-generated tokens equal the reference configuration's.  The correctness
-matrix and the TPF of each configuration then go to ``rl_risk_select``,
-which deploys the fastest configuration whose reference-relative risk passes
-the exact binomial test under Holm's correction.
+Every configuration lambda = (tau, n_inflight) or (tau, n_inflight, tau_semi,
+tau_add) decodes the same calibration prompts through ``bd_decode``; a decode
+is *correct* when its final ``tail`` generated tokens equal the reference
+configuration's.  The correctness matrix and the TPF of each configuration
+then go to ``rl_select`` (Holm by default), which deploys the fastest
+configuration whose reference-relative risk passes the exact binomial test,
+and to ``rl_alpha_sweep`` for the smallest budget with a gain.
 
-Run: ``python -m paper_2609_33887_amd.sweep --prompts 1000`` (prints JSON).
+Grids: ``tau-nb`` -- accept threshold x in-flight blocks against the
+one-token-per-step reference; ``engine`` -- accept {0.85, 0.90, 0.95, 0.99} x
+semi-completion {0.70, 0.90} at admission 0.10 and two blocks in flight, with
+the engine default acc95/semi90 as the reference (the shape of the paper's
+grids, App. G).
+
+Run: ``python -m paper_2609_33887_amd.sweep --prompts 1000 [--grid engine]``
+(prints JSON).
 """
 from __future__ import annotations
 
@@ -21,34 +29,55 @@ import numpy as np
 from . import bd
 
 
-def decode_all(model, prompts, G, tau, nb, B, batch):
-    """Decode ``prompts`` in batches; returns tokens [n][G] and forwards [n]."""
+ENGINE_REFERENCE = (0.95, 2, 0.90, 0.10)
+ENGINE_GRID = [(acc, 2, semi, 0.10) for acc in (0.85, 0.90, 0.95, 0.99) for semi in (0.70, 0.90)
+               if (acc, semi) != (0.95, 0.90)]
+
+
+def label(cfg) -> str:
+    """acc85/semi70/add0.10-style label (nb suffix for the tau x nb grid)."""
+    tau, nb = cfg[0], cfg[1]
+    if len(cfg) == 2:
+        return f"acc{round(100 * tau)}/nb{nb}" if tau <= 1 else f"one-token/nb{nb}"
+    return f"acc{round(100 * tau)}/semi{round(100 * cfg[2])}/add{cfg[3]:.2f}"
+
+
+def decode_all(model, prompts, G, cfg, B, batch):
+    """Decode ``prompts`` in batches under cfg = (tau, nb[, tau_semi, tau_add]);
+    returns tokens [n][G] and forwards [n]."""
+    tau, nb = cfg[0], cfg[1]
+    ts, ta = (cfg[2], cfg[3]) if len(cfg) == 4 else (None, 0.0)
     toks, fwd = [], []
     for i in range(0, prompts.shape[0], batch):
-        t, _, f = bd.decode(model, prompts[i:i + batch], G, tau, nb, B)
+        t, _, f = bd.decode(model, prompts[i:i + batch], G, tau, nb, B, ts, ta)
         toks.append(t)
         fwd.append(f)
     return np.concatenate(toks), np.concatenate(fwd)
 
 
 def redline_sweep(model, prompts, G, B, candidates, reference, alpha, delta, tail=16, batch=64,
-                  progress=None):
-    """candidates / reference: (tau, n_inflight) pairs.  The reference is the
-    first row of the grid (the grid includes it, §4.2 (i))."""
+                  progress=None, method="holm", alphas=None):
+    """candidates / reference: (tau, n_inflight[, tau_semi, tau_add]).  The
+    reference is the first row of the grid (the grid includes it, §4.2 (i))."""
     grid = [tuple(reference)] + [tuple(c) for c in candidates]
     outs, tpf = [], []
-    for j, (tau, nb) in enumerate(grid):
+    for j, cfg in enumerate(grid):
         t0 = time.perf_counter()
-        toks, fwd = decode_all(model, prompts, G, tau, nb, B, batch)
+        toks, fwd = decode_all(model, prompts, G, cfg, B, batch)
         outs.append(toks)
         tpf.append(toks.size / float(fwd.sum()))
         if progress:
-            progress(f"config {j} tau={tau} nb={nb}: TPF {tpf[-1]:.4f} ({time.perf_counter() - t0:.1f} s)")
+            progress(f"config {j} {label(cfg)}: TPF {tpf[-1]:.4f} ({time.perf_counter() - t0:.1f} s)")
     ref_tail = outs[0][:, -tail:]
     correct = np.stack([np.all(o[:, -tail:] == ref_tail, axis=1) for o in outs]).astype(np.uint8)
-    V, p, valid, sel, near = bd.rl_risk_select(correct, np.array(tpf), 0, alpha, delta)
-    return {"grid": grid, "tpf": tpf, "correct": correct, "V": V, "p": p, "valid": valid,
-            "selected": sel, "near_ties": near, "tokens": outs}
+    V, p, valid, sel = bd.rl_select(correct, np.array(tpf), 0, alpha, delta, method)
+    out = {"grid": grid, "labels": [label(c) for c in grid], "tpf": tpf, "correct": correct, "V": V,
+           "p": p, "valid": valid, "selected": sel, "tokens": outs}
+    if alphas is not None:
+        sweep_sel, n_valid, hat = bd.rl_alpha_sweep(correct, np.array(tpf), 0, alphas, delta, method)
+        out.update(alphas=list(alphas), alpha_selected=sweep_sel.tolist(), alpha_n_valid=n_valid.tolist(),
+                   alpha_hat=hat)
+    return out
 
 
 def main():
@@ -57,6 +86,8 @@ def main():
     ap.add_argument("--prompts", type=int, default=1000)
     ap.add_argument("--alpha", type=float, default=0.10)
     ap.add_argument("--delta", type=float, default=0.05)
+    ap.add_argument("--grid", choices=["tau-nb", "engine"], default="tau-nb")
+    ap.add_argument("--method", choices=list(bd.RL_METHODS), default="holm")
     args = ap.parse_args()
     import os
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
@@ -64,15 +95,19 @@ def main():
     w = workload(args.config)
     model = bd.Model(w, make_weights(w))
     prompts = make_prompts(w, args.prompts)
-    cands = [(t, nb) for t in (0.95, 0.9, 0.8, 0.7) for nb in (1, 2, 3)]
+    if args.grid == "engine":
+        cands, ref = ENGINE_GRID, ENGINE_REFERENCE
+    else:
+        cands, ref = [(t, nb) for t in (0.95, 0.9, 0.8, 0.7) for nb in (1, 2, 3)], (2.0, 1)
     say = lambda m: print(m, file=sys.stderr, flush=True)
-    r = redline_sweep(model, prompts, w.gen_len, w.block_size, cands, (2.0, 1), args.alpha, args.delta,
-                      batch=w.batch, progress=say)
+    r = redline_sweep(model, prompts, w.gen_len, w.block_size, cands, ref, args.alpha, args.delta,
+                      batch=w.batch, progress=say, method=args.method,
+                      alphas=[i / 100 for i in range(1, 31)])
     print(json.dumps({"workload": w.name, "prompts": args.prompts, "alpha": args.alpha,
-                      "delta": args.delta, "grid": r["grid"], "tpf": r["tpf"],
+                      "delta": args.delta, "method": args.method, "grid": r["labels"], "tpf": r["tpf"],
                       "V": r["V"].tolist(), "p": r["p"].tolist(), "valid": r["valid"].tolist(),
-                      "selected": r["selected"], "selected_config": r["grid"][r["selected"]],
-                      "near_ties": r["near_ties"]}))
+                      "selected": r["selected"], "selected_config": r["labels"][r["selected"]],
+                      "alpha_hat": r["alpha_hat"]}))
 
 
 if __name__ == "__main__":

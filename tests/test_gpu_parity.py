@@ -271,3 +271,28 @@ def test_config4_redline_sweep_matches_oracle():
     for a, b in zip(r["p"], o.p):
         assert abs(a - float(b)) <= 1e-11 * float(b) + 1e-300
     _say(f"  TPF {['%.3f' % t for t in r['tpf']]} V {r['V'].tolist()} selected {r['grid'][r['selected']]}")
+
+
+def test_engine_grid_sweep_matches_oracle():
+    """The acc x semi grid at admission 0.10 and two blocks in flight (the
+    shape of the paper's grids) on the small MHA model, 48 calibration
+    prompts against the engine default acc95/semi90: selection and the budget
+    sweep of the C implementation equal the oracle's on the GPU-decoded
+    matrix (each configuration's decode is checked against the oracle by
+    test_small_models_semi_add)."""
+    from paper_2609_33887_amd.sweep import redline_sweep, ENGINE_GRID, ENGINE_REFERENCE
+    from oracle import redline as orl
+    _need_gpu()
+    w = SMALL["mha64"]
+    model, ws = get_model(w)
+    prompts = make_prompts(w, 48)
+    alphas = [0.05, 0.1, 0.15, 0.2, 0.3]
+    r = redline_sweep(model, prompts, w.gen_len, w.block_size, ENGINE_GRID, ENGINE_REFERENCE, 0.10, 0.10,
+                      tail=8, batch=16, progress=_say, alphas=alphas)
+    o = orl.select(r["correct"], r["tpf"], 0, 0.10, 0.10)
+    assert r["V"].tolist() == o.V.tolist() and r["valid"].tolist() == o.valid.tolist()
+    assert r["selected"] == o.selected
+    sel, nval, hat = orl.alpha_sweep(r["correct"], r["tpf"], 0, alphas, 0.10)
+    assert r["alpha_selected"] == sel and r["alpha_n_valid"] == nval and r["alpha_hat"] == hat
+    for j in range(len(r["grid"])):
+        _say(f"  {r['labels'][j]}: TPF {r['tpf'][j]:.3f} V {int(r['V'][j])} valid {bool(r['valid'][j])}")
