@@ -34,6 +34,17 @@ the engine description of the paper:
   Without ``tau_semi`` the forced commit is one per sequence, over all active
   blocks (the base rule above).  Resolved fractions are float32 ratios
   compared with float32 thresholds.
+* Static skip rule (§3 "The allocation lever", App. "Participation
+  schedules"): with ``skip_masked`` an active block that is still fully
+  masked at the start of a step is left out of that step's forward while an
+  older block is active; it gets no confidences and no commits.
+* Participation counters (the same appendix, measured here on the live
+  decode rather than on a replayed trace), summed over steps: active
+  block-forwards, those that commit nothing, those the static rule would
+  skip (fully masked with an older active block) split into the ones that
+  commit nothing (the FLOPs the rule saves) and the ones that commit
+  (deferred), the one-step cache writes forwarded, and the active blocks a
+  live skip rule left out.
 * TPF (§2.1): tokens committed per model forward; a forward is a step in
   which the sequence has at least one active block.  Prefill is not counted
   (App. G.1).
@@ -49,7 +60,10 @@ from .model import OracleModel, lm_stats
 
 PLACEHOLDER, ACTIVE, PENDING, CACHED = 0, 1, 2, 3
 
-__all__ = ["SeqDecoder", "commit_set", "commit_set_semi", "frac_at_least", "decode_batch", "PLACEHOLDER", "ACTIVE", "PENDING", "CACHED"]
+PART_NAMES = ("active_forwards", "zero_commit", "static_saved", "static_deferred", "cache_writes",
+              "skipped")
+
+__all__ = ["PART_NAMES", "SeqDecoder", "commit_set", "commit_set_semi", "frac_at_least", "decode_batch", "PLACEHOLDER", "ACTIVE", "PENDING", "CACHED"]
 
 
 def frac_at_least(resolved: int, B: int, thr: float) -> bool:
@@ -103,12 +117,14 @@ class SeqDecoder:
     positions in ``G // B`` blocks, at most ``n_inflight`` active blocks."""
 
     def __init__(self, model: OracleModel, prompt: np.ndarray, G: int, B: int, n_inflight: int,
-                 tau: float, tau_semi: Optional[float] = None, tau_add: float = 0.0):
+                 tau: float, tau_semi: Optional[float] = None, tau_add: float = 0.0,
+                 skip_masked: bool = False):
         P = len(prompt)
         if B < 1 or n_inflight < 1 or P % B or G % B:
             raise ValueError("need B >= 1, n_inflight >= 1, P % B == 0 and G % B == 0")
         self.model, self.P, self.G, self.B, self.nb, self.tau = model, P, G, B, n_inflight, tau
-        self.tau_semi, self.tau_add = tau_semi, tau_add
+        self.tau_semi, self.tau_add, self.skip_masked = tau_semi, tau_add, skip_masked
+        self.part = np.zeros(len(PART_NAMES), dtype=np.int64)
         self.mask_id = model.mask_id
         self.tokens = np.concatenate([np.asarray(prompt, dtype=np.int64),
                                       np.full(G, self.mask_id, dtype=np.int64)])
@@ -140,11 +156,43 @@ class SeqDecoder:
     def done(self) -> bool:
         return not np.any((self.status == ACTIVE) | (self.status == PLACEHOLDER))
 
+    def forwarded(self) -> np.ndarray:
+        """Active blocks that take part in this step's forward: all of them,
+        or under the static skip rule those that are the oldest active block
+        or already hold a resolved position."""
+        act = np.nonzero(self.status == ACTIVE)[0]
+        if not self.skip_masked:
+            return act
+        return np.array([b for j, b in enumerate(act) if j == 0 or self.resolved(int(b)) > 0],
+                        dtype=np.int64)
+
     def window(self):
         """Absolute positions [start, end) of this step's forward: pending
-        blocks (clean rows for their cache write) followed by active blocks."""
-        live = np.nonzero((self.status == PENDING) | (self.status == ACTIVE))[0]
+        blocks (clean rows for their cache write) followed by the forwarded
+        active blocks (the skip rule only ever leaves out the youngest)."""
+        fwd = self.forwarded()
+        live = np.concatenate([np.nonzero(self.status == PENDING)[0], fwd])
+        if self.skip_masked:
+            assert np.array_equal(live, np.arange(live[0], live[-1] + 1)), "window not contiguous"
         return self.cache_len, self.P + self.B * (int(live[-1]) + 1)
+
+    def count_participation(self, committed: np.ndarray):
+        """Add this step's participation counters (see the module notes);
+        ``committed`` are the absolute positions committed by the step."""
+        act = np.nonzero(self.status == ACTIVE)[0]
+        fwd = set(int(b) for b in self.forwarded())
+        blk = (np.asarray(committed, dtype=np.int64) - self.P) // self.B
+        for j, b in enumerate(act):
+            b = int(b)
+            if b not in fwd:
+                self.part[5] += 1
+                continue
+            n_commit = int(np.count_nonzero(blk == b))
+            self.part[0] += 1
+            self.part[1] += n_commit == 0
+            if j > 0 and self.resolved(b) == 0:
+                self.part[2 if n_commit == 0 else 3] += 1
+        self.part[4] += int(np.count_nonzero(self.status == PENDING))
 
     # -- prefill --------------------------------------------------------------
     def prefill(self):
@@ -210,6 +258,7 @@ class SeqDecoder:
             positions = masked[sel]
         else:
             positions, toks = decide(self, step, masked, conf, tok, p2, own)
+        self.count_participation(np.asarray(positions, dtype=np.int64))
         self.apply(np.asarray(positions, dtype=np.int64), np.asarray(toks, dtype=np.int64), step)
         if self.keep_records:
             self.records.append(StepRecord(step, masked, conf, tok, p2, np.asarray(positions),
@@ -222,6 +271,7 @@ class BatchResult:
     commit_step: np.ndarray     # [b][G] step index at which each position committed
     forwards: np.ndarray        # [b]
     steps: int
+    participation: np.ndarray = None   # [len(PART_NAMES)], summed over sequences
 
     @property
     def tpf(self) -> float:
@@ -232,7 +282,7 @@ class BatchResult:
 def decode_batch(model: OracleModel, prompts: np.ndarray, G: int, B: int, n_inflight: int,
                  tau: float, decide: Optional[Callable] = None, max_steps: int | None = None,
                  keep_records: bool = False, tau_semi: Optional[float] = None,
-                 tau_add: float = 0.0) -> BatchResult:
+                 tau_add: float = 0.0, skip_masked: bool = False) -> BatchResult:
     """Decode independent sequences; batch rows never interact, so each runs
     its own state machine and the global step index equals its forward index
     while it is active."""
@@ -240,9 +290,10 @@ def decode_batch(model: OracleModel, prompts: np.ndarray, G: int, B: int, n_infl
     toks = np.zeros((b, G), dtype=np.int64)
     cs = np.zeros((b, G), dtype=np.int64)
     fw = np.zeros(b, dtype=np.int64)
+    part = np.zeros(len(PART_NAMES), dtype=np.int64)
     steps = 0
     for i in range(b):
-        d = SeqDecoder(model, prompts[i], G, B, n_inflight, tau, tau_semi, tau_add)
+        d = SeqDecoder(model, prompts[i], G, B, n_inflight, tau, tau_semi, tau_add, skip_masked)
         d.keep_records = keep_records
         d.seq_index = i
         d.prefill()
@@ -256,4 +307,5 @@ def decode_batch(model: OracleModel, prompts: np.ndarray, G: int, B: int, n_infl
         toks[i] = d.tokens[d.P:]
         cs[i] = d.commit_step
         fw[i] = d.forwards
-    return BatchResult(toks, cs, fw, steps)
+        part += d.part
+    return BatchResult(toks, cs, fw, steps, part)

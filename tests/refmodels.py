@@ -187,7 +187,8 @@ def torch_causal_logits(cfg, ws, tokens):
 
 
 # ---------------------------------------------------------------- brute decode
-def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward, tau_semi=None, tau_add=0.0):
+def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward, tau_semi=None, tau_add=0.0,
+                 skip_masked=False, counters=None):
     """Decode by recomputing the whole sequence every step.
 
     Block k of the generation is committed once it and all blocks before it
@@ -199,7 +200,15 @@ def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward, tau_sem
     or had at least the fraction tau_semi of its positions unmasked when the
     step began.  A further block is admitted while fewer than nb are active
     and either none is active or the last admitted one has at least the
-    fraction tau_add of its positions unmasked (fractions in float32)."""
+    fraction tau_add of its positions unmasked (fractions in float32).
+    With ``skip_masked`` an active block other than the first one that has
+    no unmasked position yet stays out of the step.  ``counters`` (a dict)
+    receives, summed over steps: "active_forwards" (active blocks in the
+    step), "zero_commit" (of those, ones that commit nothing),
+    "static_saved" / "static_deferred" (of those, ones other than the first
+    active block with nothing unmasked before the step that commit nothing /
+    something), "cache_writes" (blocks committed in the previous step, which
+    this step recomputes) and "skipped" (active blocks left out)."""
     P = len(prompt)
     tokens = list(prompt) + [cfg.mask_id] * G
     nblk = G // B
@@ -219,10 +228,19 @@ def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward, tau_sem
     commit_step = [-1] * G
     steps = 0
     tau32 = float(np.float32(tau))
+    cnt = {k: 0 for k in ("active_forwards", "zero_commit", "static_saved", "static_deferred",
+                          "cache_writes", "skipped")}
+    newly_committed = 0
     while committed < nblk:
-        end = P + admitted * B
+        live = [k for k in range(committed, admitted)
+                if not (skip_masked and k > committed and unmasked(k) == 0)]
+        cnt["skipped"] += (admitted - committed) - len(live)
+        cnt["cache_writes"] += newly_committed
+        before = {k: unmasked(k) for k in live}
+        end = P + (live[-1] + 1) * B
         z = forward(cfg, ws, tokens[:end], B)
-        cand = [p for p in range(P + committed * B, end) if tokens[p] == cfg.mask_id]
+        cand = [p for p in range(P + committed * B, end)
+                if tokens[p] == cfg.mask_id and (p - P) // B in live]
         stats = []
         for p in cand:
             row = z[p]
@@ -247,8 +265,18 @@ def brute_decode(cfg, ws, prompt, G, B, nb, tau, forward=scalar_forward, tau_sem
         for i in chosen:
             tokens[cand[i]] = stats[i][1]
             commit_step[cand[i] - P] = steps
+        for k in live:
+            n = sum(1 for i in chosen if (cand[i] - P) // B == k)
+            cnt["active_forwards"] += 1
+            cnt["zero_commit"] += n == 0
+            if k > committed and before[k] == 0:
+                cnt["static_saved" if n == 0 else "static_deferred"] += 1
+        was = committed
         while committed < admitted and cfg.mask_id not in tokens[P + committed * B:P + (committed + 1) * B]:
             committed += 1
+        newly_committed = committed - was
         admitted = admit(committed, admitted)
         steps += 1
+    if counters is not None:
+        counters.update(cnt)
     return np.array(tokens[P:]), np.array(commit_step), steps

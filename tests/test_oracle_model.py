@@ -11,7 +11,7 @@ import torch
 
 from oracle.model import OracleModel, round_bf16, lm_stats
 from oracle.decode import (SeqDecoder, decode_batch, commit_set, ACTIVE, PENDING, CACHED,
-                           PLACEHOLDER)
+                           PLACEHOLDER, PART_NAMES)
 from tests.refmodels import TinyCfg, tiny_weights, scalar_forward, torch_causal_logits, brute_decode
 
 
@@ -225,6 +225,106 @@ def test_add_one_or_single_block_reduces_to_one_block_decoding(tau):
         np.testing.assert_array_equal(r.tokens, base.tokens)
     r = decode_batch(m, prompts, G, B, 1, tau, tau_semi=0.9, tau_add=0.3)
     np.testing.assert_array_equal(r.commit_step, base.commit_step)
+
+
+# ------------------------------------------- static skip rule and participation
+SKIP_CASES = [(P, B, nb, tau, ts, skip) for B in (1, 2, 4) for P in range(0, 8 - B, B) for nb in (2, 3)
+              for tau in (0.0, 0.5, 0.9, 2.0) for ts in (None, 0.5) for skip in (False, True)]
+
+
+@pytest.mark.parametrize("P,B,nb,tau,tau_semi,skip", SKIP_CASES)
+def test_participation_and_skip_match_brute_force(P, B, nb, tau, tau_semi, skip):
+    """Participation counters (App. "Participation schedules") and the live
+    static skip rule (§3 "The allocation lever"): cached oracle decode = full
+    recomputation with the rule and the counts restated independently."""
+    G = 8 - P
+    cfg, ws, m = _model(TinyCfg())
+    prompt = np.random.default_rng(P * 100 + B + 11).integers(0, cfg.vocab - 1, P)
+    cnt = {}
+    bt, bs, bsteps = brute_decode(cfg, ws, list(prompt), G, B, nb, tau, tau_semi=tau_semi,
+                                  skip_masked=skip, counters=cnt)
+    r = decode_batch(m, prompt[None, :], G, B, nb, tau, tau_semi=tau_semi, skip_masked=skip)
+    np.testing.assert_array_equal(r.tokens[0], bt)
+    np.testing.assert_array_equal(r.commit_step[0], bs)
+    assert r.forwards[0] == bsteps
+    assert dict(zip(PART_NAMES, r.participation.tolist())) == cnt
+
+
+def _sweep_steps(commit_step, B):
+    """Step at which each block leaves the active set: the latest commit of
+    the block and of every block before it (in-order sweep)."""
+    last = commit_step.reshape(-1, B).max(axis=1)
+    return np.maximum.accumulate(last)
+
+
+@pytest.mark.parametrize("nb,tau,ts", [(2, 0.5, None), (3, 0.8, None), (2, 0.8, 0.6), (3, 2.0, None),
+                                       (3, 0.3, 0.0)])
+def test_skip_rule_reduces_to_one_block_in_flight(nb, tau, ts):
+    """A fully masked block can only gain a token by being forwarded, and the
+    skip rule forwards it only once no older block is active; so only the
+    oldest active block ever takes part and the decode is the n_inflight = 1
+    decode, position by position, while the n_inflight - 1 admitted blocks
+    behind it are skipped at every step where they exist."""
+    cfg, ws, m = _model(TinyCfg(vocab=31), seed=5, std=0.4)
+    P, G, B = 4, 32, 4
+    prompts = np.random.default_rng(19).integers(0, cfg.vocab - 1, (3, P))
+    base = decode_batch(m, prompts, G, B, 1, tau, tau_semi=ts)
+    r = decode_batch(m, prompts, G, B, nb, tau, tau_semi=ts, skip_masked=True)
+    np.testing.assert_array_equal(r.tokens, base.tokens)
+    np.testing.assert_array_equal(r.commit_step, base.commit_step)
+    np.testing.assert_array_equal(r.forwards, base.forwards)
+    part = dict(zip(PART_NAMES, r.participation.tolist()))
+    assert part["active_forwards"] == int(base.forwards.sum())
+    assert part["static_saved"] == part["static_deferred"] == 0
+    # skipped: at each step min(nb, blocks not yet swept) - 1 blocks wait
+    nblk = G // B
+    expect = 0
+    for i in range(len(prompts)):
+        sw = _sweep_steps(r.commit_step[i], B)
+        for t in range(int(r.forwards[i])):
+            left = nblk - int(np.count_nonzero(sw < t))
+            expect += min(nb, left) - 1
+    assert part["skipped"] == expect
+
+
+@pytest.mark.parametrize("nb,tau,ts", [(1, 0.7, None), (2, 0.7, None), (3, 0.5, 0.5), (2, 0.0, None),
+                                       (3, 2.0, None), (1, 2.0, None)])
+def test_participation_closed_forms(nb, tau, ts):
+    """Counter identities that follow from the rules alone:
+    * every step of a sequence forwards each active block once, so the active
+      block-forwards are the sum over steps of the blocks neither swept nor
+      unadmitted, min(nb, blocks not yet swept) without admission thresholds;
+    * cache writes: every block swept before a sequence's final step is
+      recomputed by the next one (App. G.2);
+    * n_inflight = 1: no block has an older active block;
+    * tau > 1 without semi-completion: exactly one block commits per step,
+      so the zero-commit forwards are the active forwards minus the forwards;
+    * tau = 0: every forwarded block resolves at once, so none commits
+      nothing and each block is forwarded once while active."""
+    cfg, ws, m = _model(TinyCfg(vocab=31), seed=5, std=0.4)
+    P, G, B = 4, 24, 4
+    prompts = np.random.default_rng(23).integers(0, cfg.vocab - 1, (3, P))
+    r = decode_batch(m, prompts, G, B, nb, tau, tau_semi=ts)
+    part = dict(zip(PART_NAMES, r.participation.tolist()))
+    nblk = G // B
+    act = cw = 0
+    for i in range(len(prompts)):
+        sw = _sweep_steps(r.commit_step[i], B)
+        final = int(r.forwards[i]) - 1
+        assert sw.max() == final
+        cw += int(np.count_nonzero(sw < final))
+        for t in range(int(r.forwards[i])):
+            act += min(nb, nblk - int(np.count_nonzero(sw < t)))
+    assert part["active_forwards"] == act
+    assert part["cache_writes"] == cw
+    assert part["skipped"] == 0
+    if nb == 1:
+        assert part["static_saved"] == part["static_deferred"] == 0
+    if tau > 1 and ts is None:
+        assert part["zero_commit"] == act - int(r.forwards.sum())
+    if tau == 0:
+        assert part["zero_commit"] == 0 and act == nblk * len(prompts)
+    assert part["static_saved"] + part["static_deferred"] <= part["active_forwards"]
 
 
 # ---------------------------------------------------------------- P2: causal decoding

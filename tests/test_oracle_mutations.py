@@ -94,6 +94,23 @@ def _apply_skip_cache_write(self, positions, toks, step):
     self.forwards += 1
 
 
+def _count_static_oldest(self, committed):
+    # counts the oldest active block as one the skip rule could leave out
+    act = np.nonzero(self.status == od.ACTIVE)[0]
+    blk = (np.asarray(committed, dtype=np.int64) - self.P) // self.B
+    for b in act:
+        n_commit = int(np.count_nonzero(blk == int(b)))
+        self.part[0] += 1
+        self.part[1] += n_commit == 0
+        if self.resolved(int(b)) == 0:
+            self.part[2 if n_commit == 0 else 3] += 1
+    self.part[4] += int(np.count_nonzero(self.status == od.PENDING))
+
+
+def _forward_ignores_skip(self):
+    return np.nonzero(self.status == od.ACTIVE)[0]
+
+
 MUTATIONS = {
     "rope_sign": ("OracleModel.rope", _rope_wrong_sign),
     "mask_strict": ("OracleModel.attention", _attention_strict_mask),
@@ -103,6 +120,8 @@ MUTATIONS = {
     "forced_top1_last": ("commit_set", _commit_last_argmax),
     "sweep_no_chain": ("SeqDecoder.apply", _apply_no_chain),
     "cache_write_early": ("SeqDecoder.apply", _apply_skip_cache_write),
+    "static_counts_oldest": ("SeqDecoder.count_participation", _count_static_oldest),
+    "skip_not_applied": ("SeqDecoder.forwarded", _forward_ignores_skip),
 }
 
 
@@ -134,6 +153,15 @@ def _run_pins():
         bt, bs, steps = brute_decode(cfg, ws, list(prompt), G, B, nb, tau)
         r = od.decode_batch(m, prompt[None], G, B, nb, tau)
         if not (np.array_equal(r.tokens[0], bt) and np.array_equal(r.commit_step[0], bs)):
+            return False
+    for skip in (False, True):
+        prompt = np.random.default_rng(5).integers(0, cfg.vocab - 1, 2)
+        cnt = {}
+        bt, bs, steps = brute_decode(cfg, ws, list(prompt), 6, 2, 3, 0.5, skip_masked=skip,
+                                     counters=cnt)
+        r = od.decode_batch(m, prompt[None], 6, 2, 3, 0.5, skip_masked=skip)
+        if not (np.array_equal(r.commit_step[0], bs)
+                and dict(zip(od.PART_NAMES, r.participation.tolist())) == cnt):
             return False
     return True
 
