@@ -94,7 +94,7 @@ def measured_traffic(workload_name, kernel_class):
             "launches": rec["launches"]}
 
 
-def cpu_baseline(w, weights, prompts, tau, target_s=12.0, tau_semi=None, tau_add=0.0):
+def cpu_baseline(w, weights, prompts, tau, target_s=12.0, tau_semi=None, tau_add=0.0, skip_masked=False):
     """The oracle as it stands, on the host cores, over whole sequences of the
     same batch until about ``target_s`` seconds of decode work (prefill
     excluded, as on the GPU)."""
@@ -109,7 +109,8 @@ def cpu_baseline(w, weights, prompts, tau, target_s=12.0, tau_semi=None, tau_add
     om = OracleModel(w, weights, "f64" if w.dtype == "f32" else "bf16")
     spent, tokens, seqs = 0.0, 0, 0
     for i in range(prompts.shape[0]):
-        d = SeqDecoder(om, prompts[i], w.gen_len, w.block_size, w.n_inflight, tau, tau_semi, tau_add)
+        d = SeqDecoder(om, prompts[i], w.gen_len, w.block_size, w.n_inflight, tau, tau_semi, tau_add,
+                       skip_masked)
         d.prefill()
         t0 = time.perf_counter()
         s = 0
@@ -137,6 +138,8 @@ def main():
                     help="semi-completion threshold (default: off)")
     ap.add_argument("--tau-add", type=float, default=0.0,
                     help="admission threshold (default 0: refill every free slot)")
+    ap.add_argument("--skip-masked", action="store_true",
+                    help="static skip rule: leave fully masked blocks behind an active one out of the forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--trace-steps", type=int, default=0, metavar="N",
@@ -171,7 +174,7 @@ def main():
     prompts = make_prompts(w)
     model = bd.Model(w, weights)
     st = bd.State(model, prompts, w.gen_len, args.tau, w.n_inflight, w.block_size, args.tau_semi,
-                  args.tau_add)
+                  args.tau_add, args.skip_masked)
     if args.trace_steps:
         torch.cuda.synchronize()
         print(f"[bench] prefill done; running {args.trace_steps} denoising steps", file=sys.stderr, flush=True)
@@ -257,7 +260,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, weights, prompts, args.tau, args.cpu_seconds, args.tau_semi, args.tau_add)
+        cpu = cpu_baseline(w, weights, prompts, args.tau, args.cpu_seconds, args.tau_semi, args.tau_add,
+                           args.skip_masked)
 
     line = {
         "metric": "committed tokens/sec/GPU (TPF at tau=0.9; step latency; HBM GB/s, MFMA util)",
@@ -267,9 +271,12 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "prompt_len": w.prompt_len, "gen_len": w.gen_len,
                    "block_size": w.block_size, "n_inflight": w.n_inflight, "tau": args.tau,
                    **({"tau_semi": args.tau_semi, "tau_add": args.tau_add}
-                      if args.tau_semi is not None or args.tau_add else {})},
+                      if args.tau_semi is not None or args.tau_add else {}),
+                   **({"skip_masked": True} if args.skip_masked else {})},
         "tpf": tpf, "denoise_steps_per_decode": S, "step_latency_us": 1e3 * ms / S,
         "wall_s": wall, "roofline": roof, "kernels": kernels, "cpu_baseline": cpu,
+        "participation": {k: stats[k] for k in ("active_forwards", "zero_commit", "static_saved",
+                                                "static_deferred", "cache_writes", "skipped")},
     }
     print(json.dumps(line))
     st.close()

@@ -82,6 +82,15 @@ typedef struct {
                               none is active or the youngest active block's
                               resolved fraction is >= tau_add; <= 0 refills
                               every free slot at once */
+    int32_t skip_masked;   /* static skip rule (§3 "The allocation lever"),
+                              0 or 1: 1 leaves an active block that is still
+                              fully masked at the start of a step out of that
+                              step's forward (no rows, no confidences, no
+                              commits) while an older block is active.  Such a
+                              block gains its first token only once it is the
+                              oldest active block, so with 1 the decode equals
+                              the n_inflight = 1 decode and the admitted blocks
+                              behind the oldest wait unforwarded. */
 } bd_decode_cfg;
 
 typedef struct bd_model bd_model;
@@ -127,7 +136,8 @@ bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev,
  *  forwards, App. G.1).  Afterwards the first min(n_inflight, G/B) blocks of
  *  every sequence are active and fully masked.
  *  Errors: BD_EINVAL if b < 1, P < 0, G < 1, B < 1, n_inflight < 1,
- *  P % B != 0, G % B != 0, tau is NaN, or a prompt id is outside [0, vocab)
+ *  P % B != 0, G % B != 0, tau is NaN, skip_masked not 0 or 1, or a prompt
+ *  id is outside [0, vocab)
  *  (checked on the device; reported by the next synchronising call).
  */
 bd_status bd_prefill(bd_model* model, const int32_t* prompt_dev, int32_t b, int32_t P, int32_t G,
@@ -192,12 +202,19 @@ bd_status bd_state_steps(const bd_state* st, int32_t* steps_out);
 
 /*
  * bd_state_stats -- work counters accumulated over the steps run since the
- *  prefill (or the last reset), copied to host out[0..n), n <= 8:
+ *  prefill (or the last reset), copied to host out[0..n), n <= 12:
  *   [0] forwards executed (steps with at least one row), [1] window rows
  *   forwarded (sum of M), [2] LM-head rows (masked positions), [3] visible
  *   query-key pairs per head (block-causal), [4] keys read per kv head
- *   (prefix + window, summed over sequences), [5] tokens committed.
- *  Synchronises the stream.
+ *   (prefix + window, summed over sequences), [5] tokens committed;
+ *   participation (App. "Participation schedules"), summed over sequences
+ *   and steps: [6] active block-forwards, [7] of those, forwards of a block
+ *   that commits nothing in the step, [8] forwards of a block that was fully
+ *   masked at the start of the step behind an older active block and commits
+ *   nothing (what the static skip rule saves), [9] the same with at least
+ *   one commit (what the rule defers), [10] blocks forwarded for their
+ *   one-step cache write, [11] active blocks left out by skip_masked.
+ *  Errors: BD_EINVAL for n outside [1, 12].  Synchronises the stream.
  */
 bd_status bd_state_stats(bd_model* model, bd_state* st, int64_t* out, int32_t n);
 

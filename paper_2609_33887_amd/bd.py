@@ -37,13 +37,19 @@ class bd_model_cfg(ctypes.Structure):
 
 class bd_decode_cfg(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("n_inflight", ctypes.c_int32), ("block_size", ctypes.c_int32),
-                ("tau_semi", ctypes.c_float), ("tau_add", ctypes.c_float)]
+                ("tau_semi", ctypes.c_float), ("tau_add", ctypes.c_float), ("skip_masked", ctypes.c_int32)]
 
 
-def decode_cfg(tau: float, n_inflight: int, block_size: int, tau_semi=None, tau_add: float = 0.0):
+def decode_cfg(tau: float, n_inflight: int, block_size: int, tau_semi=None, tau_add: float = 0.0,
+               skip_masked: bool = False):
     """The C configuration; ``tau_semi=None`` switches semi-completion off."""
     return bd_decode_cfg(tau=tau, n_inflight=n_inflight, block_size=block_size,
-                         tau_semi=-1.0 if tau_semi is None else tau_semi, tau_add=tau_add)
+                         tau_semi=-1.0 if tau_semi is None else tau_semi, tau_add=tau_add,
+                         skip_masked=1 if skip_masked else 0)
+
+
+STAT_NAMES = ("forwards", "rows", "lm_rows", "pairs", "keys", "committed", "active_forwards",
+              "zero_commit", "static_saved", "static_deferred", "cache_writes", "skipped")
 
 
 class BDError(RuntimeError):
@@ -156,9 +162,9 @@ def bd_state_steps(state: int) -> int:
 
 
 def bd_state_stats(model: int, state: int):
-    out = (ctypes.c_int64 * 8)()
-    _check(lib.bd_state_stats(model, state, out, 8))
-    return dict(zip(["forwards", "rows", "lm_rows", "pairs", "keys", "committed"], list(out)[:6]))
+    out = (ctypes.c_int64 * len(STAT_NAMES))()
+    _check(lib.bd_state_stats(model, state, out, len(STAT_NAMES)))
+    return dict(zip(STAT_NAMES, list(out)))
 
 
 def bd_profile(model: int, enable: bool):
@@ -336,13 +342,13 @@ class State:
     """A decode state of ``b`` sequences (prefill done on creation)."""
 
     def __init__(self, model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int,
-                 tau_semi=None, tau_add: float = 0.0):
+                 tau_semi=None, tau_add: float = 0.0, skip_masked: bool = False):
         torch = model.torch
         self.m = model
         self.prompts = torch.as_tensor(prompts, dtype=torch.int32).to(model.device).contiguous()
         self.b, self.P = self.prompts.shape
         self.G = G
-        self.cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add)
+        self.cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add, skip_masked)
         self.handle = bd_prefill(model.handle, self.prompts.data_ptr(), self.b, self.P, G, self.cfg)
 
     def step(self, conf=None, tok=None, logits=None):
@@ -383,7 +389,7 @@ class State:
 
 
 def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int, tau_semi=None,
-           tau_add: float = 0.0):
+           tau_add: float = 0.0, skip_masked: bool = False):
     """Whole decode through ``bd_decode``; returns numpy (tokens, commit_step, forwards)."""
     torch = model.torch
     pr = torch.as_tensor(prompts, dtype=torch.int32).to(model.device).contiguous()
@@ -391,6 +397,6 @@ def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_siz
     t = torch.empty((b, G), dtype=torch.int32, device=model.device)
     c = torch.empty((b, G), dtype=torch.int32, device=model.device)
     f = torch.empty((b,), dtype=torch.int32, device=model.device)
-    cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add)
+    cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add, skip_masked)
     bd_decode(model.handle, pr.data_ptr(), b, P, G, cfg, t.data_ptr(), c.data_ptr(), f.data_ptr())
     return t.cpu().numpy(), c.cpu().numpy(), f.cpu().numpy()

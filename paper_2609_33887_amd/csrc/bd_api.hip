@@ -114,6 +114,7 @@ struct bd_state {
   int b, P, G, B, nb;
   float tau;
   int semi_min, add_min;   // thresholds as resolved counts (see min_resolved)
+  int skip;                // static skip rule on
   int maxpos, rows_step, rows_pre, rows_cap, lm_cap, win_step;
   int32_t *tokens, *commit_step, *seq_state, *commit_flag;
   int32_t* plan_buf[3];
@@ -152,7 +153,7 @@ struct bd_state {
   int steps;
   bool pending;
   int32_t* host_flag;    // pinned
-  long long* stats;      // device [8]
+  long long* stats;      // device [BD_NSTATS]
   std::vector<void*> allocs;
 };
 
@@ -476,6 +477,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   if (P % B || G % B) return fail(BD_EINVAL, "P and G must be multiples of the block size");
   if (isnan(cfg->tau) || isnan(cfg->tau_semi) || isnan(cfg->tau_add))
     return fail(BD_EINVAL, "tau, tau_semi or tau_add is NaN");
+  if (cfg->skip_masked != 0 && cfg->skip_masked != 1) return fail(BD_EINVAL, "skip_masked must be 0 or 1");
   if (P > 0 && !prompt) return fail(BD_EINVAL, "NULL prompt");
   if (b > 256) return fail(BD_EUNSUPPORTED, "at most 256 sequences per state");
   if (nb > 8) return fail(BD_EUNSUPPORTED, "at most 8 in-flight blocks");
@@ -485,6 +487,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   s->b = b; s->P = P; s->G = G; s->B = B; s->nb = nb; s->tau = cfg->tau;
   s->semi_min = cfg->tau_semi < 0.0f ? -1 : min_resolved(cfg->tau_semi, B);
   s->add_min = min_resolved(cfg->tau_add, B);
+  s->skip = cfg->skip_masked;
   s->maxpos = P + G;
   s->win_step = 2 * nb * B;
   s->rows_step = round_up(b * s->win_step, 256);
@@ -506,7 +509,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ALLOC(s->tokens, (size_t)b * (P + G) * 4);
   ALLOC(s->commit_step, (size_t)b * G * 4);
   ALLOC(s->seq_state, (size_t)b * SS_N * 4);
-  ALLOC(s->stats, 8 * sizeof(long long));
+  ALLOC(s->stats, BD_NSTATS * sizeof(long long));
   ALLOC(s->commit_flag, (size_t)s->lm_cap * 4);
   for (int i = 0; i < 3; ++i) {
     const int rc = i < 2 ? s->rows_step : s->rows_pre;
@@ -604,6 +607,7 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ia.seq_state = s->seq_state;
   ia.b = b; ia.P = P; ia.G = G; ia.B = B; ia.nb = nb; ia.mask_id = c.mask_id; ia.vocab = c.vocab;
   ia.add_min = s->add_min;
+  ia.skip = s->skip;
   ia.err_flag = m->err_flag;
   ia.stats = s->stats;
   e = launch_init_decode(ia, m->stream);
@@ -634,6 +638,7 @@ extern "C" bd_status bd_state_reset(bd_model* m, bd_state* s) {
   ia.commit_step = s->commit_step;
   ia.seq_state = s->seq_state;
   ia.b = s->b; ia.P = s->P; ia.G = s->G; ia.B = s->B; ia.nb = s->nb; ia.add_min = s->add_min;
+  ia.skip = s->skip;
   ia.mask_id = m->cfg.mask_id; ia.vocab = m->cfg.vocab; ia.err_flag = m->err_flag;
   ia.stats = s->stats;
   HIPCHK(launch_init_decode(ia, m->stream));
@@ -692,6 +697,7 @@ extern "C" bd_status bd_commit(bd_model* m, bd_state* s, int32_t* all_done_host)
   a.tau = s->tau;
   a.semi_min = s->semi_min;
   a.add_min = s->add_min;
+  a.skip = s->skip;
   a.stats = s->stats;
   LAUNCH(BD_PROF_COMMIT, launch_commit(a, m->stream));
   s->cur ^= 1;
@@ -757,8 +763,8 @@ extern "C" bd_status bd_decode(bd_model* m, const int32_t* prompt, int32_t b, in
 }
 
 extern "C" bd_status bd_state_stats(bd_model* m, bd_state* s, int64_t* out, int32_t n) {
-  if (!m || !s || !out || n < 1 || n > 8) return fail(BD_EINVAL, "bad arguments");
-  long long tmp[8];
+  if (!m || !s || !out || n < 1 || n > BD_NSTATS) return fail(BD_EINVAL, "bad arguments");
+  long long tmp[BD_NSTATS];
   HIPCHK(hipMemcpyAsync(tmp, s->stats, sizeof tmp, hipMemcpyDeviceToHost, m->stream));
   HIPCHK(hipStreamSynchronize(m->stream));
   for (int i = 0; i < n; ++i) out[i] = (int64_t)tmp[i];

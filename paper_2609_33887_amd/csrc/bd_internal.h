@@ -24,6 +24,7 @@ enum {
   SS_NEXT_BLK = 4,    // first block not yet admitted
   SS_DONE = 5,
   SS_FORWARDS = 6,
+  SS_N_FWD = 7,       // active blocks the next forward takes (the first ones)
   SS_N = 8
 };
 
@@ -229,6 +230,8 @@ hipError_t launch_rmsnorm(bool is_bf16, float* X, const float* g, int d, float e
 hipError_t launch_rope_kv(const float* QKV, PlanView plan, int rows_cap, int H, int Hkv, int hd,
                           const double* inv_freq, float* Q, const KvView& kv, hipStream_t st);
 
+constexpr int BD_NSTATS = 12;
+
 struct CommitArgs {
   PlanView in, out;
   const float* conf;        // [lm rows of `in`]
@@ -238,11 +241,12 @@ struct CommitArgs {
   int32_t* commit_step;     // [b][G]
   int32_t* seq_state;       // [b][SS_N]
   int32_t* commit_flag;     // scratch [lm_cap]
-  long long* stats;         // [8] work counters of the executed steps
+  long long* stats;         // [BD_NSTATS] work and participation counters of the executed steps
   int b, P, G, B, nb, mask_id, step;
   float tau;
   int semi_min;             // semi-completion: resolved count that fully activates the next block; -1 = off
   int add_min;              // admission: resolved count of the youngest active block that admits the next
+  int skip;                 // static skip rule: leave fully masked blocks behind an active one out
 };
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 
@@ -255,8 +259,9 @@ struct InitArgs {
   int32_t* seq_state;
   int b, P, G, B, nb, mask_id, vocab;
   int add_min;              // as in CommitArgs
+  int skip;                 // as in CommitArgs
   int32_t* err_flag;
-  long long* stats;         // [8], cleared
+  long long* stats;         // [BD_NSTATS], cleared
 };
 hipError_t launch_init_decode(const InitArgs& a, hipStream_t st);
 

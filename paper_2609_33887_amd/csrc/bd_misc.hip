@@ -245,15 +245,22 @@ __device__ __forceinline__ int wave_popc(bool p) { return __popcll(__ballot(p));
 
 // Single workgroup; wave w owns sequences w, w + 16, ...
 //  phase 1: commit rule, token/commit-step writes, per-block resolution counts,
-//           cache write of the pending blocks, in-order sweep, admission;
+//           cache write of the pending blocks, in-order sweep, admission,
+//           the blocks the next forward takes, participation counts;
 //  phase 2: prefix sums of the next window sizes and masked-row counts;
-//  phase 3: the next step plan (rows = [pending blocks][active blocks],
-//           masked rows ascending).
+//  phase 3: the next step plan (rows = [pending blocks][forwarded active
+//           blocks], masked rows ascending).
+// The forwarded active blocks are always the first n_fwd of the active list:
+// all of them, or under the static skip rule the oldest one and the ones
+// after it that already hold a resolved position (a fully masked block can
+// only gain one by being forwarded, so they form a prefix).
 __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
   __shared__ int s_win[MAXB], s_lm[MAXB], s_rs[MAXB], s_ls[MAXB];
-  __shared__ int s_cl[MAXB], s_fa[MAXB], s_sw[MAXB], s_nb0[MAXB], s_adm[MAXB], s_lmn[MAXB], s_lm0[MAXB];
+  __shared__ int s_cl[MAXB], s_fa[MAXB], s_sw[MAXB], s_nf[MAXB], s_full0[MAXB], s_nfull[MAXB], s_lmn[MAXB],
+      s_lm0[MAXB];
   __shared__ long long s_pairs[MAXB], s_keys[MAXB];
   __shared__ int s_ncommit[MAXB];
+  __shared__ int s_part[MAXB][6];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
   const int P = a.P, G = a.G, B = a.B;
 
@@ -264,11 +271,13 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
     const int lmn = done ? 0 : a.in.seq_lm_cnt[s];
     int cache_len = ss[SS_CACHE_LEN], n_pend = ss[SS_N_PEND], first_act = ss[SS_FIRST_ACT];
     int n_act = ss[SS_N_ACT], next_blk = ss[SS_NEXT_BLK];
+    const int n_fwd = ss[SS_N_FWD];
     if (done) {
       if (lane == 0) {
         s_win[s] = 0; s_lm[s] = 0; s_cl[s] = cache_len; s_fa[s] = first_act; s_sw[s] = 0;
-        s_nb0[s] = next_blk; s_adm[s] = 0; s_lmn[s] = 0; s_lm0[s] = lm0;
+        s_nf[s] = 0; s_full0[s] = 0; s_nfull[s] = 0; s_lmn[s] = 0; s_lm0[s] = lm0;
         s_pairs[s] = 0; s_keys[s] = 0; s_ncommit[s] = 0;
+        for (int q = 0; q < 6; ++q) s_part[s][q] = 0;
       }
       continue;
     }
@@ -301,7 +310,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < MAXNB; ++k) {
-        if (k >= n_act) break;                 // wave-uniform
+        if (k >= n_fwd) break;                 // wave-uniform
         const bool mine = valid && kb == k;
         blk_masked[k] += wave_popc(mine);
         blk_any[k] |= mine && cf >= a.tau;
@@ -313,7 +322,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < MAXNB; ++k) {
-      if (k >= n_act) break;
+      if (k >= n_fwd) break;
       blk_any[k] = __ballot(blk_any[k]) != 0;
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
@@ -325,6 +334,10 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
         }
       }
     }
+    // blocks left out of the forward are fully masked
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k)
+      if (k >= n_fwd && k < n_act) blk_masked[k] = B;
     // forced commits.  Semi-completion off: one per sequence when no position
     // clears tau, the most confident over all blocks (blocks are in position
     // order, so the first block holding the maximum has its lowest position).
@@ -341,7 +354,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
 #pragma unroll
       for (int k = 0; k < MAXNB; ++k) {
         any |= blk_any[k];
-        if (k < n_act && blk_masked[k] > 0 && (bp < 0 || blk_best[k] > best)) {
+        if (k < n_fwd && blk_masked[k] > 0 && (bp < 0 || blk_best[k] > best)) {
           best = blk_best[k];
           bp = blk_best_pos[k];
         }
@@ -351,7 +364,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
 #pragma unroll
       for (int k = 0; k < MAXNB; ++k) {
         const bool full = k == 0 || (B - blk_masked[k > 0 ? k - 1 : 0]) >= a.semi_min;
-        if (k < n_act && blk_masked[k] > 0 && full && !blk_any[k]) forced_pos[k] = blk_best_pos[k];
+        if (k < n_fwd && blk_masked[k] > 0 && full && !blk_any[k]) forced_pos[k] = blk_best_pos[k];
       }
     }
     // pass 2: commit, and count committed positions per active block
@@ -389,11 +402,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
 #pragma unroll
     for (int k = 0; k < MAXNB; ++k)
       if (sw == k && k < n_act && blk_masked[k] == blk_commit[k]) sw = k + 1;
-    int left = 0;
-#pragma unroll
-    for (int k = 0; k < MAXNB; ++k)
-      if (k >= sw && k < n_act) left += blk_masked[k] - blk_commit[k];
-    const int first_act_old = first_act, next_blk_old = next_blk;
+    const int first_act_old = first_act, n_act_old = n_act;
     first_act += sw;
     n_act -= sw;
     const int nblk = G / B;
@@ -403,12 +412,45 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
 #pragma unroll
     for (int k = 0; k < MAXNB; ++k)
       if (k == sw + n_act - 1) young = B - (blk_masked[k] - blk_commit[k]);
-    int adm = 0;
     while (n_act < a.nb && next_blk < nblk && (n_act == 0 || young >= a.add_min)) {
-      ++n_act; ++next_blk; ++adm;
+      ++n_act; ++next_blk;
       young = 0;
     }
     const int now_done = (n_act == 0);
+    // blocks of the next forward: pre-sweep blocks sw .. sw + nf - 1, those
+    // past n_act_old being newly admitted (fully masked)
+    int nf = n_act;
+    if (a.skip && n_act > 0) {
+      nf = 1;
+      bool run = true;
+#pragma unroll
+      for (int k = 0; k < MAXNB; ++k) {
+        if (run && k > sw && k < n_act_old) {
+          if (blk_masked[k] - blk_commit[k] < B) ++nf;
+          else run = false;
+        }
+      }
+    }
+    // masked rows of the next forward: the unresolved positions of blocks
+    // forwarded this step, then whole blocks that were not
+    int left = 0;
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k)
+      if (k >= sw && k < sw + nf && k < n_fwd) left += blk_masked[k] - blk_commit[k];
+    const int full0 = sw > n_fwd ? sw : n_fwd;
+    const int nfull = sw + nf - full0 > 0 ? sw + nf - full0 : 0;
+    // participation of the forward just executed
+    int p_zero = 0, p_save = 0, p_defer = 0;
+#pragma unroll
+    for (int k = 0; k < MAXNB; ++k) {
+      if (k < n_fwd) {
+        p_zero += blk_commit[k] == 0;
+        if (k > 0 && blk_masked[k] == B) {
+          if (blk_commit[k] == 0) ++p_save;
+          else ++p_defer;
+        }
+      }
+    }
     if (lane == 0) {
       ss[SS_CACHE_LEN] = cache_len;
       ss[SS_N_PEND] = sw;
@@ -417,11 +459,15 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       ss[SS_NEXT_BLK] = next_blk;
       ss[SS_DONE] = now_done;
       ss[SS_FORWARDS] += 1;
-      s_win[s] = now_done ? 0 : (sw + n_act) * B;
-      s_lm[s] = now_done ? 0 : left + adm * B;
-      s_cl[s] = cache_len; s_fa[s] = first_act_old; s_sw[s] = sw; s_nb0[s] = next_blk_old;
-      s_adm[s] = adm; s_lmn[s] = now_done ? 0 : lmn; s_lm0[s] = lm0;
+      ss[SS_N_FWD] = now_done ? 0 : nf;
+      s_win[s] = now_done ? 0 : (sw + nf) * B;
+      s_lm[s] = now_done ? 0 : left + nfull * B;
+      s_cl[s] = cache_len; s_fa[s] = first_act_old; s_sw[s] = sw; s_nf[s] = nf;
+      s_full0[s] = first_act_old + full0; s_nfull[s] = now_done ? 0 : nfull;
+      s_lmn[s] = now_done ? 0 : lmn; s_lm0[s] = lm0;
       s_ncommit[s] = ncommit;
+      s_part[s][0] = n_fwd; s_part[s][1] = p_zero; s_part[s][2] = p_save; s_part[s][3] = p_defer;
+      s_part[s][4] = n_pend; s_part[s][5] = n_act_old - n_fwd;
     }
   }
   __syncthreads();
@@ -443,6 +489,11 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
     a.stats[3] += pairs;
     a.stats[4] += keys;
     a.stats[5] += nc;
+    for (int q = 0; q < 6; ++q) {
+      long long t = 0;
+      for (int s = 0; s < a.b; ++s) t += s_part[s][q];
+      a.stats[6 + q] += t;
+    }
   }
   __syncthreads();
   for (int s = wave; s < a.b; s += nw) {
@@ -455,7 +506,7 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       a.out.row_seq[rs + e] = s;
       a.out.row_pos[rs + e] = cl + e;
     }
-    const int lmn = s_lmn[s], lm0 = s_lm0[s], fa = s_fa[s], sw = s_sw[s];
+    const int lmn = s_lmn[s], lm0 = s_lm0[s], fa = s_fa[s], sw = s_sw[s], nf = s_nf[s];
     int w = 0;
     for (int base = 0; base < lmn; base += 64) {
       const int i = base + lane;
@@ -463,15 +514,16 @@ __global__ __launch_bounds__(1024) void k_commit(CommitArgs a) {
       int pos = 0;
       if (i < lmn) {
         pos = a.in.row_pos[a.in.lm_row[lm0 + i]];
-        keep = !a.commit_flag[lm0 + i] && ((pos - P) / B - fa) >= sw;
+        const int kb = (pos - P) / B - fa;
+        keep = !a.commit_flag[lm0 + i] && kb >= sw && kb < sw + nf;
       }
       const unsigned long long m = __ballot(keep);
       const int pre = __popcll(m & ((1ull << lane) - 1ull));
       if (keep) a.out.lm_row[ls + w + pre] = rs + (pos - cl);
       w += __popcll(m);
     }
-    const int adm = s_adm[s], p0 = P + s_nb0[s] * B;
-    for (int e = lane; e < adm * B; e += 64) a.out.lm_row[ls + w + e] = rs + (p0 + e - cl);
+    const int nfull = s_nfull[s], p0 = P + s_full0[s] * B;
+    for (int e = lane; e < nfull * B; e += 64) a.out.lm_row[ls + w + e] = rs + (p0 + e - cl);
   }
 }
 
@@ -490,6 +542,7 @@ __global__ __launch_bounds__(1024) void k_init_decode(InitArgs a) {
   // ones while the youngest (nothing resolved yet) reaches add_min
   int nact = min(1, nblk);
   while (nact < a.nb && nact < nblk && 0 >= a.add_min) ++nact;
+  const int nfwd = a.skip ? min(nact, 1) : nact;     // admitted blocks are fully masked
   for (int s = wave; s < a.b; s += nw) {
     int32_t* t = a.tokens + (size_t)s * stride;
     if (a.prompt) {
@@ -506,8 +559,8 @@ __global__ __launch_bounds__(1024) void k_init_decode(InitArgs a) {
     if (lane == 0) {
       int32_t* ss = a.seq_state + s * SS_N;
       ss[SS_CACHE_LEN] = a.P; ss[SS_N_PEND] = 0; ss[SS_FIRST_ACT] = 0; ss[SS_N_ACT] = nact;
-      ss[SS_NEXT_BLK] = nact; ss[SS_DONE] = 0; ss[SS_FORWARDS] = 0; ss[7] = 0;
-      s_win[s] = nact * a.B;
+      ss[SS_NEXT_BLK] = nact; ss[SS_DONE] = 0; ss[SS_FORWARDS] = 0; ss[SS_N_FWD] = nfwd;
+      s_win[s] = nfwd * a.B;
     }
   }
   __syncthreads();
@@ -515,7 +568,7 @@ __global__ __launch_bounds__(1024) void k_init_decode(InitArgs a) {
     int r = 0;
     for (int s = 0; s < a.b; ++s) { s_rs[s] = r; r += s_win[s]; }
     a.plan.hdr[0] = r; a.plan.hdr[1] = r; a.plan.hdr[2] = (r == 0);
-    for (int k = 0; k < 8; ++k) a.stats[k] = 0;
+    for (int k = 0; k < BD_NSTATS; ++k) a.stats[k] = 0;
     if (a.prefill.hdr) {
       a.prefill.hdr[0] = a.b * a.P; a.prefill.hdr[1] = 0; a.prefill.hdr[2] = 0;
     }

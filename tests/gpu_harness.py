@@ -34,13 +34,14 @@ class GpuTrace:
     tokens: np.ndarray               # [b][G]
     commit_step: np.ndarray          # [b][G]
     forwards: np.ndarray             # [b]
+    stats: dict = None               # bd_state_stats after the decode
 
 
 def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=None, logit_steps=None,
-                      progress=None, tau_semi=None, tau_add=0.0):
+                      progress=None, tau_semi=None, tau_add=0.0, skip_masked=False):
     import torch
     from paper_2609_33887_amd import bd
-    st = bd.State(model, prompts, G, tau, nb, B, tau_semi, tau_add)
+    st = bd.State(model, prompts, G, tau, nb, B, tau_semi, tau_add, skip_masked)
     b = st.b
     dev = model.device
     V = model.w.vocab
@@ -71,8 +72,9 @@ def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=No
         if done:
             break
     tokens, cstep, fwd = st.read()
+    stats = st.stats()
     st.close()
-    return GpuTrace(steps, tokens, cstep, fwd)
+    return GpuTrace(steps, tokens, cstep, fwd, stats)
 
 
 @dataclass
@@ -85,17 +87,20 @@ class Report:
     t4: int = 0
     positions: int = 0
     failures: list = field(default_factory=list)
+    participation: dict = None       # oracle counters summed over the replayed sequences
+    complete: bool = True            # every replayed sequence ran to its end
 
 
 def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, conf_tol, logit_tol,
-             max_steps=None, progress=None, tau_semi=None, tau_add=0.0):
+             max_steps=None, progress=None, tau_semi=None, tau_add=0.0, skip_masked=False):
     """Replay the chosen sequences in the oracle against ``trace`` (the first
     ``max_steps`` steps of each when given)."""
-    from oracle.decode import SeqDecoder
+    from oracle.decode import SeqDecoder, PART_NAMES
     rep = Report()
+    part = np.zeros(len(PART_NAMES), dtype=np.int64)
     tau32 = float(np.float32(tau))
     for i in seq_ids:
-        d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau, tau_semi, tau_add)
+        d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau, tau_semi, tau_add, skip_masked)
         if progress:
             progress(f"  oracle prefill of sequence {i}")
         d.prefill()
@@ -117,6 +122,7 @@ def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, con
             if gaps and min(float(np.min(g)) for g in gaps) <= ROUTER_NEAR:
                 rep.t4 += 1
                 gsel = trace.commit_step[i, masked - P] == step
+                d.count_participation(masked[gsel])
                 d.apply(masked[gsel], trace.tokens[i, masked - P][gsel], step)
                 step += 1
                 continue
@@ -156,10 +162,14 @@ def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, con
                     rep.t2 += 1
                 else:
                     rep.failures.append((i, step, f"token differs at position {masked[k] - P}"))
+            d.count_participation(masked[gsel])
             d.apply(masked[gsel], gtoks[gsel], step)
             step += 1
         if d.done and d.forwards != trace.forwards[i]:
             rep.failures.append((i, step, f"forwards {d.forwards} vs GPU {trace.forwards[i]}"))
         if d.done and not np.array_equal(d.tokens[P:], trace.tokens[i]):
             rep.failures.append((i, step, "final tokens differ"))
+        rep.complete &= bool(d.done)
+        part += d.part
+    rep.participation = dict(zip(PART_NAMES, part.tolist()))
     return rep

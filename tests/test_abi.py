@@ -26,6 +26,33 @@ def test_library_exports_every_declared_symbol():
     assert sorted(bd.EXPORTED) == names
 
 
+def test_binding_structs_match_the_header(tmp_path):
+    """The ctypes mirrors of bd_model_cfg and bd_decode_cfg have the sizes
+    and field offsets the C compiler gives the header's structs."""
+    import ctypes
+    import subprocess
+    from paper_2609_33887_amd import bd
+    fields = {"bd_model_cfg": [f[0] for f in bd.bd_model_cfg._fields_],
+              "bd_decode_cfg": [f[0] for f in bd.bd_decode_cfg._fields_]}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "bd.h"', "int main(void) {"]
+    for t, fs in fields.items():
+        lines.append(f'  printf("{t} %zu\\n", sizeof({t}));')
+        for f in fs:
+            lines.append(f'  printf("{t}.{f} %zu\\n", offsetof({t}, {f}));')
+    lines.append("  return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = dict(l.split() for l in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                 text=True).stdout.splitlines())
+    for t, fs in fields.items():
+        cls = getattr(bd, t)
+        assert int(out[t]) == ctypes.sizeof(cls), t
+        for f in fs:
+            assert int(out[f"{t}.{f}"]) == getattr(cls, f).offset, (t, f)
+
+
 def test_redline_matches_oracle_on_paper_tables():
     from paper_2609_33887_amd import bd
     from oracle import redline as rl

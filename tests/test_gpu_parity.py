@@ -74,27 +74,33 @@ def get_model(w):
 
 
 def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None, tau_semi=None,
-               tau_add=0.0):
+               tau_add=0.0, skip_masked=False):
     from oracle.model import OracleModel
     from tests.gpu_harness import capture_gpu_trace, lockstep
     _need_gpu()
     _say(f"[parity] {w.name} tau={tau} b={w.batch} P={w.prompt_len} G={w.gen_len} B={w.block_size} "
-         f"nb={w.n_inflight} tau_semi={tau_semi} tau_add={tau_add}")
+         f"nb={w.n_inflight} tau_semi={tau_semi} tau_add={tau_add} skip={skip_masked}")
     model, ws = get_model(w)
     prompts = make_prompts(w)
     ids = list(range(w.batch)) if seq_ids is None else list(seq_ids)
     tr = capture_gpu_trace(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size,
                            logits_for=set(ids) if logits else (), logit_steps=logit_steps, progress=_say,
-                           tau_semi=tau_semi, tau_add=tau_add)
+                           tau_semi=tau_semi, tau_add=tau_add, skip_masked=skip_masked)
     om = OracleModel(w, ws, "f64" if w.dtype == "f32" else "bf16")
     rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, w.n_inflight, w.block_size, *TOL[w.dtype],
-                   max_steps=max_steps, progress=_say, tau_semi=tau_semi, tau_add=tau_add)
+                   max_steps=max_steps, progress=_say, tau_semi=tau_semi, tau_add=tau_add,
+                   skip_masked=skip_masked)
     ctol, ltol = TOL[w.dtype]
     _say(f"  positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} max|dlogit|={rep.max_logit_diff:.3g} "
          f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} T4(steps)={rep.t4} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
     assert not rep.failures, rep.failures[:5]
     assert rep.max_conf_diff <= ctol
     assert rep.max_logit_diff <= ltol
+    if rep.complete and len(ids) == w.batch:
+        # participation counters (App. "Participation schedules"): bit-exact
+        gp = {k: tr.stats[k] for k in rep.participation}
+        _say(f"  participation GPU {gp}")
+        assert gp == rep.participation, (gp, rep.participation)
     return tr, rep
 
 
@@ -138,6 +144,52 @@ def test_config2_multiblock_semi_add():
     run_parity(workload(2), 0.9, seq_ids=[5], max_steps=16, logit_steps=2, tau_semi=0.7, tau_add=0.1)
 
 
+@pytest.mark.parametrize("name", ["mha64", "gqa128_ragged", "moe", "f32_gqa"])
+@pytest.mark.parametrize("tau,tau_semi", [(0.9, None), (0.7, None), (0.85, 0.7)])
+def test_small_models_static_skip(name, tau, tau_semi):
+    """Static skip rule (§3 "The allocation lever"): parity with the oracle's
+    skip rule and its participation counters, and the closed form that
+    follows from the rule -- the decode is the one-block-in-flight decode,
+    bit for bit, with the admitted blocks behind the oldest never forwarded."""
+    from tests.gpu_harness import capture_gpu_trace
+    w = SMALL[name]
+    tr, rep = run_parity(w, tau, logits=False, tau_semi=tau_semi, skip_masked=True)
+    model, _ = get_model(w)
+    one = capture_gpu_trace(model, make_prompts(w), w.gen_len, tau, 1, w.block_size, tau_semi=tau_semi)
+    np.testing.assert_array_equal(tr.tokens, one.tokens)
+    np.testing.assert_array_equal(tr.commit_step, one.commit_step)
+    np.testing.assert_array_equal(tr.forwards, one.forwards)
+    assert tr.stats["rows"] == one.stats["rows"] and tr.stats["lm_rows"] == one.stats["lm_rows"]
+    assert tr.stats["active_forwards"] == int(one.forwards.sum())
+    assert tr.stats["static_saved"] == tr.stats["static_deferred"] == 0
+    assert tr.stats["skipped"] > 0
+
+
+def _sweep_steps(commit_step, B):
+    last = commit_step.reshape(-1, B).max(axis=1)
+    return np.maximum.accumulate(last)
+
+
+def _check_participation_identities(tr, nb, G, B):
+    """Counter identities on the GPU's own full-size trace (admission without
+    a threshold): active block-forwards = sum over steps of min(nb, blocks
+    not yet swept); cache writes = blocks swept before a sequence's last step."""
+    nblk = G // B
+    act = cw = 0
+    for i in range(tr.commit_step.shape[0]):
+        sw = _sweep_steps(tr.commit_step[i], B)
+        final = int(tr.forwards[i]) - 1
+        cw += int(np.count_nonzero(sw < final))
+        for t in range(int(tr.forwards[i])):
+            act += min(nb, nblk - int(np.count_nonzero(sw < t)))
+    assert tr.stats["active_forwards"] == act
+    assert tr.stats["cache_writes"] == cw
+    s = tr.stats
+    _say(f"  no-op share {s['zero_commit'] / s['active_forwards']:.3f}; static rule saves "
+         f"{s['static_saved'] / s['active_forwards']:.3f} of active block-forwards, defers "
+         f"{s['static_deferred'] / s['active_forwards']:.3f}")
+
+
 def test_config0_tiny_f32():
     w = workload(0)
     for tau in w.taus:
@@ -159,7 +211,9 @@ def test_config2_multiblock_full_size(tau):
     vocab 152064, batch 32, prompts 1024, 3 blocks in flight, 1024 generated
     tokens): the GPU decodes the whole batch; the oracle replays sequence 5
     for its first 16 steps (logits compared on the first 3)."""
-    run_parity(workload(2), tau, seq_ids=[5], max_steps=16, logit_steps=3)
+    w = workload(2)
+    tr, _ = run_parity(w, tau, seq_ids=[5], max_steps=16, logit_steps=3)
+    _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
 
 
 def test_config3_long_prefix_full_size():
@@ -174,7 +228,9 @@ def test_config4_moe_full_size(tau):
     """Full-size MoE model (20 layers, d 2048, 64 experts top-8 with FFN 512
     plus a shared expert, vocab 152064, batch 64, prompts 256, 128 generated
     tokens); the oracle replays sequence 17 for 12 steps."""
-    run_parity(workload(4), tau, seq_ids=[17], max_steps=12, logit_steps=2)
+    w = workload(4)
+    tr, _ = run_parity(w, tau, seq_ids=[17], max_steps=12, logit_steps=2)
+    _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
 
 
 def test_decode_entry_point_matches_stepwise_and_is_deterministic():
@@ -227,6 +283,11 @@ def test_error_paths():
     assert e.value.status == bd.BD_EINVAL
     with pytest.raises(bd.BDError) as e:
         bd.State(model, pr, 64, float("nan"), 2, 16)
+    assert e.value.status == bd.BD_EINVAL
+    cfg = bd.decode_cfg(0.9, 2, 16)
+    cfg.skip_masked = 2
+    with pytest.raises(bd.BDError) as e:
+        bd.bd_prefill(model.handle, 0, 3, 0, 64, cfg)
     assert e.value.status == bd.BD_EINVAL
     st = bd.State(model, pr, 64, 0.9, 2, 16)
     with pytest.raises(bd.BDError) as e:
