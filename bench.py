@@ -32,14 +32,17 @@ PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # fp32 vector
 
 
-def algorithmic_work(w, stats):
+def algorithmic_work(w, stats, wq="bf16"):
     """FLOPs and HBM bytes per kernel class for the work recorded in ``stats``
     (counters summed over one decode).  Bytes count each weight once per
     forward (for MoE layers, every expert: an upper bound, as nearly all of
     the 64 experts receive rows at these batch sizes), the K/V read once per
     (sequence, kv head, layer) and the window K/V written; FLOPs count only
-    visible query-key pairs and masked LM rows."""
-    esz = 2 if w.dtype == "bf16" else 4     # weights
+    visible query-key pairs and masked LM rows.  With fp8 layer weights the
+    layer projections read 1 byte per weight (the per-row scales are
+    negligible); the LM head stays bf16."""
+    esz = 2 if w.dtype == "bf16" else 4     # LM-head weights
+    lsz = 1 if wq == "fp8" else esz         # decoder-layer projection weights
     asz = 4                                  # activations / KV: fp32 or a bf16 hi/lo pair
     d, H, Hkv, hd, F, V, L = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.ffn_dim, w.vocab, w.n_layers
     qkv = (H + 2 * Hkv) * hd
@@ -50,15 +53,15 @@ def algorithmic_work(w, stats):
     out = {}
     for k, (N, K) in gemm.items():
         flops = 2.0 * rows * N * K * L
-        byts = (N * K * esz * fw + rows * K * asz + rows * N * 4) * L
+        byts = (N * K * lsz * fw + rows * K * asz + rows * N * 4) * L
         out[k] = (flops, byts)
     if w.n_experts:
         # routed experts: each row meets top_k experts; the shared experts see every row
         Fe, Fs, E, k = w.expert_ffn, w.n_shared * w.expert_ffn, w.n_experts, w.top_k
         out["gemm_gu"] = (2.0 * rows * (k * 2 * Fe + 2 * Fs) * d * L,
-                          ((E + w.n_shared) * 2 * Fe * d * esz * fw + rows * (k + 1) * d * asz) * L)
+                          ((E + w.n_shared) * 2 * Fe * d * lsz * fw + rows * (k + 1) * d * asz) * L)
         out["gemm_down"] = (2.0 * rows * (k * Fe + Fs) * d * L,
-                            ((E + w.n_shared) * Fe * d * esz * fw + rows * (k + 1) * (Fe * asz + d * 4)) * L)
+                            ((E + w.n_shared) * Fe * d * lsz * fw + rows * (k + 1) * (Fe * asz + d * 4)) * L)
     out["attn"] = (4.0 * hd * H * stats["pairs"] * L,
                    (stats["keys"] * Hkv * hd * 2 * asz + rows * H * hd * asz
                     + rows * H * hd * asz) * L)
@@ -138,6 +141,8 @@ def main():
                     help="semi-completion threshold (default: off)")
     ap.add_argument("--tau-add", type=float, default=0.0,
                     help="admission threshold (default 0: refill every free slot)")
+    ap.add_argument("--wq", choices=["bf16", "fp8"], default="bf16",
+                    help="weight precision of the decoder-layer projections")
     ap.add_argument("--skip-masked", action="store_true",
                     help="static skip rule: leave fully masked blocks behind an active one out of the forward")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -172,7 +177,7 @@ def main():
     print(f"[bench] workload {w.name}: building weights", file=sys.stderr, flush=True)
     weights = make_weights(w)
     prompts = make_prompts(w)
-    model = bd.Model(w, weights)
+    model = bd.Model(w, weights, wq=None if args.wq == "bf16" else args.wq)
     st = bd.State(model, prompts, w.gen_len, args.tau, w.n_inflight, w.block_size, args.tau_semi,
                   args.tau_add, args.skip_masked)
     if args.trace_steps:
@@ -226,7 +231,7 @@ def main():
         one_decode()
     prof = bd.bd_profile_read(model.handle)
     bd.bd_profile(model.handle, False)
-    work = algorithmic_work(w, stats)
+    work = algorithmic_work(w, stats, args.wq)
     kernels = {}
     for k, (tms, n) in prof.items():
         if n == 0:
@@ -260,7 +265,11 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, weights, prompts, args.tau, args.cpu_seconds, args.tau_semi, args.tau_add,
+        ow = weights
+        if args.wq == "fp8":
+            from oracle.quant import fp8_weights
+            ow = fp8_weights(w, weights)
+        cpu = cpu_baseline(w, ow, prompts, args.tau, args.cpu_seconds, args.tau_semi, args.tau_add,
                            args.skip_masked)
 
     line = {
@@ -272,7 +281,8 @@ def main():
                    "block_size": w.block_size, "n_inflight": w.n_inflight, "tau": args.tau,
                    **({"tau_semi": args.tau_semi, "tau_add": args.tau_add}
                       if args.tau_semi is not None or args.tau_add else {}),
-                   **({"skip_masked": True} if args.skip_masked else {})},
+                   **({"skip_masked": True} if args.skip_masked else {}),
+                   **({"weights": args.wq} if args.wq != "bf16" else {})},
         "tpf": tpf, "denoise_steps_per_decode": S, "step_latency_us": 1e3 * ms / S,
         "wall_s": wall, "roofline": roof, "kernels": kernels, "cpu_baseline": cpu,
         "participation": {k: stats[k] for k in ("active_forwards", "zero_commit", "static_saved",

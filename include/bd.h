@@ -54,7 +54,22 @@ typedef struct {
     float logit_scale;     /* LM-head logits are multiplied by this */
     int32_t mask_id;       /* placeholder token id, in [0, vocab) */
     int32_t dtype;         /* bd_dtype of matrices, activations and KV cache */
+    int32_t wq;            /* weight precision of the decoder-layer projections
+                              (the precision axis of a serving configuration,
+                              §4.3 and the quantization grid of App. E):
+                              BD_WQ_NONE keeps the model dtype; BD_WQ_FP8 (bf16
+                              models only) has bd_init_model quantize every
+                              decoder-layer projection (QKV, O, gate, up, down,
+                              expert and shared-expert matrices) to fp8 E4M3
+                              with one power-of-two scale per output row (see
+                              bd_quantize_fp8); embeddings, norms, router and
+                              LM head stay as given.  The GEMMs read the fp8
+                              codes and compute exactly as bf16 GEMMs on the
+                              dequantized weights (code value x scale, which
+                              bf16 holds exactly). */
 } bd_model_cfg;
+
+enum { BD_WQ_NONE = 0, BD_WQ_FP8 = 1 };
 
 /* One serving configuration: the paper's operating point lambda (§2.1, the
  * notation table and App. G): accept threshold, in-flight block count, block
@@ -120,14 +135,28 @@ typedef struct bd_state bd_state;
  *  With n_shared == 0 the three shared-expert pointers may be NULL.
  *  Errors: BD_EINVAL for inconsistent dimensions (head_dim not 64 or 128,
  *  n_heads not a multiple of n_kv_heads, mask_id out of range, wrong
- *  n_weights, top_k outside [1, n_experts], n_experts > 64),
- *  BD_EUNSUPPORTED (MoE with the f32 dtype; shapes off the GEMM tiles: with
+ *  n_weights, top_k outside [1, n_experts], n_experts > 64, wq not a
+ *  BD_WQ_* value),
+ *  BD_EUNSUPPORTED (MoE or BD_WQ_FP8 with the f32 dtype; shapes off the GEMM tiles: with
  *  bf16 every projection's output and input widths -- (H + 2 Hkv) hd, d,
  *  H hd, vocab, 2 ffn or 2 Fe, ffn or Fe -- must be multiples of 128),
  *  BD_ENOMEM, BD_EHIP.
  */
 bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev, int32_t n_weights,
                         void* stream, bd_model** out);
+
+/*
+ * bd_quantize_fp8 -- fp8 weight quantization of one bf16 matrix (the format
+ *  bd_init_model uses for BD_WQ_FP8).
+ *  w_dev: bf16 [rows][cols] device.  For each row, E is the smallest integer
+ *  with max|w| / 2^E <= 448 (E = 0 for an all-zero row); scale_dev[row]
+ *  (float32, device) receives 2^E and codes_dev[row][cols] (uint8, device)
+ *  the OCP fp8 E4M3 code nearest to w / 2^E (ties to even mantissa; sign
+ *  bit set for negative values).  Asynchronous on stream (NULL = default).
+ *  Errors: BD_EINVAL for NULL pointers or rows, cols < 1; BD_EHIP.
+ */
+bd_status bd_quantize_fp8(const void* w_dev, int32_t rows, int32_t cols, uint8_t* codes_dev,
+                          float* scale_dev, void* stream);
 
 /*
  * bd_prefill -- encode b prompts and create a decode state.

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libbd.so")
 BD_OK, BD_EINVAL, BD_ENOMEM, BD_EHIP, BD_ESTATE, BD_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 BD_F32, BD_BF16 = 0, 1
 
-EXPORTED = ["bd_init_model", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
+EXPORTED = ["bd_init_model", "bd_quantize_fp8", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
             "bd_decode", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
             "bd_profile_read", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select",
             "rl_select", "rl_alpha_sweep", "rl_split_exceedance", "rl_monte_carlo"]
@@ -32,7 +32,11 @@ class bd_model_cfg(ctypes.Structure):
                                               "ffn_dim", "vocab", "n_experts", "top_k", "expert_ffn",
                                               "n_shared")] + \
                [("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("logit_scale", ctypes.c_float),
-                ("mask_id", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("mask_id", ctypes.c_int32), ("dtype", ctypes.c_int32), ("wq", ctypes.c_int32)]
+
+
+BD_WQ_NONE, BD_WQ_FP8 = 0, 1
+WQ = {None: BD_WQ_NONE, "bf16": BD_WQ_NONE, "fp8": BD_WQ_FP8}
 
 
 class bd_decode_cfg(ctypes.Structure):
@@ -68,6 +72,7 @@ def _load():
     P, I32, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_void_p
     sig = {
         "bd_init_model": [P(bd_model_cfg), P(VP), I32, VP, P(VP)],
+        "bd_quantize_fp8": [VP, I32, I32, VP, VP, VP],
         "bd_prefill": [VP, VP, I32, I32, I32, P(bd_decode_cfg), P(VP)],
         "bd_denoise_step": [VP, VP, VP, VP, VP],
         "bd_commit": [VP, VP, P(I32)],
@@ -121,6 +126,26 @@ def bd_init_model(cfg: bd_model_cfg, weight_ptrs: Sequence[int], stream: int = 0
     _check(lib.bd_init_model(ctypes.byref(cfg), arr, len(weight_ptrs), ctypes.c_void_p(stream),
                              ctypes.byref(out)))
     return out.value
+
+
+def bd_quantize_fp8(w_ptr: int, rows: int, cols: int, codes_ptr: int, scale_ptr: int, stream: int = 0):
+    _check(lib.bd_quantize_fp8(w_ptr, rows, cols, codes_ptr, scale_ptr, ctypes.c_void_p(stream)))
+
+
+def quantize_fp8(w_bf16_bits, device: str = "cuda:0"):
+    """fp8 E4M3 codes and row scales of a bf16 matrix given as uint16 bit
+    patterns [rows][cols] (numpy); returns numpy (codes uint8, scale float32)."""
+    import numpy as np
+    import torch
+    a = np.ascontiguousarray(w_bf16_bits)
+    rows, cols = a.shape
+    w = torch.from_numpy(a.view(np.int16)).to(device)
+    codes = torch.empty((rows, cols), dtype=torch.uint8, device=device)
+    scale = torch.empty((rows,), dtype=torch.float32, device=device)
+    bd_quantize_fp8(w.data_ptr(), rows, cols, codes.data_ptr(), scale.data_ptr(),
+                    torch.cuda.current_stream(device).cuda_stream)
+    torch.cuda.synchronize(device)
+    return codes.cpu().numpy(), scale.cpu().numpy()
 
 
 def bd_prefill(model: int, prompt_ptr: int, b: int, P: int, G: int, cfg: bd_decode_cfg) -> int:
@@ -307,7 +332,9 @@ def model_cfg_from(w) -> bd_model_cfg:
 class Model:
     """Device copy of the weights plus the library handle."""
 
-    def __init__(self, workload, weights, device: str = "cuda:0"):
+    def __init__(self, workload, weights, device: str = "cuda:0", wq=None):
+        """``wq``: None (weights in the model dtype) or "fp8" (decoder-layer
+        projections quantized by the library, see bd_quantize_fp8)."""
         import numpy as np
         import torch
         self.torch = torch
@@ -324,6 +351,8 @@ class Model:
         self.stream = torch.cuda.current_stream(self.device)
         torch.cuda.synchronize(self.device)
         self.cfg = model_cfg_from(workload)
+        self.cfg.wq = WQ[wq]
+        self.wq = wq
         self.handle = bd_init_model(self.cfg, [t.data_ptr() for t in self.tensors], self.stream.cuda_stream)
 
     def close(self):

@@ -9,6 +9,11 @@
 // global-to-LDS loads into a four-stage ring (K-stages of 32, swizzled rows);
 // one barrier per stage; the residual projections may split K (the partial
 // sums are folded in by the next RMSNorm).
+// fp8 weights (W8): W holds OCP fp8 E4M3 codes, one byte per element, with
+// a power-of-two scale per output row; the W stage holds 32-byte rows, each
+// lane converts its 8 codes of a fragment to bf16 (exact) before the MFMA,
+// and the epilogue multiplies each output column by its row scale (exact, so
+// the result equals the bf16 product with the dequantized weights).
 // f32 path (small fp32 models): 64x64x16 SIMT tiles.
 //
 // The row count M is read from device memory so that a launch sized for the
@@ -58,12 +63,34 @@ __device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int BM, int BN>
+template <int BM, int BN, bool W8 = false>
 struct GemmStage {
   bf16_t ah[BM * SK];
   bf16_t al[BM * SK];
-  bf16_t b[BN * SK];
+  bf16_t b[W8 ? BN * SK / 2 : BN * SK];   // bf16 rows of 64 B, or fp8 rows of 32 B
 };
+
+// fp8 W loads per wave and stage: BN = 128 -> one 16-byte load per lane
+// (32 rows of 32 B per wave); BN = 64 -> two 4-byte loads (8 rows each).
+template <int BN>
+struct W8Load {
+  static constexpr int bytes = BN == 128 ? 16 : 4;
+  static constexpr int loads = BN * SK / (4 * 64 * bytes);
+  static constexpr int rows = 64 * bytes / SK;      // rows per load instruction
+};
+
+// Eight E4M3 codes (bytes 0..7 of v, k order) -> eight bf16 (exact).
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint2 v) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, false);
+  const bf16x2_t b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.x, 1.0f, true);
+  const bf16x2_t c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, false);
+  const bf16x2_t d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(v.y, 1.0f, true);
+  bf16x8 o;
+  o[0] = a[0]; o[1] = a[1]; o[2] = b[0]; o[3] = b[1];
+  o[4] = c[0]; o[5] = c[1]; o[6] = d[0]; o[7] = d[1];
+  return o;
+}
 
 template <int BM, int BN>
 struct MfmaTile {
@@ -79,40 +106,61 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Per-thread source pointers of one tile's loads: A rows (hi plane; lo at
 // + a_plane) and W rows, each already offset to this lane's 16-byte chunk.
-template <int BM, int BN>
+template <int BM, int BN, bool W8 = false>
 struct TileSrc {
   const bf16_t* a[BM / 64];
-  const bf16_t* w[BN / 64];
+  const bf16_t* w[W8 ? 1 : BN / 64];
+  const uint8_t* w8[W8 ? W8Load<BN>::loads : 1];
 };
 
-template <int BM, int BN>
-__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN>& src, size_t a_plane, int k,
-                                            GemmStage<BM, BN>& s, int wave) {
+template <int BM, int BN, bool W8>
+__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8>& src, size_t a_plane, int k,
+                                            GemmStage<BM, BN, W8>& s, int wave) {
 #pragma unroll
   for (int i = 0; i < BM / 64; ++i) {
     const int r = (i * 4 + wave) * 16;
     __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k), (lds_void_t*)(s.ah + r * SK), 16, 0, 0);
     __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k + a_plane), (lds_void_t*)(s.al + r * SK), 16, 0, 0);
   }
+  if constexpr (W8) {
+    typedef W8Load<BN> L;
+    uint8_t* b8 = (uint8_t*)s.b;
 #pragma unroll
-  for (int i = 0; i < BN / 64; ++i) {
-    const int r = (i * 4 + wave) * 16;
-    __builtin_amdgcn_global_load_lds((const void*)(src.w[i] + k), (lds_void_t*)(s.b + r * SK), 16, 0, 0);
+    for (int i = 0; i < L::loads; ++i) {
+      const int r = (wave * L::loads + i) * L::rows;
+      __builtin_amdgcn_global_load_lds((const void*)(src.w8[i] + k), (lds_void_t*)(b8 + r * SK), L::bytes, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < BN / 64; ++i) {
+      const int r = (i * 4 + wave) * 16;
+      __builtin_amdgcn_global_load_lds((const void*)(src.w[i] + k), (lds_void_t*)(s.b + r * SK), 16, 0, 0);
+    }
   }
 }
 
 // One stage of MFMAs: 4 waves in a 2x2 arrangement, each accumulating a
 // (BM/2)x(BN/2) sub-tile of (BM/32)x(BN/32) MFMA 16x16x32 tiles.
-template <int BM, int BN>
-__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN>& s, MfmaTile<BM, BN>& t, int wave) {
+template <int BM, int BN, bool W8>
+__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaTile<BM, BN>& t, int wave) {
   constexpr int FM = BM / 32, FN = BN / 32;
   const int lane = threadIdx.x & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int r16 = lane & 15;
   const int pos = ((lane >> 4) ^ swz(r16)) * 8;   // fragment rows are r16 + 16 j
   u32x4 bfr[FN];
+  if constexpr (W8) {
+    // fp8 rows of 32 B, unswizzled: a fragment's 16 rows are 512 contiguous bytes
+    const uint8_t* b8 = (const uint8_t*)s.b;
 #pragma unroll
-  for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&s.b[(wn * (BN / 2) + j * 16 + r16) * SK + pos]);
+    for (int j = 0; j < FN; ++j) {
+      const uint2 raw = *(const uint2*)(b8 + (wn * (BN / 2) + j * 16 + r16) * SK + (lane >> 4) * 8);
+      bfr[j] = __builtin_bit_cast(u32x4, fp8x8_to_bf16(raw));
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&s.b[(wn * (BN / 2) + j * 16 + r16) * SK + pos]);
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int row = wm * (BM / 2) + i * 16 + r16;
@@ -134,36 +182,49 @@ __device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN>& s, MfmaTile<
 // are separate LDS objects so the compiler can tell the loads into one stage
 // from the reads of another.  All waves of the workgroup must run the same
 // number of stages (the barriers are workgroup-wide).
-template <int BM, int BN>
+template <int BM, int BN, bool W8 = false>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int lda, size_t a_plane,
-                                              const bf16_t* __restrict__ W, int ldw, int k0,
+                                              const void* __restrict__ Wv, int ldw, int k0,
                                               int klen, int m0, int n0, MfmaTile<BM, BN>& t,
-                                              GemmStage<BM, BN>& s0, GemmStage<BM, BN>& s1,
-                                              GemmStage<BM, BN>& s2, GemmStage<BM, BN>& s3,
+                                              GemmStage<BM, BN, W8>& s0, GemmStage<BM, BN, W8>& s1,
+                                              GemmStage<BM, BN, W8>& s2, GemmStage<BM, BN, W8>& s3,
                                               int wave, const int32_t* __restrict__ arows = nullptr,
                                               int nvalid = 0) {
-  constexpr int LPS = 2 * (BM / 64) + BN / 64;   // load instructions per thread per stage
+  // load instructions per thread per stage
+  constexpr int LPS = 2 * (BM / 64) + (W8 ? W8Load<BN>::loads : BN / 64);
   const int lane = threadIdx.x & 63;
   const int rsub = lane >> 2, chunk = (lane & 3) ^ swz(rsub);
-  TileSrc<BM, BN> src;
+  TileSrc<BM, BN, W8> src;
 #pragma unroll
   for (int i = 0; i < BM / 64; ++i) {
     const int r = (i * 4 + wave) * 16 + rsub;
     const int grow = arows ? arows[r < nvalid ? r : 0] : m0 + r;
     src.a[i] = A + (size_t)grow * lda + k0 + chunk * 8;
   }
+  if constexpr (W8) {
+    typedef W8Load<BN> L;
+    const uint8_t* W = (const uint8_t*)Wv;
+    const int per_row = SK / L::bytes;       // lanes per 32-byte row
 #pragma unroll
-  for (int i = 0; i < BN / 64; ++i)
-    src.w[i] = W + (size_t)(n0 + (i * 4 + wave) * 16 + rsub) * ldw + k0 + chunk * 8;
+    for (int i = 0; i < L::loads; ++i) {
+      const int r = (wave * L::loads + i) * L::rows + lane / per_row;
+      src.w8[i] = W + (size_t)(n0 + r) * ldw + k0 + (lane % per_row) * L::bytes;
+    }
+  } else {
+    const bf16_t* W = (const bf16_t*)Wv;
+#pragma unroll
+    for (int i = 0; i < BN / 64; ++i)
+      src.w[i] = W + (size_t)(n0 + (i * 4 + wave) * 16 + rsub) * ldw + k0 + chunk * 8;
+  }
 #pragma unroll
   for (int i = 0; i < BM / 32; ++i)
 #pragma unroll
     for (int j = 0; j < BN / 32; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = klen / SK;     // multiple of 4, >= 4
-  stage_issue<BM, BN>(src, a_plane, 0, s0, wave);
-  stage_issue<BM, BN>(src, a_plane, SK, s1, wave);
-  stage_issue<BM, BN>(src, a_plane, 2 * SK, s2, wave);
+  stage_issue<BM, BN, W8>(src, a_plane, 0, s0, wave);
+  stage_issue<BM, BN, W8>(src, a_plane, SK, s1, wave);
+  stage_issue<BM, BN, W8>(src, a_plane, 2 * SK, s2, wave);
   int kt = 0;
   // each step: own loads of stage kt done (the two younger stages may still
   // be in flight), barrier (everyone's loads done, everyone past stage kt-1),
@@ -171,8 +232,8 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
 #define BD_GEMM_STEP(CUR, NXT, KNEXT)                            \
   wait_vmcnt<2 * LPS>();                                         \
   __builtin_amdgcn_s_barrier();                                  \
-  stage_issue<BM, BN>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
-  stage_mfma<BM, BN>(CUR, t, wave);
+  stage_issue<BM, BN, W8>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
+  stage_mfma<BM, BN, W8>(CUR, t, wave);
   for (; kt + 4 < nk; kt += 4) {
     BD_GEMM_STEP(s0, s3, kt + 3)
     BD_GEMM_STEP(s1, s0, kt + 4)
@@ -183,21 +244,37 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
   // the last four stages (kt + 3 == nk - 1)
   wait_vmcnt<2 * LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_issue<BM, BN>(src, a_plane, (kt + 3) * SK, s3, wave);
-  stage_mfma<BM, BN>(s0, t, wave);
+  stage_issue<BM, BN, W8>(src, a_plane, (kt + 3) * SK, s3, wave);
+  stage_mfma<BM, BN, W8>(s0, t, wave);
   wait_vmcnt<2 * LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN>(s1, t, wave);
+  stage_mfma<BM, BN, W8>(s1, t, wave);
   wait_vmcnt<LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN>(s2, t, wave);
+  stage_mfma<BM, BN, W8>(s2, t, wave);
   wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN>(s3, t, wave);
+  stage_mfma<BM, BN, W8>(s3, t, wave);
 }
 
-#define BD_GEMM_SMEM(BM, BN)                                                     \
-  __shared__ __attribute__((aligned(1024))) GemmStage<BM, BN> gs0, gs1, gs2, gs3
+#define BD_GEMM_SMEM(BM, BN, W8)                                                 \
+  __shared__ __attribute__((aligned(1024))) GemmStage<BM, BN, W8> gs0, gs1, gs2, gs3
+
+// fp8 weights: multiply accumulator column n (of this wave's fragments) by
+// the row scale sc[n] of the weight, a power of two.
+template <int BM, int BN>
+__device__ __forceinline__ void scale_columns(MfmaTile<BM, BN>& t, const float* __restrict__ sc, int n0,
+                                              int wave) {
+  const int lane = threadIdx.x & 63, wn = wave & 1;
+#pragma unroll
+  for (int j = 0; j < BN / 32; ++j) {
+    const float f = sc[n0 + wn * (BN / 2) + j * 16 + (lane & 15)];
+#pragma unroll
+    for (int i = 0; i < BM / 32; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) t.acc[i][j][r] *= f;
+  }
+}
 
 // GEMM, epilogue applied in registers.  Items (split z, column tile x, row
 // tile y) are numbered z-major, then x, then y: an XCD's range shares the A
@@ -207,13 +284,14 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
 // split stores its raw partial tile to ws[split][row][col] (rows padded to
 // whole tiles) and the next RMSNorm of the residual stream adds the partials
 // in split order.
-template <int BM, int BN, int EPI>
+template <int BM, int BN, int EPI, bool W8>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
-                                                   size_t a_plane, const bf16_t* __restrict__ W,
+                                                   size_t a_plane, const void* __restrict__ W,
                                                    int ldw, int N, int K,
                                                    const int32_t* __restrict__ Mp,
                                                    void* __restrict__ out, int ldo, size_t out_plane,
-                                                   float* __restrict__ ws, int zmax) {
+                                                   float* __restrict__ ws, int zmax,
+                                                   const float* __restrict__ wscale) {
   constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
   const int X = N / BN, Y = (M + BM - 1) / BM;
@@ -230,10 +308,11 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
   const int m0 = (xy % Y) * BM, n0 = (xy / Y) * BN;
   const int klen = K / S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  BD_GEMM_SMEM(BM, BN);
+  BD_GEMM_SMEM(BM, BN, W8);
   MfmaTile<BM, BN> t;
-  mfma_mainloop<BM, BN>(A, lda, a_plane, W, ldw, z * klen, klen, m0, n0, t, gs0, gs1, gs2,
-                        gs3, wave);
+  mfma_mainloop<BM, BN, W8>(A, lda, a_plane, W, ldw, z * klen, klen, m0, n0, t, gs0, gs1, gs2,
+                            gs3, wave);
+  if constexpr (W8) scale_columns<BM, BN>(t, wscale, n0, wave);
   const int wm = wave >> 1, wn = wave & 1;
   float* wz = (EPI == EPI_ADD_F32 && S > 1) ? ws + (size_t)z * ((M + BM - 1) / BM) * BM * N
                                             : nullptr;
@@ -285,10 +364,11 @@ __device__ __forceinline__ void store_pair4(bf16_t* p, size_t plane, const float
       make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
 }
 
-template <int BM, int BN>
+template <int BM, int BN, bool W8>
 __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, int lda,
-                                                  size_t a_plane, const bf16_t* __restrict__ W,
-                                                  int K, const int32_t* __restrict__ Mp, QkvEpi e) {
+                                                  size_t a_plane, const void* __restrict__ W,
+                                                  int K, const int32_t* __restrict__ Mp, QkvEpi e,
+                                                  const float* __restrict__ wscale) {
   constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
   const int X = (e.H + 2 * e.Hkv) * e.hd / BN, Y = (M + BM - 1) / BM;
@@ -296,9 +376,10 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, 
   if (u >= X * Y) return;
   const int m0 = (u % Y) * BM, n0 = (u / Y) * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  BD_GEMM_SMEM(BM, BN);
+  BD_GEMM_SMEM(BM, BN, W8);
   MfmaTile<BM, BN> t;
-  mfma_mainloop<BM, BN>(A, lda, a_plane, W, K, 0, K, m0, n0, t, gs0, gs1, gs2, gs3, wave);
+  mfma_mainloop<BM, BN, W8>(A, lda, a_plane, W, K, 0, K, m0, n0, t, gs0, gs1, gs2, gs3, wave);
+  if constexpr (W8) scale_columns<BM, BN>(t, wscale, n0, wave);
   const int wm = wave >> 1, wn = wave & 1;
   const int hd = e.hd, half = hd >> 1;
   const int qcols = e.H * hd, qkcols = (e.H + e.Hkv) * hd;
@@ -366,27 +447,30 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, 
 // expert-sorted outputs.  The A rows are gathered through a_rows (token rows
 // of the expert-sorted assignments) or, with a_rows == NULL, read from the
 // expert-sorted layout itself.  W of expert e starts at W + e * w_stride.
-template <int EPI>
+template <int EPI, bool W8>
 __global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__ A, int lda,
-                                                      size_t a_plane, const bf16_t* __restrict__ W,
+                                                      size_t a_plane, const void* __restrict__ W,
                                                       int ldw, int K, GroupTiles g,
                                                       void* __restrict__ out, int ldo,
-                                                      size_t out_plane) {
+                                                      size_t out_plane,
+                                                      const float* __restrict__ wscale,
+                                                      int scale_stride) {
   constexpr int BM = 128, BN = 128, FM = BM / 32, FN = BN / 32;
   const int ti = blockIdx.y;
   if (ti >= *g.ntiles) return;
   const int e = g.tile_e[ti], m0 = g.tile_m0[ti];
   const int cnt = g.e_cnt[e], base = g.e_off[e];
   const int n0 = blockIdx.x * BN;
-  BD_GEMM_SMEM(BM, BN);
+  BD_GEMM_SMEM(BM, BN, W8);
   MfmaTile<BM, BN> t;
-  const bf16_t* We = W + (size_t)e * g.w_stride;
+  const void* We = (const uint8_t*)W + (size_t)e * g.w_stride * (W8 ? 1 : 2);
   if (g.a_rows)
-    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, 0, n0, t, gs0, gs1, gs2, gs3,
-                          threadIdx.x >> 6, g.a_rows + base + m0, cnt - m0);
+    mfma_mainloop<BM, BN, W8>(A, lda, a_plane, We, ldw, 0, K, 0, n0, t, gs0, gs1, gs2, gs3,
+                              threadIdx.x >> 6, g.a_rows + base + m0, cnt - m0);
   else
-    mfma_mainloop<BM, BN>(A, lda, a_plane, We, ldw, 0, K, base + m0, n0, t, gs0, gs1, gs2, gs3,
-                          threadIdx.x >> 6);
+    mfma_mainloop<BM, BN, W8>(A, lda, a_plane, We, ldw, 0, K, base + m0, n0, t, gs0, gs1, gs2, gs3,
+                              threadIdx.x >> 6);
+  if constexpr (W8) scale_columns<BM, BN>(t, wscale + (size_t)e * scale_stride, n0, threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -414,15 +498,18 @@ __global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__
 
 hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
                                int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
-                               int ldo, size_t out_plane, hipStream_t st) {
+                               int ldo, size_t out_plane, const float* wscale, hipStream_t st) {
   if (N % 128 || K % KALIGN) return hipErrorInvalidValue;
   dim3 grid(N / 128, max_tiles);
-  if (epi == EPI_SWIGLU)
-    k_gemm_grouped<EPI_SWIGLU><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W,
-                                                     ldw, K, g, out, ldo, out_plane);
-  else
-    k_gemm_grouped<EPI_STORE_F32><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane,
-                                                        (const bf16_t*)W, ldw, K, g, out, ldo, 0);
+  const bf16_t* a = (const bf16_t*)A;
+#define BD_GROUPED(EPI_, W8_, OP_) \
+  k_gemm_grouped<EPI_, W8_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, ldw, K, g, out, ldo, OP_, wscale, N)
+  if (epi == EPI_SWIGLU) {
+    if (wscale) BD_GROUPED(EPI_SWIGLU, true, out_plane); else BD_GROUPED(EPI_SWIGLU, false, out_plane);
+  } else {
+    if (wscale) BD_GROUPED(EPI_STORE_F32, true, 0); else BD_GROUPED(EPI_STORE_F32, false, 0);
+  }
+#undef BD_GROUPED
   return hipGetLastError();
 }
 
@@ -445,11 +532,12 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
   if (u >= X * Y) return;
   const int m0 = (u % Y) * TBM, n0 = (u / Y) * TBN;
   const int vt = u / Y;
-  BD_GEMM_SMEM(TBM, TBN);
+  BD_GEMM_SMEM(TBM, TBN, false);
   __shared__ float red_m[2][TBM], red_s[2][TBM];
   __shared__ int32_t red_a[2][TBM];
   MfmaTile<TBM, TBN> t;
-  mfma_mainloop<TBM, TBN>(A, d, a_plane, W, d, 0, d, m0, n0, t, gs0, gs1, gs2, gs3, threadIdx.x >> 6);
+  mfma_mainloop<TBM, TBN, false>(A, d, a_plane, W, d, 0, d, m0, n0, t, gs0, gs1, gs2, gs3,
+                                 threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -656,19 +744,22 @@ __global__ __launch_bounds__(256) void k_lm_merge(const float* __restrict__ pmax
 
 // ------------------------------------------------------------------ launchers
 
-template <int BM, int BN>
-static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const bf16_t* w,
+template <int BM, int BN, bool W8>
+static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const void* w,
                             int ldw, int N, int K, const int32_t* M_dev, void* o, int ldo, size_t op,
-                            float* ws, int zmax, hipStream_t st) {
+                            float* ws, int zmax, const float* wscale, hipStream_t st) {
   switch (epi) {
     case EPI_ADD_F32:
-      k_gemm_bf16<BM, BN, EPI_ADD_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws, zmax);
+      k_gemm_bf16<BM, BN, EPI_ADD_F32, W8><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws,
+                                                                 zmax, wscale);
       break;
     case EPI_SWIGLU:
-      k_gemm_bf16<BM, BN, EPI_SWIGLU><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr, 1);
+      k_gemm_bf16<BM, BN, EPI_SWIGLU, W8><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
+                                                                nullptr, 1, wscale);
       break;
     default:
-      k_gemm_bf16<BM, BN, EPI_STORE_F32><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, nullptr, 1);
+      k_gemm_bf16<BM, BN, EPI_STORE_F32, W8><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
+                                                                   nullptr, 1, wscale);
       break;
   }
 }
@@ -686,7 +777,7 @@ GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap) {
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
                                int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
-                               hipStream_t st) {
+                               hipStream_t st, const float* wscale) {
   const bool big = p.bm == 128 && p.bn == 128, small = p.bm == 64 && p.bn == 64;
   if ((!big && !small) || p.zmax < 1 || p.zmax > 8) return hipErrorInvalidValue;
   if (N % p.bn || K % KALIGN) return hipErrorInvalidValue;
@@ -695,25 +786,32 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
   // (see xcd_item)
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) * p.zmax + 7);
   const bf16_t* a = (const bf16_t*)A;
-  const bf16_t* w = (const bf16_t*)W;
-  if (big) launch_bf16_cfg<128, 128>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, st);
-  else launch_bf16_cfg<64, 64>(epi, grid, a, lda, a_plane, w, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, st);
+#define BD_CFG(BM_, BN_, W8_) \
+  launch_bf16_cfg<BM_, BN_, W8_>(epi, grid, a, lda, a_plane, W, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, \
+                                 wscale, st)
+  if (wscale) {
+    if (big) BD_CFG(128, 128, true); else BD_CFG(64, 64, true);
+  } else {
+    if (big) BD_CFG(128, 128, false); else BD_CFG(64, 64, false);
+  }
+#undef BD_CFG
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                              int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
-                             int ldx, float* ws, ResidSplit* fold, hipStream_t st) {
+                             int ldx, float* ws, ResidSplit* fold, hipStream_t st, const float* wscale) {
   fold->ws = nullptr;
   if (!is_bf16 || !ws)
-    return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st);
+    return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st,
+                       wscale);
   // deep products (K >= 4096) take 128x128 tiles: with K split, their A and
   // W re-reads halve against 64x64 at the same parallelism
   GemmPlan p = plan_gemm(true, N, K, rows_cap);
   if (K >= 4096 && N % 128 == 0) p = GemmPlan{128, 128, 1};
   p.zmax = 8;
   hipError_t e = launch_gemm_planned(p, EPI_ADD_F32, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap,
-                                     X, ldx, 0, ws, st);
+                                     X, ldx, 0, ws, st, wscale);
   if (e != hipSuccess) return e;
   fold->ws = ws;
   fold->Mp = M_dev;
@@ -725,27 +823,31 @@ hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plan
 }
 
 hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W, int K,
-                           const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st) {
+                           const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st,
+                           const float* wscale) {
   const int N = (e.H + 2 * e.Hkv) * e.hd;
   if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
   const GemmPlan p = plan_gemm(true, N, K, rows_cap);
   if (N % p.bn) return hipErrorInvalidValue;
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) + 7);
-  if (p.bm == 128)
-    k_gemm_qkv<128, 128><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W, K,
-                                                M_dev, e);
-  else
-    k_gemm_qkv<64, 64><<<grid, 256, 0, st>>>((const bf16_t*)A, lda, a_plane, (const bf16_t*)W, K, M_dev,
-                                              e);
+  const bf16_t* a = (const bf16_t*)A;
+#define BD_QKV(BM_, W8_) k_gemm_qkv<BM_, BM_, W8_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, wscale)
+  if (wscale) {
+    if (p.bm == 128) BD_QKV(128, true); else BD_QKV(64, true);
+  } else {
+    if (p.bm == 128) BD_QKV(128, false); else BD_QKV(64, false);
+  }
+#undef BD_QKV
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       size_t out_plane, hipStream_t st) {
+                       size_t out_plane, hipStream_t st, const float* wscale) {
   if (is_bf16)
     return launch_gemm_planned(plan_gemm(true, N, K, rows_cap), epi, A, lda, a_plane, W, ldw, N, K,
-                               M_dev, rows_cap, out, ldo, out_plane, nullptr, st);
+                               M_dev, rows_cap, out, ldo, out_plane, nullptr, st, wscale);
+  if (wscale) return hipErrorInvalidValue;
   if (N % SBN || K % SBK) return hipErrorInvalidValue;
   dim3 grid(N / SBN, cdiv(rows_cap, SBM));
   const float* a = (const float*)A;

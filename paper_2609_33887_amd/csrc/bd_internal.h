@@ -99,9 +99,11 @@ __device__ __forceinline__ int resid_splits(int M, const ResidSplit& r) {
 //   EPI_STORE_F32 / EPI_ADD_F32: out fp32 [M][ldo]
 //   EPI_SWIGLU: silu(gate) * up [M][ldo] (W packed gate/up in 16-row groups),
 //   as a bf16 plane pair (out_plane) for bf16 models, fp32 otherwise
+// wscale (bf16 models only): NULL for bf16 weights; otherwise W holds fp8
+// E4M3 codes [N][K] and wscale[N] the power-of-two scale of each row.
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       size_t out_plane, hipStream_t st);
+                       size_t out_plane, hipStream_t st, const float* wscale = nullptr);
 // Expert tiles of a grouped GEMM (all device pointers).
 struct GroupTiles {
   const int32_t* tile_e;    // [max_tiles] expert of each tile
@@ -114,9 +116,10 @@ struct GroupTiles {
 };
 constexpr int GROUP_BM = 128;
 // out rows are expert-sorted rows; EPI_SWIGLU writes bf16 planes, EPI_STORE_F32 fp32.
+// wscale: as launch_gemm, [E][N] (expert e's scales at wscale + e N).
 hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
                                int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
-                               int ldo, size_t out_plane, hipStream_t st);
+                               int ldo, size_t out_plane, const float* wscale, hipStream_t st);
 
 // MoE routing: softmax over E router logits (fp32 weights, transposed
 // [d][E]), top_k experts (lowest id among equals), weights renormalised.
@@ -150,14 +153,15 @@ GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap);
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
                                int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
-                               hipStream_t st);
+                               hipStream_t st, const float* wscale = nullptr);
 // X[M][N] += A . W^T for the residual stream.  bf16 with ws (RESID_WS_FLOATS
 // floats): the kernel may split K (see ResidSplit) and *fold describes the
 // pending partials, which the next launch_rmsnorm of X must be given; else
 // the add is done in place and fold->ws is NULL.
 hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                              int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
-                             int ldx, float* ws, ResidSplit* fold, hipStream_t st);
+                             int ldx, float* ws, ResidSplit* fold, hipStream_t st,
+                             const float* wscale = nullptr);
 
 // LM head: per-row softmax statistics over the vocabulary of
 // z = scale * (A . W^T), mask column suppressed.  Writes per-(tile,row)
@@ -249,6 +253,9 @@ struct CommitArgs {
   int skip;                 // static skip rule: leave fully masked blocks behind an active one out
 };
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
+// fp8 E4M3 codes of a bf16 matrix [rows][cols], one power-of-two scale per
+// row (scale[row] = 2^E, the smallest with max |w| / 2^E <= 448).
+hipError_t launch_quant_fp8_rows(const void* W, int rows, int cols, uint8_t* Q, float* scale, hipStream_t st);
 
 struct InitArgs {
   PlanView plan;            // step plan to build
@@ -286,7 +293,8 @@ struct QkvEpi {
                             // positions of one sequence (block size % 4 == 0)
 };
 hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W, int K,
-                           const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st);
+                           const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st,
+                           const float* wscale = nullptr);
 // Copy of a [(H + 2 Hkv) hd][d] QKV weight with the q and k head rows
 // pair-interleaved (see QkvEpi); v rows unchanged.
 hipError_t launch_permute_qk_rows(const void* W, void* out, int H, int Hkv, int hd, size_t row_bytes,

@@ -604,6 +604,63 @@ hipError_t launch_init_decode(const InitArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ fp8 weights
+// Nearest E4M3 code (ties to even) of |v| <= 448: the spacing of representable
+// values is 2^(floor(log2|v|) - 3) from the smallest normal 2^-6 up and 2^-9
+// below it; the rounded magnitude is then split into exponent and mantissa
+// fields (rounding may have carried it into the next binade).  All steps
+// are exact in fp32 except the one rounding of rintf.
+__device__ __forceinline__ uint32_t e4m3_code(float v) {
+  const float a = fabsf(v);
+  uint32_t code = 0;
+  if (a > 0.f) {
+    int ea;
+    (void)frexpf(a, &ea);                       // a = f 2^ea, 0.5 <= f < 1
+    const int qe = a >= 0x1p-6f ? ea - 4 : -9;
+    const float q = ldexpf(rintf(ldexpf(a, -qe)), qe);
+    if (q >= 0x1p-6f) {
+      int eq;
+      (void)frexpf(q, &eq);
+      code = ((uint32_t)(eq + 6) << 3) | (uint32_t)(ldexpf(q, 1 - eq) * 8.0f - 8.0f);
+    } else {
+      code = (uint32_t)ldexpf(q, 9);
+    }
+  }
+  return v < 0.f ? (code | 0x80u) : code;
+}
+
+// One workgroup per row: the row's largest magnitude gives the scale 2^E
+// with E the smallest integer such that amax / 2^E <= 448 (amax = f 2^x,
+// 448 = 0.875 2^9: E = x - 9, or x - 8 when f > 0.875; 0 for a zero row),
+// then every element is coded as w / 2^E.
+__global__ __launch_bounds__(256) void k_quant_fp8_rows(const bf16_t* __restrict__ W, int cols,
+                                                        uint8_t* __restrict__ Q, float* __restrict__ scale) {
+  __shared__ float red[4];
+  const size_t row = blockIdx.x;
+  const bf16_t* w = W + row * cols;
+  float amax = 0.f;
+  for (int c = threadIdx.x; c < cols; c += 256) amax = fmaxf(amax, fabsf(bf2f_m(w[c])));
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  int E = 0;
+  if (amax > 0.f) {
+    int x;
+    const float f = frexpf(amax, &x);
+    E = x - 9 + (f > 0.875f ? 1 : 0);
+  }
+  for (int c = threadIdx.x; c < cols; c += 256) Q[row * cols + c] = (uint8_t)e4m3_code(ldexpf(bf2f_m(w[c]), -E));
+  if (threadIdx.x == 0) scale[row] = ldexpf(1.0f, E);
+}
+
+hipError_t launch_quant_fp8_rows(const void* W, int rows, int cols, uint8_t* Q, float* scale, hipStream_t st) {
+  if (rows < 1 || cols < 1) return hipErrorInvalidValue;
+  k_quant_fp8_rows<<<rows, 256, 0, st>>>((const bf16_t*)W, cols, Q, scale);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ debug
 __global__ void k_scatter_logits(const float* __restrict__ logits, const int32_t* __restrict__ hdr,
                                  const int32_t* __restrict__ lm_row,

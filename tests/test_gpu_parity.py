@@ -64,23 +64,29 @@ SMALL = {
 _models = {}
 
 
-def get_model(w):
+def get_model(w, wq=None):
+    """The GPU model and the weights the oracle uses: for fp8 models the
+    oracle's own quantization of the layer projections, dequantized."""
     from paper_2609_33887_amd import bd
-    key = (w.name, w.seed)
+    key = (w.name, w.seed, wq)
     if key not in _models:
         ws = make_weights(w)
-        _models[key] = (bd.Model(w, ws), ws)
+        model = bd.Model(w, ws, wq=wq)
+        if wq == "fp8":
+            from oracle.quant import fp8_weights
+            ws = fp8_weights(w, ws)
+        _models[key] = (model, ws)
     return _models[key]
 
 
 def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None, tau_semi=None,
-               tau_add=0.0, skip_masked=False):
+               tau_add=0.0, skip_masked=False, wq=None):
     from oracle.model import OracleModel
     from tests.gpu_harness import capture_gpu_trace, lockstep
     _need_gpu()
     _say(f"[parity] {w.name} tau={tau} b={w.batch} P={w.prompt_len} G={w.gen_len} B={w.block_size} "
-         f"nb={w.n_inflight} tau_semi={tau_semi} tau_add={tau_add} skip={skip_masked}")
-    model, ws = get_model(w)
+         f"nb={w.n_inflight} tau_semi={tau_semi} tau_add={tau_add} skip={skip_masked} wq={wq}")
+    model, ws = get_model(w, wq)
     prompts = make_prompts(w)
     ids = list(range(w.batch)) if seq_ids is None else list(seq_ids)
     tr = capture_gpu_trace(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size,
@@ -188,6 +194,100 @@ def _check_participation_identities(tr, nb, G, B):
     _say(f"  no-op share {s['zero_commit'] / s['active_forwards']:.3f}; static rule saves "
          f"{s['static_saved'] / s['active_forwards']:.3f} of active block-forwards, defers "
          f"{s['static_deferred'] / s['active_forwards']:.3f}")
+
+
+# ---------------------------------------------------------------- fp8 weights
+def test_quantize_fp8_matches_oracle():
+    """bd_quantize_fp8 against the oracle's quantizer, code for code and
+    scale for scale: random bf16 rows of several magnitudes, a zero row, rows
+    whose maximum sits exactly on a scale boundary (448 2^k) or just past it,
+    and rows of exact rounding midpoints."""
+    from paper_2609_33887_amd import bd
+    from oracle.quant import quantize_fp8_rows
+    from bd_synth import f32_to_bf16_bits
+    _need_gpu()
+    rng = np.random.default_rng(41)
+    rows = [rng.normal(0, s, 300) for s in (0.02, 1.0, 1e-4, 37.0)]
+    rows.append(np.zeros(300))
+    for k in (-12, 0, 3):
+        r = rng.uniform(-1, 1, 300) * 448 * 2.0 ** k
+        r[7] = 448 * 2.0 ** k
+        rows.append(r)
+        r2 = r.copy()
+        r2[7] = 452 * 2.0 ** k     # bf16-exact, just past the boundary
+        rows.append(r2)
+    # midpoints between neighbouring E4M3 values (scale 1: the row maximum is 448)
+    from oracle.quant import e4m3_value
+    vals = np.unique(e4m3_value(np.arange(0, 127, dtype=np.uint8)))
+    mids = (vals[:-1] + vals[1:]) / 2
+    r = np.zeros(300)
+    r[:len(mids)] = mids[:300]
+    r[299] = 448.0
+    rows.append(r)
+    rows.append(-r)
+    W = np.stack(rows)
+    bits = f32_to_bf16_bits(W.astype(np.float32))
+    wb = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    codes, scale = bd.quantize_fp8(bits)
+    oc, oe = quantize_fp8_rows(wb)
+    np.testing.assert_array_equal(scale, np.ldexp(1.0, oe).astype(np.float32))
+    np.testing.assert_array_equal(codes, oc)
+
+
+@pytest.mark.parametrize("name", ["mha64", "gqa128_ragged", "moe", "stream128"])
+@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
+def test_small_models_fp8(name, tau):
+    """fp8 E4M3 decoder-layer weights (precision axis of the configuration):
+    the GPU decode against the oracle run on the oracle's own quantization of
+    the weights, at the bf16 tolerances."""
+    run_parity(SMALL[name], tau, wq="fp8")
+
+
+def test_config1_dense_fp8_full_size():
+    """Full-size dense model with fp8 layer weights at tau 0.9: the GPU
+    decodes the batch, the oracle replays sequence 3."""
+    run_parity(workload(1), 0.9, seq_ids=[3], logits=True, logit_steps=3, wq="fp8")
+
+
+def test_precision_sweep_matches_oracle():
+    """Redline over the precision axis on the small MHA model, 48 calibration
+    prompts: bf16 weights at acc 0.9 as the reference, fp8 layer weights at
+    acc 0.9 and 0.8 as candidates, cost = weight-memory reduction.  Counts,
+    valid set and the deployed configuration equal the oracle's on the
+    GPU-decoded matrix (each fp8 decode is checked against the oracle by
+    test_small_models_fp8)."""
+    from paper_2609_33887_amd import bd
+    from paper_2609_33887_amd.sweep import precision_sweep, weight_bytes
+    from oracle import redline as orl
+    _need_gpu()
+    w = SMALL["mha64"]
+    models = {"bf16": get_model(w)[0], "fp8": get_model(w, "fp8")[0]}
+    prompts = make_prompts(w, 48)
+    r = precision_sweep(w, models, prompts, w.gen_len, w.block_size, ("bf16", (0.9, 2)),
+                        [("fp8", (0.9, 2)), ("fp8", (0.8, 2))], 0.10, 0.10, tail=8, batch=16, progress=_say)
+    assert r["weight_bytes"][1] < r["weight_bytes"][0] == weight_bytes(w)
+    o = orl.select(r["correct"], r["cost"], 0, 0.10, 0.10)
+    assert r["V"].tolist() == o.V.tolist() and r["valid"].tolist() == o.valid.tolist()
+    assert r["selected"] == o.selected
+    _say(f"  V {r['V'].tolist()} valid {r['valid'].tolist()} deployed {r['labels'][r['selected']]}")
+
+
+def test_fp8_model_errors():
+    from paper_2609_33887_amd import bd
+    _need_gpu()
+    w = SMALL["f32_gqa"]
+    with pytest.raises(bd.BDError) as e:
+        bd.Model(w, make_weights(w), wq="fp8")
+    assert e.value.status == bd.BD_EUNSUPPORTED
+    w = SMALL["mha64"]
+    cfg = bd.model_cfg_from(w)
+    cfg.wq = 7
+    with pytest.raises(bd.BDError) as e:
+        bd.bd_init_model(cfg, [0] * 17, 0)
+    assert e.value.status == bd.BD_EINVAL
+    with pytest.raises(bd.BDError) as e:
+        bd.bd_quantize_fp8(0, 4, 4, 0, 0)
+    assert e.value.status == bd.BD_EINVAL
 
 
 def test_config0_tiny_f32():
