@@ -7,7 +7,7 @@
  * block, causal across blocks and to the prefix), a mask-suppressed LM-head
  * softmax per masked position giving confidence and argmax (App. B.1), and
  * the threshold commit rule with in-order block commit and a one-step cache
- * write (App. C, App. G).  It also exports the host-side Redline selection
+ * write (App. C, App. F).  It also exports the host-side Redline selection
  * test (§4.2, App. A).
  *
  * Conventions
@@ -56,7 +56,7 @@ typedef struct {
     int32_t dtype;         /* bd_dtype of matrices, activations and KV cache */
     int32_t wq;            /* weight precision of the decoder-layer projections
                               (the precision axis of a serving configuration,
-                              §4.3 and the quantization grid of App. E):
+                              §4.2 (iv) and the quantization grid of App. E):
                               BD_WQ_NONE keeps the model dtype; BD_WQ_FP8 (bf16
                               models only) has bd_init_model quantize every
                               decoder-layer projection (QKV, O, gate, up, down,
@@ -72,7 +72,7 @@ typedef struct {
 enum { BD_WQ_NONE = 0, BD_WQ_FP8 = 1 };
 
 /* One serving configuration: the paper's operating point lambda (§2.1, the
- * notation table and App. G): accept threshold, in-flight block count, block
+ * notation table and App. F): accept threshold, in-flight block count, block
  * size, semi-completion and admission thresholds.  "Resolved fraction" below
  * is (unmasked positions of a block) / B as a float32 ratio, compared with
  * the threshold as float32. */
@@ -162,7 +162,7 @@ bd_status bd_quantize_fp8(const void* w_dev, int32_t rows, int32_t cols, uint8_t
  * bd_prefill -- encode b prompts and create a decode state.
  *  prompt_dev: int32 [b][P] device.  The prompt forward runs under the same
  *  block-causal mask with no LM head (prompt steps are not counted as
- *  forwards, App. G.1).  Afterwards the first min(n_inflight, G/B) blocks of
+ *  forwards, App. F.1).  Afterwards the first min(n_inflight, G/B) blocks of
  *  every sequence are active and fully masked.
  *  Errors: BD_EINVAL if b < 1, P < 0, G < 1, B < 1, n_inflight < 1,
  *  P % B != 0, G % B != 0, tau is NaN, skip_masked not 0 or 1, or a prompt

@@ -3,7 +3,7 @@
 One sequence is decoded as a state machine over generation blocks, following
 the engine description of the paper:
 
-* Block slots (App. G): a generation block is a placeholder (all mask, not
+* Block slots (App. F): a generation block is a placeholder (all mask, not
   admitted), active (admitted, being denoised), committed and awaiting its
   cache write, or cached.  Here a committed block waiting for its cache write
   is called *pending*.
@@ -14,16 +14,16 @@ the engine description of the paper:
 * Commit sweep (App. C.2, part 1): blocks are visited oldest first; a complete
   active block whose predecessors are all committed becomes committed, chains
   commit in one step, and the sweep stops at the first incomplete block.
-* One-step cache write (App. G.2): a committed block's K/V are recomputed
+* One-step cache write (App. F.2): a committed block's K/V are recomputed
   from its clean tokens in the next forward, where its rows ride along in
   front of the active blocks; after that forward it is cached.
-* Admission (App. G: the admission threshold turns a placeholder into an
+* Admission (App. F: the admission threshold turns a placeholder into an
   active block): at the end of a step, and after the prefill, placeholders
   are admitted in order while fewer than ``n_inflight`` blocks are active and
   either no block is active or the youngest active block has resolved a
   fraction >= ``tau_add`` of its positions.  ``tau_add <= 0`` refills every
   free slot at once.
-* Semi-completion (App. G: the accept and semi-completion thresholds decide
+* Semi-completion (App. F: the accept and semi-completion thresholds decide
   which positions an active block resolves): with ``tau_semi`` given, an
   active block whose predecessor is still active and has resolved a fraction
   < ``tau_semi`` of its positions is semi-activated and commits only positions
@@ -47,7 +47,7 @@ the engine description of the paper:
   live skip rule left out.
 * TPF (§2.1): tokens committed per model forward; a forward is a step in
   which the sequence has at least one active block.  Prefill is not counted
-  (App. G.1).
+  (App. F.1).
 """
 from __future__ import annotations
 

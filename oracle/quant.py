@@ -2,7 +2,7 @@
 
 The paper treats numeric precision as one axis of a serving configuration and
 calibrates weight quantization against bf16 weights as the reference, with the
-embeddings and the output head kept in bf16 (§4.3 and the quantization grid
+embeddings and the output head kept in bf16 (§4.2 (iv) and the quantization grid
 of App. E).  The format here is the OCP fp8 E4M3 encoding that gfx950's
 matrix cores read, with one power-of-two scale per output row:
 

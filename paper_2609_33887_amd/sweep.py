@@ -12,7 +12,7 @@ Grids: ``tau-nb`` -- accept threshold x in-flight blocks against the
 one-token-per-step reference; ``engine`` -- accept {0.85, 0.90, 0.95, 0.99} x
 semi-completion {0.70, 0.90} at admission 0.10 and two blocks in flight, with
 the engine default acc95/semi90 as the reference (the shape of the paper's
-grids, App. G); ``precision`` -- the same decode configuration served with
+grids, App. D); ``precision`` -- the same decode configuration served with
 bf16 weights (the reference) and with fp8 E4M3 layer weights, deploying the
 valid configuration with the least weight memory (the paper's quantization
 grid: §4.2 (iv) "for quantization the one with the least memory").

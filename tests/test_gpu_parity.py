@@ -129,7 +129,7 @@ def test_degenerate_thresholds(tau):
         assert (tr.forwards == w.gen_len).all()
 
 
-# semi-completion / admission thresholds (App. G): acc x semi x add points
+# semi-completion / admission thresholds (App. F): acc x semi x add points
 # like the paper's grids, on multi-block small models
 ENGINE_POINTS = [(0.9, 0.7, 0.1), (0.85, 0.9, 0.3), (0.95, 0.5, 0.0), (2.0, 0.0, 0.0)]
 

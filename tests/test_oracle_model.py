@@ -173,7 +173,7 @@ SEMI_CASES = [(P, B, nb, tau, ts, ta) for B in (2, 4) for P in range(0, 8 - B, B
 
 @pytest.mark.parametrize("P,B,nb,tau,tau_semi,tau_add", SEMI_CASES)
 def test_decode_with_semi_and_add_matches_brute_force(P, B, nb, tau, tau_semi, tau_add):
-    """The semi-completion and admission thresholds (App. G): cached oracle
+    """The semi-completion and admission thresholds (App. F): cached oracle
     decode = full recomputation with the rules restated independently."""
     G = 8 - P
     cfg, ws, m = _model(TinyCfg())
@@ -295,7 +295,7 @@ def test_participation_closed_forms(nb, tau, ts):
       block-forwards are the sum over steps of the blocks neither swept nor
       unadmitted, min(nb, blocks not yet swept) without admission thresholds;
     * cache writes: every block swept before a sequence's final step is
-      recomputed by the next one (App. G.2);
+      recomputed by the next one (App. F.2);
     * n_inflight = 1: no block has an older active block;
     * tau > 1 without semi-completion: exactly one block commits per step,
       so the zero-commit forwards are the active forwards minus the forwards;
