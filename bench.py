@@ -82,14 +82,16 @@ def measured_traffic(workload_name, kernel_class):
     summary of this workload (FETCH_SIZE and WRITE_SIZE passes, scaled by the
     plain-copy calibration), or None when there is none or when the kernel
     source has changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"{workload_name}_{kernel_class}_hbm_counters.md")
+    path = os.path.join(ROOT, "profiles", f"{workload_name}_hbm_counters.md")
     if not os.path.exists(path):
         return None
     rec = {}
     with open(path) as f:
         for line in f:
             if line.startswith("counters:"):
-                rec = dict(kv.split("=", 1) for kv in line.split()[1:])
+                r = dict(kv.split("=", 1) for kv in line.split()[1:])
+                if r.get("class") == kernel_class:
+                    rec = r
     if not rec or source_tag(os.path.join(ROOT, rec["source"])) != rec["source_sha256_12"]:
         return None
     return {"bytes_per_launch": float(rec["bytes_per_launch"]),
