@@ -13,6 +13,8 @@ Modules
              one-step cache write, as a per-sequence state machine.
   redline -- reference-relative violation counts, exact binomial p-values,
              Holm step-down and the fastest-valid deployment rule.
+  quant   -- fp8 E4M3 weight quantization with a power-of-two scale per
+             output row (the precision axis of a configuration).
 
 Parity pins (see the tests under ``tests/``) tie every function here to
 something other than itself: closed forms, brute force, textbook special

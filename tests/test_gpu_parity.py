@@ -316,6 +316,17 @@ def test_config2_multiblock_full_size(tau):
     _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
 
 
+def test_config2_multiblock_static_skip_full_size():
+    """Full-size multi-block model under the static skip rule at tau 0.9: the
+    oracle (with the same rule) replays sequence 5 for 16 steps; the GPU's
+    own trace must forward only the oldest active block (active
+    block-forwards = forwards, nothing saved or deferred)."""
+    w = workload(2)
+    tr, _ = run_parity(w, 0.9, seq_ids=[5], max_steps=16, logit_steps=2, skip_masked=True)
+    assert tr.stats["active_forwards"] == int(tr.forwards.sum())
+    assert tr.stats["static_saved"] == tr.stats["static_deferred"] == 0 and tr.stats["skipped"] > 0
+
+
 def test_config3_long_prefix_full_size():
     """Full-size long-prefix model (prompts of 8192 tokens encoded by the
     prefill, block 64, 2 blocks in flight, batch 8) at tau 0.8: the oracle
