@@ -5,7 +5,8 @@
 // so one key range [0, end of the query's block) covers prefix and window.
 //
 // bf16 kernel (Q, K and V are bf16 hi/lo pairs in two planes; V is kept
-// transposed in the cache, in tiles of 64 keys [dim][64]): one workgroup =
+// transposed in the cache, in tiles of 64 keys [dim][64 slots], the keys of
+// each 32-key group in the slot order of vt_slot): one workgroup =
 // 16 NW queries of one (sequence, kv head) -- window rows x the q-heads that
 // share the kv head -- as NW wave64s x 16 queries (NW = 2 when a window
 // holds at most 32 such queries, else 4); a wave with no query of its own
@@ -129,7 +130,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict_
         pkl[it] = *(const u32x4*)(Kp + o + k_plane);                            \
       }                                                                         \
       const int dim = ci / (AK / 8), kc8 = (ci % (AK / 8)) * 8;                 \
-      const size_t ov = vt_off((K0) + kc8, dim, HD);                            \
+      const size_t ov = vt_row((K0), dim, HD) + kc8;                            \
       pvh[it] = *(const u32x4*)(Vp + ov);                                       \
       pvl[it] = *(const u32x4*)(Vp + ov + v_plane);                             \
     }                                                                           \
@@ -207,24 +208,16 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict_
         pl[st >> 1][(st & 1) * 4 + r] = __builtin_bit_cast(__bf16, lb);
       }
     // O^T += V^T P^T over 2 chunks of 32 keys; k-slot 8g+r <-> key 32kc+4g+r,
-    // k-slot 8g+4+r <-> key 32kc+16+4g+r (same permutation as the scores):
-    // Vh.Ph + Vh.Pl + Vl.Ph
+    // k-slot 8g+4+r <-> key 32kc+16+4g+r (same permutation as the scores),
+    // which the V^T slot order (vt_slot) stores as slots 32kc+8g..+7: one
+    // 16-byte read per plane.  Vh.Ph + Vh.Pl + Vl.Ph
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
 #pragma unroll
       for (int t = 0; t < HD / 16; ++t) {
-        const int off = (t * 16 + c) * VP + kc * 32 + 4 * g;
-        bf16x8 vh, vl;
-        {
-          const bf16x4 a0 = *(const bf16x4*)(sVh + off);
-          const bf16x4 a1 = *(const bf16x4*)(sVh + off + 16);
-          const bf16x4 b0 = *(const bf16x4*)(sVl + off);
-          const bf16x4 b1 = *(const bf16x4*)(sVl + off + 16);
-          vh[0] = a0[0]; vh[1] = a0[1]; vh[2] = a0[2]; vh[3] = a0[3];
-          vh[4] = a1[0]; vh[5] = a1[1]; vh[6] = a1[2]; vh[7] = a1[3];
-          vl[0] = b0[0]; vl[1] = b0[1]; vl[2] = b0[2]; vl[3] = b0[3];
-          vl[4] = b1[0]; vl[5] = b1[1]; vl[6] = b1[2]; vl[7] = b1[3];
-        }
+        const int off = (t * 16 + c) * VP + kc * 32 + 8 * g;
+        const bf16x8 vh = __builtin_bit_cast(bf16x8, *(const u32x4*)(sVh + off));
+        const bf16x8 vl = __builtin_bit_cast(bf16x8, *(const u32x4*)(sVl + off));
         oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, ph[kc], oacc[t], 0, 0, 0);
         oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, pl[kc], oacc[t], 0, 0, 0);
         oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl, ph[kc], oacc[t], 0, 0, 0);

@@ -188,16 +188,27 @@ __device__ __forceinline__ int xcd_item(int id, int items) {
 
 // One layer's KV cache.  K: [seq][kv head][pos][hd].  V: bf16 models keep
 // it transposed in tiles of 64 keys, [seq][kv head][pos / 64][hd][64]: a
-// tile is one contiguous block per plane (DRAM page locality when streamed)
-// and a 16-byte load holds 8 consecutive keys of one dimension (the MFMA
-// operand layout of P.V); vt_off gives the offset inside a (seq, kv head)
-// slice of hd * vstride elements, vstride = maxpos rounded up to 64.  fp32
+// tile is one contiguous block per plane (DRAM page locality when streamed).
+// Inside a tile row, key k sits at slot vt_slot(k): every group of 32 keys is
+// reordered so that keys 4j..4j+3 and 16+4j..16+4j+3 fill the 8 adjacent
+// slots 8j..8j+7 -- the 8 keys one lane feeds to a P.V MFMA, so that
+// fragment is one 16-byte read; aligned runs of 4 keys stay contiguous.
+// vt_off gives the offset of (pos, dim) inside a (seq, kv head) slice of
+// hd * vstride elements, vstride = maxpos rounded up to 64; vt_row the
+// offset of slot 0 of a tile row.  fp32
 // models keep V as K.  bf16 models store pairs: lo planes at + k_plane /
 // + v_plane elements.  The whole cache is cleared at allocation, so padding
 // and not yet written positions are finite.
 constexpr int VTILE = 64;
+__host__ __device__ __forceinline__ int vt_slot(int k) {
+  const int q = k & 31;
+  return (k & 32) + 8 * ((q & 15) >> 2) + 4 * (q >> 4) + (q & 3);
+}
+__host__ __device__ __forceinline__ size_t vt_row(int pos, int dim, int hd) {
+  return ((size_t)(pos / VTILE) * hd + dim) * VTILE;
+}
 __host__ __device__ __forceinline__ size_t vt_off(int pos, int dim, int hd) {
-  return ((size_t)(pos / VTILE) * hd + dim) * VTILE + (pos % VTILE);
+  return vt_row(pos, dim, hd) + vt_slot(pos % VTILE);
 }
 struct KvView {
   void* K;
