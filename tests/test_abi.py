@@ -249,3 +249,31 @@ def test_redline_variants_reject_bad_arguments():
                             np.asarray(cost).ctypes.data_as(bd._f64), 0.1, 0.1, 7, None, None, None, None,
                             bd.ctypes.byref(bd.ctypes.c_int32()))
     assert code == bd.BD_EINVAL and "unknown procedure" in bd.bd_last_error()
+
+
+def test_weight_bytes_counts_every_tensor():
+    """The weight-memory cost of the precision sweep against a count over
+    the ABI tensor list: bf16 matrices 2 bytes, fp32 norms and router 4;
+    with fp8 the decoder-layer projections take 1 byte plus a 4-byte scale
+    per output row."""
+    import numpy as np
+    from bd_synth import Workload, tensor_specs
+    from oracle.quant import quantized_layer_slots
+    from paper_2609_33887_amd.sweep import weight_bytes
+    for kw in (dict(ffn_dim=512), dict(ffn_dim=0, n_experts=8, top_k=2, expert_ffn=128, n_shared=1),
+               dict(ffn_dim=0, n_experts=4, top_k=1, expert_ffn=128, n_shared=0)):
+        w = Workload(name="wb", seed=1, n_layers=3, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                     vocab=1024, dtype="bf16", batch=1, prompt_len=8, block_size=4, n_inflight=1, gen_len=8,
+                     **kw)
+        specs = tensor_specs(w)
+        slots = set(quantized_layer_slots(w))
+        bf16 = fp8 = 0
+        for i, (name, shape, kind) in enumerate(specs):
+            n = int(np.prod(shape))
+            if n == 0:
+                continue
+            size = 4 * n if kind in ("norm", "router") else 2 * n
+            bf16 += size
+            fp8 += (n + 4 * (n // shape[-1])) if i in slots else size
+        assert weight_bytes(w) == bf16
+        assert weight_bytes(w, "fp8") == fp8
