@@ -277,3 +277,33 @@ def test_weight_bytes_counts_every_tensor():
             fp8 += (n + 4 * (n // shape[-1])) if i in slots else size
         assert weight_bytes(w) == bf16
         assert weight_bytes(w, "fp8") == fp8
+
+
+def test_argument_errors_before_any_device_work():
+    """Argument checks of the entry points that return before any HIP call
+    (so they run without a GPU): fp8 quantization of a NULL or empty matrix,
+    an unknown weight precision, fp8 weights on an fp32 model, and NULL
+    handles."""
+    import ctypes
+    from paper_2609_33887_amd import bd
+    from bd_synth import Workload
+    lib = bd.lib
+    assert lib.bd_quantize_fp8(None, 4, 4, None, None, None) == bd.BD_EINVAL
+    assert lib.bd_quantize_fp8(ctypes.c_void_p(16), 0, 4, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                               None) == bd.BD_EINVAL
+    assert "rows, cols" in bd.bd_last_error()
+    w = Workload(name="e", seed=1, n_layers=1, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                 ffn_dim=512, vocab=1024, dtype="bf16", batch=1, prompt_len=8, block_size=4,
+                 n_inflight=1, gen_len=8)
+    out = ctypes.c_void_p()
+    arr = (ctypes.c_void_p * 10)()
+    cfg = bd.model_cfg_from(w)
+    cfg.wq = 7
+    assert lib.bd_init_model(ctypes.byref(cfg), arr, 10, None, ctypes.byref(out)) == bd.BD_EINVAL
+    cfg.wq = bd.BD_WQ_FP8
+    cfg.dtype = bd.BD_F32
+    assert lib.bd_init_model(ctypes.byref(cfg), arr, 10, None, ctypes.byref(out)) == bd.BD_EUNSUPPORTED
+    dc = bd.decode_cfg(0.9, 1, 4, skip_masked=True)
+    assert lib.bd_prefill(None, None, 1, 8, 8, ctypes.byref(dc), ctypes.byref(out)) == bd.BD_EINVAL
+    stats = (ctypes.c_int64 * 12)()
+    assert lib.bd_state_stats(None, None, stats, 12) == bd.BD_EINVAL
