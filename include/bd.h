@@ -97,7 +97,7 @@ typedef struct {
                               none is active or the youngest active block's
                               resolved fraction is >= tau_add; <= 0 refills
                               every free slot at once */
-    int32_t skip_masked;   /* static skip rule (§3 "The allocation lever"),
+    int32_t skip_masked;   /* static skip rule (§3.3),
                               0 or 1: 1 leaves an active block that is still
                               fully masked at the start of a step out of that
                               step's forward (no rows, no confidences, no
@@ -236,7 +236,7 @@ bd_status bd_state_steps(const bd_state* st, int32_t* steps_out);
  *   forwarded (sum of M), [2] LM-head rows (masked positions), [3] visible
  *   query-key pairs per head (block-causal), [4] keys read per kv head
  *   (prefix + window, summed over sequences), [5] tokens committed;
- *   participation (App. "Participation schedules"), summed over sequences
+ *   participation (App. B.3), summed over sequences
  *   and steps: [6] active block-forwards, [7] of those, forwards of a block
  *   that commits nothing in the step, [8] forwards of a block that was fully
  *   masked at the start of the step behind an older active block and commits
@@ -292,7 +292,7 @@ bd_status rl_risk_select(int32_t n, int32_t m, int32_t ref_index, const uint8_t*
                          int32_t* near_ties_out);
 
 /*
- * Multiple-testing procedures (App. A.3 and the baselines of App. D); valid
+ * Multiple-testing procedures (App. A.3, A.4 and the baselines of App. D); valid
  * means the null R(lambda) > alpha is rejected.
  *  RL_HOLM            Holm step-down at family-wise level delta (primary).
  *  RL_BONFERRONI      p <= delta / m.

@@ -34,10 +34,10 @@ the engine description of the paper:
   Without ``tau_semi`` the forced commit is one per sequence, over all active
   blocks (the base rule above).  Resolved fractions are float32 ratios
   compared with float32 thresholds.
-* Static skip rule (§3 "The allocation lever", App. "Participation
-  schedules"): with ``skip_masked`` an active block that is still fully
-  masked at the start of a step is left out of that step's forward while an
-  older block is active; it gets no confidences and no commits.
+* Static skip rule (§3.3, App. B.3): with ``skip_masked`` an active block
+  that is still fully masked at the start of a step is left out of that
+  step's forward while an older block is active; it gets no confidences and
+  no commits.
 * Participation counters (the same appendix, measured here on the live
   decode rather than on a replayed trace), summed over steps: active
   block-forwards, those that commit nothing, those the static rule would

@@ -103,7 +103,7 @@ def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=No
     assert rep.max_conf_diff <= ctol
     assert rep.max_logit_diff <= ltol
     if rep.complete and len(ids) == w.batch:
-        # participation counters (App. "Participation schedules"): bit-exact
+        # participation counters (App. B.3): bit-exact
         gp = {k: tr.stats[k] for k in rep.participation}
         _say(f"  participation GPU {gp}")
         assert gp == rep.participation, (gp, rep.participation)
@@ -153,7 +153,7 @@ def test_config2_multiblock_semi_add():
 @pytest.mark.parametrize("name", ["mha64", "gqa128_ragged", "moe", "f32_gqa"])
 @pytest.mark.parametrize("tau,tau_semi", [(0.9, None), (0.7, None), (0.85, 0.7)])
 def test_small_models_static_skip(name, tau, tau_semi):
-    """Static skip rule (§3 "The allocation lever"): parity with the oracle's
+    """Static skip rule (§3.3): parity with the oracle's
     skip rule and its participation counters, and the closed form that
     follows from the rule -- the decode is the one-block-in-flight decode,
     bit for bit, with the admitted blocks behind the oldest never forwarded."""

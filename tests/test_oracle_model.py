@@ -234,8 +234,8 @@ SKIP_CASES = [(P, B, nb, tau, ts, skip) for B in (1, 2, 4) for P in range(0, 8 -
 
 @pytest.mark.parametrize("P,B,nb,tau,tau_semi,skip", SKIP_CASES)
 def test_participation_and_skip_match_brute_force(P, B, nb, tau, tau_semi, skip):
-    """Participation counters (App. "Participation schedules") and the live
-    static skip rule (§3 "The allocation lever"): cached oracle decode = full
+    """Participation counters (App. B.3) and the live
+    static skip rule (§3.3): cached oracle decode = full
     recomputation with the rule and the counts restated independently."""
     G = 8 - P
     cfg, ws, m = _model(TinyCfg())

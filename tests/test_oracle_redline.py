@@ -73,7 +73,7 @@ def test_unlock_table():
 
 
 def test_holm_beats_bonferroni_at_alpha_007():
-    """App. D.2: on LLaDA2 math at alpha = 0.07, acc90/semi90 (p = 0.0190)
+    """App. D.3: on LLaDA2 math at alpha = 0.07, acc90/semi90 (p = 0.0190)
     fails Bonferroni's 0.1/7 and passes Holm's threshold at its rank."""
     rows = load("grid_llada2_math")
     tpf = [float(r["tpf"]) for r in rows]
@@ -105,7 +105,7 @@ def test_samplesize_margin():
 
 @pytest.mark.parametrize("delta", [0.05, 0.01])
 def test_delta_sensitivity_math(delta):
-    """App. D.2: the math deployments at alpha = 0.10 survive delta = 0.05 and 0.01."""
+    """App. D.3: the math deployments at alpha = 0.10 survive delta = 0.05 and 0.01."""
     for grid, want in (("grid_llada2_math", "acc85/semi70"), ("grid_sdar_math", "acc90/semi90")):
         rows = load(grid)
         ps = [rl.binom_pvalue(1012, 0.10, int(r["k"])) for r in rows]
@@ -284,7 +284,7 @@ def test_alpha_sweep_reproduces_unlock_table():
 
 
 def test_alpha_sweep_bonferroni_example():
-    """App. D.2 at alpha = 0.07: the sweep under Bonferroni deploys acc95/semi70
+    """App. D.3 at alpha = 0.07: the sweep under Bonferroni deploys acc95/semi70
     where Holm deploys acc90/semi90."""
     rows = load("grid_llada2_math")
     tpf = [float(r["tpf"]) for r in rows]
