@@ -196,6 +196,24 @@ def _check_participation_identities(tr, nb, G, B):
          f"{s['static_deferred'] / s['active_forwards']:.3f}")
 
 
+# ---------------------------------------------------------------- edge cases
+def test_empty_prompt():
+    """No prompt (P = 0): the first blocks attend only to themselves and the
+    cache starts empty."""
+    run_parity(small("noprompt", seed=98, batch=2, prompt_len=0, block_size=16, n_inflight=2,
+                     gen_len=64), 0.9)
+
+
+def test_maximum_batch_and_inflight():
+    """256 sequences (the most a state holds) with 8 blocks in flight (the
+    most the commit kernel tracks), every block admitted at once: the GPU
+    decodes the batch, the oracle replays three sequences."""
+    w = small("maxsize", seed=99, vocab=512, batch=256, prompt_len=16, block_size=8, n_inflight=8,
+              gen_len=64)
+    tr, _ = run_parity(w, 0.9, seq_ids=[0, 137, 255], logits=False)
+    assert tr.stats["forwards"] >= 1 and (tr.commit_step >= 0).all()
+
+
 # ---------------------------------------------------------------- fp8 weights
 def test_quantize_fp8_matches_oracle():
     """bd_quantize_fp8 against the oracle's quantizer, code for code and
