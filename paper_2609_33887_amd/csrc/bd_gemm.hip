@@ -764,13 +764,18 @@ static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t
   }
 }
 
-// Tile choice: 128x128 when that tiling gives at least 512 workgroups over
-// the row capacity (the 64x64 tile runs out of LDS bandwidth on large
-// products), else 64x64.  zmax: the largest residual split (1 = none).
-GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap) {
+// Tile choice: 128x128 when that tiling gives enough workgroups over the
+// row capacity (the 64x64 tile runs out of LDS bandwidth on large products),
+// else 64x64.  Enough: 1024 for plain products (below that the 128x128 grid
+// leaves part of the chip idle for a round: the gate/up product of the dense
+// decode, 512 workgroups over its 1024-row capacity, runs 6% faster in
+// 64x64 tiles), 512 for residual projections, whose split-K partials grow
+// with the tile count (the multi-block O projection ran 18% slower in 64x64
+// tiles).  zmax: the largest residual split (1 = none).
+GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid) {
   (void)K;
   if (!is_bf16) return GemmPlan{64, 64, 1};
-  if (N % 128 == 0 && (N / 128) * cdiv(rows_cap, 128) >= 512) return GemmPlan{128, 128, 1};
+  if (N % 128 == 0 && (N / 128) * cdiv(rows_cap, 128) >= (resid ? 512 : 1024)) return GemmPlan{128, 128, 1};
   return GemmPlan{64, 64, 1};
 }
 
@@ -807,7 +812,7 @@ hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plan
                        wscale);
   // deep products (K >= 4096) take 128x128 tiles: with K split, their A and
   // W re-reads halve against 64x64 at the same parallelism
-  GemmPlan p = plan_gemm(true, N, K, rows_cap);
+  GemmPlan p = plan_gemm(true, N, K, rows_cap, true);
   if (K >= 4096 && N % 128 == 0) p = GemmPlan{128, 128, 1};
   p.zmax = 8;
   hipError_t e = launch_gemm_planned(p, EPI_ADD_F32, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap,

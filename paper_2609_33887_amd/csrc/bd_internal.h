@@ -147,7 +147,7 @@ hipError_t launch_transpose_f32(const float* in, float* out, int rows, int cols,
 struct GemmPlan {
   int bm, bn, zmax;        // tile; largest residual K-split (1 = none)
 };
-GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap);
+GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid = false);
 // bf16 GEMM with an explicit plan (128x128 or 64x64; K % KALIGN == 0;
 // zmax > 1 only for EPI_ADD_F32 with a residual-split workspace ws).
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
