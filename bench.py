@@ -157,7 +157,7 @@ def main():
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (batch rows would shard "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (batch rows would shard "
               "across GPUs with no exchange during decode)", file=sys.stderr)
         sys.exit(2)
 

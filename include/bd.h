@@ -38,7 +38,7 @@ typedef enum {
     BD_ENOMEM = -2,        /* device or host allocation failed */
     BD_EHIP = -3,          /* a HIP runtime call failed */
     BD_ESTATE = -4,        /* call not valid in the object's current state */
-    BD_EUNSUPPORTED = -5   /* valid but not supported by this build */
+    BD_EUNSUPPORTED = -5   /* valid but not supported by this library */
 } bd_status;
 
 typedef enum { BD_F32 = 0, BD_BF16 = 1 } bd_dtype;

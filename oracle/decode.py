@@ -7,7 +7,7 @@ the engine description of the paper:
   admitted), active (admitted, being denoised), committed and awaiting its
   cache write, or cached.  Here a committed block waiting for its cache write
   is called *pending*.
-* Commit rule (benchmark spec; single-block form in App. B.2): every
+* Commit rule (stated for one block in App. B.2, applied per sequence): every
   masked position of an active block whose confidence is at least ``tau`` is
   committed; when none clears ``tau`` the single most confident position is
   committed (lowest position among equals).

@@ -144,8 +144,9 @@ def test_small_models_semi_add(name, tau, tau_semi, tau_add):
         assert (tr.forwards == w.gen_len // w.n_inflight).all()
 
 
-def test_config2_multiblock_semi_add():
-    """Config 2 (3 blocks in flight) at acc 0.9 / semi 0.7 / add 0.1: the
+def test_multiblock_2048_semi_add():
+    """The multi-block workload (24 layers, d 2048, 3 blocks in flight) at
+    acc 0.9 / semi 0.7 / add 0.1: the
     whole batch on the GPU, the oracle replays sequence 5 for 16 steps."""
     run_parity(workload(2), 0.9, seq_ids=[5], max_steps=16, logit_steps=2, tau_semi=0.7, tau_add=0.1)
 
@@ -261,7 +262,7 @@ def test_small_models_fp8(name, tau):
     run_parity(SMALL[name], tau, wq="fp8")
 
 
-def test_config1_dense_fp8_full_size():
+def test_dense_1024_fp8_full_size():
     """Full-size dense model with fp8 layer weights at tau 0.9: the GPU
     decodes the batch, the oracle replays sequence 3."""
     run_parity(workload(1), 0.9, seq_ids=[3], logits=True, logit_steps=3, wq="fp8")
@@ -308,14 +309,14 @@ def test_fp8_model_errors():
     assert e.value.status == bd.BD_EINVAL
 
 
-def test_config0_tiny_f32():
+def test_tiny_256_f32():
     w = workload(0)
     for tau in w.taus:
         run_parity(w, tau)
 
 
 @pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
-def test_config1_dense_bf16_full_size(tau):
+def test_dense_1024_bf16_full_size(tau):
     """Full-size dense bf16 model (12 layers, d 1024, vocab 32768, batch 16,
     prompts 512, 256 generated tokens); the oracle replays 2 of the 16
     sequences (sequences are independent, so the subset is exact)."""
@@ -324,7 +325,7 @@ def test_config1_dense_bf16_full_size(tau):
 
 
 @pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
-def test_config2_multiblock_full_size(tau):
+def test_multiblock_2048_full_size(tau):
     """Full-size multi-block GQA model (24 layers, d 2048, 16/4 heads x 128,
     vocab 152064, batch 32, prompts 1024, 3 blocks in flight, 1024 generated
     tokens): the GPU decodes the whole batch; the oracle replays sequence 5
@@ -334,7 +335,7 @@ def test_config2_multiblock_full_size(tau):
     _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
 
 
-def test_config2_multiblock_static_skip_full_size():
+def test_multiblock_2048_static_skip_full_size():
     """Full-size multi-block model under the static skip rule at tau 0.9: the
     oracle (with the same rule) replays sequence 5 for 16 steps; the GPU's
     own trace must forward only the oldest active block (active
@@ -345,7 +346,7 @@ def test_config2_multiblock_static_skip_full_size():
     assert tr.stats["static_saved"] == tr.stats["static_deferred"] == 0 and tr.stats["skipped"] > 0
 
 
-def test_config3_long_prefix_full_size():
+def test_long_prefix_8192_full_size():
     """Full-size long-prefix model (prompts of 8192 tokens encoded by the
     prefill, block 64, 2 blocks in flight, batch 8) at tau 0.8: the oracle
     encodes one 8192-token prompt and replays sequence 3 for 8 steps."""
@@ -353,7 +354,7 @@ def test_config3_long_prefix_full_size():
 
 
 @pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
-def test_config4_moe_full_size(tau):
+def test_moe_2048_full_size(tau):
     """Full-size MoE model (20 layers, d 2048, 64 experts top-8 with FFN 512
     plus a shared expert, vocab 152064, batch 64, prompts 256, 128 generated
     tokens); the oracle replays sequence 17 for 12 steps."""
@@ -438,7 +439,7 @@ def test_error_paths():
     st.close()
 
 
-def test_config4_redline_sweep_matches_oracle():
+def test_moe_2048_redline_sweep_matches_oracle():
     """Redline on the GPU-decoded MoE sweep: 12 candidates (tau x in-flight
     blocks) plus the reference (tau > 1, one block) on one batch of 64
     calibration prompts; correctness = the final 16 tokens equal the
