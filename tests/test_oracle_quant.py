@@ -120,3 +120,117 @@ def test_fp8_weights_replace_exactly_the_layer_projections():
                 assert np.all(np.abs(b.reshape(rows.shape) - rows) <= bound)
             else:
                 assert b is a
+
+
+# ---------------------------------------------------------------- MXFP4
+E2M1_MAGNITUDES = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]   # the format's value set
+
+
+def test_e2m1_codes_are_the_format_values():
+    from oracle.quant import e2m1_value
+    v = e2m1_value(np.arange(16))
+    np.testing.assert_array_equal(v[:8], E2M1_MAGNITUDES)
+    np.testing.assert_array_equal(v[8:], [-m for m in E2M1_MAGNITUDES])
+
+
+def _nearest_code(x):
+    """Exhaustive search: the magnitude nearest |x| after saturation at 6,
+    the even code on a tie, then the sign bit."""
+    a = min(abs(x), 6.0)
+    d = [abs(a - m) for m in E2M1_MAGNITUDES]
+    best = min(d)
+    cands = [i for i, di in enumerate(d) if di == best]
+    code = cands[0] if len(cands) == 1 else next(i for i in cands if i % 2 == 0)
+    return code | (8 if x < 0 else 0)
+
+
+def test_e2m1_encode_matches_exhaustive_nearest_search():
+    from oracle.quant import e2m1_encode
+    grid = np.concatenate([np.arange(-9.0, 9.0, 0.03125), np.arange(-9.0, 9.0, 0.0137),
+                           np.random.default_rng(3).normal(0, 3, 4000), [0.25, 0.75, 1.25, 2.5, 3.5, 5.0, 7.0]])
+    got = e2m1_encode(grid)
+    want = np.array([_nearest_code(float(x)) for x in grid], dtype=np.uint8)
+    # the sign of zero is free: compare values where the result is zero
+    from oracle.quant import e2m1_value
+    zero = e2m1_value(want) == 0
+    np.testing.assert_array_equal(got[~zero], want[~zero])
+    assert np.all(e2m1_value(got[zero]) == 0)
+
+
+def test_mx_block_scale_and_saturation():
+    """The shared exponent puts the block maximum in [4, 8) (so it codes to
+    4, 6 or saturates to 6); an all-zero block takes the smallest scale."""
+    from oracle.quant import mx_block_exponent, quantize_mxfp4_rows, dequantize_mxfp4_rows, e2m1_value
+    rng = np.random.default_rng(4)
+    amax = np.abs(rng.normal(0, 1, 5000)) + 1e-12
+    e = mx_block_exponent(amax)
+    r = amax / np.ldexp(1.0, e)
+    assert np.all((r >= 4) & (r < 8))
+    assert mx_block_exponent(np.zeros(1))[0] == -127
+    w = rng.normal(0, 0.02, (16, 128))
+    w[3, 32:64] = 0.0
+    codes, exps = quantize_mxfp4_rows(w)
+    assert exps.shape == (16, 4) and exps[3, 1] == -127
+    dq = dequantize_mxfp4_rows(codes, exps)
+    scaled = np.abs(w.reshape(16, 4, 32)) / np.ldexp(1.0, exps)[:, :, None]
+    vals = np.abs(e2m1_value(codes)).reshape(16, 4, 32)
+    # within half a spacing of the scaled value, or saturated at 6
+    spacing = np.where(scaled >= 4, 2.0, np.where(scaled >= 2, 1.0, 0.5))
+    ok = (np.abs(vals - scaled) <= spacing / 2 + 1e-12) | ((scaled > 6) & (vals == 6))
+    assert np.all(ok)
+    assert np.all(np.abs(dq) <= 6 * np.ldexp(1.0, np.repeat(exps, 32, axis=1)))
+
+
+def test_mxfp4_weights_are_exact_bf16_and_touch_only_layer_projections():
+    from bd_synth import Workload, make_weights
+    from oracle.model import round_bf16
+    from oracle.quant import mxfp4_weights, quantized_layer_slots
+    w = Workload(name="mx", seed=5, n_layers=2, d_model=128, n_heads=2, n_kv_heads=1, head_dim=64,
+                 ffn_dim=256, vocab=256, dtype="bf16", batch=1, prompt_len=8, block_size=4, n_inflight=1,
+                 gen_len=8)
+    ws = make_weights(w)
+    q = mxfp4_weights(w, ws)
+    slots = set(quantized_layer_slots(w))
+    for i, (a, b) in enumerate(zip(ws, q)):
+        if i in slots:
+            assert b.dtype == np.float32
+            np.testing.assert_array_equal(round_bf16(b.astype(np.float64)), b.astype(np.float64))
+        else:
+            assert b is a
+
+
+def test_planted_mxfp4_mistakes_are_caught(monkeypatch):
+    """Ties away from zero, a scale one binade too large, and no saturation
+    are each caught by the pins above."""
+    import oracle.quant as oq
+    good_enc, good_exp = oq.e2m1_encode, oq.mx_block_exponent
+
+    def enc_ties_away(x):
+        x = np.asarray(x, dtype=np.float64)
+        a = np.abs(x)
+        _, ex = np.frexp(a)
+        qe = np.where(a >= 1.0, ex - 2, -1)
+        q = np.minimum(np.ldexp(np.floor(np.ldexp(a, -qe) + 0.5), qe), 6.0)
+        return good_enc(np.where(x < 0, -q, q))
+
+    def exp_one_up(amax):
+        return good_exp(amax) + 1
+
+    def enc_no_saturation(x):
+        x = np.asarray(x, dtype=np.float64)
+        if np.any(np.abs(x) > 6.5):
+            raise ValueError("out of range")
+        return good_enc(x)
+
+    checks = [test_e2m1_encode_matches_exhaustive_nearest_search, test_mx_block_scale_and_saturation]
+    for name, fn in (("e2m1_encode", enc_ties_away), ("mx_block_exponent", exp_one_up),
+                     ("e2m1_encode", enc_no_saturation)):
+        monkeypatch.setattr(oq, name, fn)
+        caught = False
+        for chk in checks:
+            try:
+                chk()
+            except (AssertionError, ValueError):
+                caught = True
+        monkeypatch.setattr(oq, name, good_enc if name == "e2m1_encode" else good_exp)
+        assert caught, f"planted mistake in {name} went unnoticed"
