@@ -160,19 +160,30 @@ def _draw(seed: int, t: int, shape) -> np.ndarray:
     return a
 
 
-def make_weights(w: Workload) -> List[np.ndarray]:
+def make_weights(w: Workload, threads: int | None = None) -> List[np.ndarray]:
     """Weights in ABI order.  "mat" tensors are float32 (f32 models) or uint16
-    bf16 bit patterns (bf16 models); "norm" and "router" tensors are float32."""
-    out = []
-    for t, (_, shape, kind) in enumerate(tensor_specs(w)):
+    bf16 bit patterns (bf16 models); "norm" and "router" tensors are float32.
+    Each tensor has its own seeded stream, so drawing them on a thread pool
+    (numpy's generators release the GIL while filling an array) gives the
+    same arrays as drawing them one after another."""
+    import concurrent.futures as cf
+    import os
+
+    def one(item):
+        t, (_, shape, kind) = item
         if kind == "norm":
-            out.append(np.ones(shape, dtype=np.float32))
-        elif kind == "router":
-            out.append(_draw(w.seed, t, shape))
-        else:
-            a = _draw(w.seed, t, shape)
-            out.append(a if w.dtype == "f32" else f32_to_bf16_bits(a))
-    return out
+            return np.ones(shape, dtype=np.float32)
+        a = _draw(w.seed, t, shape)
+        if kind == "router" or w.dtype == "f32":
+            return a
+        return f32_to_bf16_bits(a)
+
+    items = list(enumerate(tensor_specs(w)))
+    n = threads or min(16, len(os.sched_getaffinity(0)))
+    if n <= 1:
+        return [one(it) for it in items]
+    with cf.ThreadPoolExecutor(max_workers=n) as ex:
+        return list(ex.map(one, items))
 
 
 def make_prompts(w: Workload, n: int | None = None, offset: int = 0) -> np.ndarray:

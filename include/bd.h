@@ -264,6 +264,22 @@ enum {
 bd_status bd_profile(bd_model* model, int32_t enable);
 bd_status bd_profile_read(bd_model* model, double* ms_out, int32_t* count_out);
 
+/*
+ * bd_plan_projection -- the tile plan a bf16 projection C[M][N] = A . W^T of
+ *  depth K takes when a state holds rows_cap window rows (host-only query; no
+ *  device work).  resid != 0 asks for a projection added to the residual
+ *  stream (the O and dense down projections), which may split K into up to
+ *  zmax parts chosen on the device from the live row count; their partials
+ *  take ws_floats floats of the state's workspace at most (the largest extent
+ *  over every live row count in [1, rows_cap]; 0 when K is never split).
+ *  bd_prefill sizes the workspace with this extent, and the step refuses a
+ *  projection whose extent exceeds it.  Outputs may be NULL.
+ *  Errors: BD_EINVAL when N, K or rows_cap < 1; BD_EUNSUPPORTED when N or K
+ *  is not a multiple of 128.
+ */
+bd_status bd_plan_projection(int32_t N, int32_t K, int32_t rows_cap, int32_t resid, int32_t* bm_out,
+                             int32_t* bn_out, int32_t* zmax_out, int64_t* ws_floats_out);
+
 bd_status bd_state_free(bd_state* st);
 bd_status bd_model_free(bd_model* model);
 

@@ -102,7 +102,16 @@ class OracleModel:
         self.d, self.V = cfg.d_model, cfg.vocab
         self.mask_id = cfg.vocab - 1
         wdt = np.float64 if precision == "f64" else np.float32
-        ws = [_bits_to_float(np.asarray(t)).astype(wdt) for t in weights]
+
+        def widen(t):
+            return _bits_to_float(np.asarray(t)).astype(wdt)
+
+        # the conversions of large models take minutes one after another;
+        # numpy releases the GIL while casting, so a thread pool runs them at once
+        import concurrent.futures as cf
+        import os
+        with cf.ThreadPoolExecutor(max_workers=min(16, len(os.sched_getaffinity(0)))) as ex:
+            ws = list(ex.map(widen, weights))
         it = iter(ws)
         self.embed = next(it)
         self.layers = []
@@ -135,10 +144,13 @@ class OracleModel:
         return split_bf16x2(x) if self.precision == "bf16" else x
 
     def _mm(self, a: np.ndarray, w: np.ndarray) -> np.ndarray:
-        """a @ w.T for a [rows][in] and a weight stored [out][in]."""
+        """a @ w.T for a [rows][in] and a weight stored [out][in], evaluated
+        as (w @ a.T).T: the same dot products, with the weight as the left
+        operand, the orientation in which BLAS runs these few-row products
+        fastest."""
         if self.precision == "f64":
-            return a @ w.T
-        return (a.astype(np.float32) @ w.T).astype(np.float64)
+            return (w @ a.T).T
+        return (w @ a.astype(np.float32).T).T.astype(np.float64)
 
     def kv_cache(self, max_pos: int) -> KVCache:
         dt = np.float64 if self.precision == "f64" else np.float32

@@ -20,7 +20,7 @@ BD_F32, BD_BF16 = 0, 1
 
 EXPORTED = ["bd_init_model", "bd_quantize_fp8", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
             "bd_decode", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
-            "bd_profile_read", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select",
+            "bd_profile_read", "bd_plan_projection", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select",
             "rl_select", "rl_alpha_sweep", "rl_split_exceedance", "rl_monte_carlo"]
 RL_METHODS = {"holm": 0, "bonferroni": 1, "fixed_sequence": 2, "uncorrected": 3, "plugin": 4}
 PROF_KINDS = ["embed", "norm", "gemm_qkv", "rope", "attn", "gemm_o", "gemm_gu", "gemm_down", "lm_head",
@@ -83,6 +83,7 @@ def _load():
         "bd_state_stats": [VP, VP, P(ctypes.c_int64), I32],
         "bd_profile": [VP, I32],
         "bd_profile_read": [VP, P(ctypes.c_double), P(I32)],
+        "bd_plan_projection": [I32, I32, I32, I32, P(I32), P(I32), P(I32), P(ctypes.c_int64)],
         "bd_state_free": [VP],
         "bd_model_free": [VP],
         "rl_risk_select": [I32, I32, I32, P(ctypes.c_uint8), P(ctypes.c_double), ctypes.c_double,
@@ -201,6 +202,15 @@ def bd_profile_read(model: int):
     n = (ctypes.c_int32 * len(PROF_KINDS))()
     _check(lib.bd_profile_read(model, ms, n))
     return {k: (ms[i], n[i]) for i, k in enumerate(PROF_KINDS)}
+
+
+def bd_plan_projection(N: int, K: int, rows_cap: int, resid: bool):
+    """Tile plan of a bf16 projection: (bm, bn, zmax, workspace floats)."""
+    bm, bn, zm = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    wsf = ctypes.c_int64()
+    _check(lib.bd_plan_projection(N, K, rows_cap, 1 if resid else 0, ctypes.byref(bm), ctypes.byref(bn),
+                                  ctypes.byref(zm), ctypes.byref(wsf)))
+    return bm.value, bn.value, zm.value, wsf.value
 
 
 def bd_state_free(state: int):

@@ -129,7 +129,8 @@ struct bd_state {
   void* Qb;
   void* Ob;
   void* Hact;
-  float* resid_ws;         // residual split-K partials (RESID_WS_FLOATS, bf16 models)
+  float* resid_ws;         // residual split-K partials (bf16 models)
+  size_t resid_ws_floats;
   void* Alm;
   float *pmax, *psum;
   int32_t* parg;
@@ -499,7 +500,8 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
                                           s->Ob, s->pl_O, plan, s->b, win_cap, H, Hkv, hd, s->B,
                                           kv_splits, s->attn_ws_o, s->attn_ws_ml, rows_cap, st));
     LAUNCH(BD_PROF_GEMM_O, launch_gemm_resid(bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d, H * hd,
-                                             plan.hdr, rows_cap, s->X, d, s->resid_ws, &pend, st, L.s_o));
+                                             plan.hdr, rows_cap, s->X, d, s->resid_ws, s->resid_ws_floats, &pend, st,
+                                             L.s_o));
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
                                         rows_cap, s->A, s->pl_A, pend, st));
     pend.ws = nullptr;
@@ -507,7 +509,7 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
       LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, s->pl_A, L.w_gu, d, 2 * F, d,
                                           plan.hdr, rows_cap, s->Hact, F, s->pl_H, st, L.s_gu));
       LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm_resid(bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
-                                                  plan.hdr, rows_cap, s->X, d, s->resid_ws, &pend,
+                                                  plan.hdr, rows_cap, s->X, d, s->resid_ws, s->resid_ws_floats, &pend,
                                                   st, L.s_down));
     } else {
       bd_status r = run_moe(m, s, L, plan, rows_cap);
@@ -541,6 +543,49 @@ static int min_resolved(float thr, int B) {
   for (int r = 0; r <= B; ++r)
     if ((float)r / (float)B >= thr) return r;
   return B + 1;
+}
+
+// Floats of residual split partials the O and down projections of a bf16
+// model may write over rows_cap rows (the largest of the two extents; they
+// never hold partials at the same time: the RMSNorm between them folds them).
+static ResidSplit resid_split_of(int N, int K, int rows_cap) {
+  const GemmPlan p = plan_resid(N, K, rows_cap);
+  ResidSplit r{};
+  r.nx = N / p.bn;
+  r.bm = p.bm;
+  r.K = K;
+  r.zmax = p.zmax;
+  return r;
+}
+
+static size_t resid_ws_need(const bd_model_cfg& c, int rows_cap) {
+  const int d = c.d_model;
+  size_t need = resid_extent_max(rows_cap, d, resid_split_of(d, c.n_heads * c.head_dim, rows_cap));
+  if (c.n_experts == 0) {
+    const size_t dn = resid_extent_max(rows_cap, d, resid_split_of(d, c.ffn_dim, rows_cap));
+    if (dn > need) need = dn;
+  }
+  return need;
+}
+
+extern "C" bd_status bd_plan_projection(int32_t N, int32_t K, int32_t rows_cap, int32_t resid,
+                                        int32_t* bm_out, int32_t* bn_out, int32_t* zmax_out,
+                                        int64_t* ws_floats_out) {
+  if (N < 1 || K < 1 || rows_cap < 1) return fail(BD_EINVAL, "need N, K, rows_cap >= 1");
+  if (N % 128 || K % KALIGN) return fail(BD_EUNSUPPORTED, "N and K must be multiples of 128");
+  GemmPlan p;
+  int64_t wsf = 0;
+  if (resid) {
+    p = plan_resid(N, K, rows_cap);
+    wsf = (int64_t)resid_extent_max(rows_cap, N, resid_split_of(N, K, rows_cap));
+  } else {
+    p = plan_gemm(true, N, K, rows_cap);
+  }
+  if (bm_out) *bm_out = p.bm;
+  if (bn_out) *bn_out = p.bn;
+  if (zmax_out) *zmax_out = p.zmax;
+  if (ws_floats_out) *ws_floats_out = wsf;
+  return BD_OK;
 }
 
 extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
@@ -625,7 +670,14 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
       return fail(BD_EHIP, "rope table: %s", hipGetErrorString(er));
     }
   }
-  if (m->bf16) ALLOC(s->resid_ws, RESID_WS_FLOATS * sizeof(float));
+  if (m->bf16) {
+    s->resid_ws_floats = resid_ws_need(c, s->rows_step);
+    const size_t pre = resid_ws_need(c, s->rows_pre);
+    if (pre > s->resid_ws_floats) s->resid_ws_floats = pre;
+    // a small workspace even when K is never split keeps the residual tile plan
+    if (s->resid_ws_floats < 64) s->resid_ws_floats = 64;
+    ALLOC(s->resid_ws, s->resid_ws_floats * sizeof(float));
+  }
   if (c.n_experts > 0) {
     const int E = c.n_experts, k = c.top_k, Fe = c.expert_ffn;
     const size_t assign_cap = (size_t)s->rows_cap * k + GROUP_BM;   // + one tile of padding rows

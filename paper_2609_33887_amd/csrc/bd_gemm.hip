@@ -803,27 +803,52 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
-                             int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
-                             int ldx, float* ws, ResidSplit* fold, hipStream_t st, const float* wscale) {
-  fold->ws = nullptr;
-  if (!is_bf16 || !ws)
-    return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st,
-                       wscale);
+size_t resid_extent(int M, int N, const ResidSplit& r) {
+  if (M < 1) return 0;
+  const int S = resid_splits(M, r);
+  return S > 1 ? (size_t)S * (size_t)cdiv(M, r.bm) * r.bm * N : 0;
+}
+
+size_t resid_extent_max(int rows_cap, int N, const ResidSplit& r) {
+  // S and the slab height depend on M only through its row-tile count
+  size_t mx = 0;
+  for (int y = 1; y <= cdiv(rows_cap, r.bm); ++y) {
+    const size_t e = resid_extent(y * r.bm < rows_cap ? y * r.bm : rows_cap, N, r);
+    if (e > mx) mx = e;
+  }
+  return mx;
+}
+
+GemmPlan plan_resid(int N, int K, int rows_cap) {
   // deep products (K >= 4096) take 128x128 tiles: with K split, their A and
   // W re-reads halve against 64x64 at the same parallelism
   GemmPlan p = plan_gemm(true, N, K, rows_cap, true);
   if (K >= 4096 && N % 128 == 0) p = GemmPlan{128, 128, 1};
   p.zmax = 8;
+  return p;
+}
+
+hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
+                             int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
+                             int ldx, float* ws, size_t ws_floats, ResidSplit* fold, hipStream_t st,
+                             const float* wscale) {
+  fold->ws = nullptr;
+  if (!is_bf16 || !ws)
+    return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st,
+                       wscale);
+  const GemmPlan p = plan_resid(N, K, rows_cap);
+  ResidSplit r{};
+  r.nx = N / p.bn;
+  r.bm = p.bm;
+  r.K = K;
+  r.zmax = p.zmax;
+  if (resid_extent_max(rows_cap, N, r) > ws_floats) return hipErrorInvalidValue;
   hipError_t e = launch_gemm_planned(p, EPI_ADD_F32, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap,
                                      X, ldx, 0, ws, st, wscale);
   if (e != hipSuccess) return e;
-  fold->ws = ws;
-  fold->Mp = M_dev;
-  fold->nx = N / p.bn;
-  fold->bm = p.bm;
-  fold->K = K;
-  fold->zmax = p.zmax;
+  r.ws = ws;
+  r.Mp = M_dev;
+  *fold = r;
   return hipSuccess;
 }
 

@@ -80,9 +80,7 @@ struct ResidSplit {
 };
 constexpr int RESID_TARGET_128 = 256;   // workgroups aimed at with 128-row tiles
 constexpr int RESID_TARGET_64 = 512;    // ... with 64-row tiles
-// S > 1 only when tiles * S <= target, so partials fit target * 128 * 128 floats
-constexpr size_t RESID_WS_FLOATS = (size_t)RESID_TARGET_128 * 128 * 128;
-__device__ __forceinline__ int resid_splits(int M, const ResidSplit& r) {
+__host__ __device__ __forceinline__ int resid_splits(int M, const ResidSplit& r) {
   const int tiles = r.nx * ((M + r.bm - 1) / r.bm);
   const int target = r.bm == 128 ? RESID_TARGET_128 : RESID_TARGET_64;
   int S = 1;
@@ -91,6 +89,13 @@ __device__ __forceinline__ int resid_splits(int M, const ResidSplit& r) {
     S *= 2;
   return S;
 }
+// Floats of split partials a residual projection of N columns writes for M
+// live rows: S(M) whole row-tile slabs of N columns, or 0 when S(M) = 1
+// (the add is then done in place).
+size_t resid_extent(int M, int N, const ResidSplit& r);
+// Largest resid_extent over every live row count M in [1, rows_cap]: the
+// workspace a state must hold for that projection.
+size_t resid_extent_max(int rows_cap, int N, const ResidSplit& r);
 
 // ---- launchers (defined in the .hip files) ---------------------------------
 // C[M][N] (+)= A[M][K] . W[N][K]^T with M read from *M_dev; grid covers rows_cap.
@@ -154,13 +159,18 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
                                int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
                                hipStream_t st, const float* wscale = nullptr);
-// X[M][N] += A . W^T for the residual stream.  bf16 with ws (RESID_WS_FLOATS
-// floats): the kernel may split K (see ResidSplit) and *fold describes the
-// pending partials, which the next launch_rmsnorm of X must be given; else
-// the add is done in place and fold->ws is NULL.
+// Plan of a residual projection (O and down of bf16 models): tile shape and
+// the largest K-split (zmax).
+GemmPlan plan_resid(int N, int K, int rows_cap);
+// X[M][N] += A . W^T for the residual stream.  bf16 with a workspace ws of
+// ws_floats floats: the kernel may split K (see ResidSplit) and *fold
+// describes the pending partials, which the next launch_rmsnorm of X must be
+// given; else the add is done in place and fold->ws is NULL.  Returns
+// hipErrorInvalidValue, launching nothing, when ws_floats is smaller than
+// resid_extent_max of the plan (the partials would not fit).
 hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                              int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
-                             int ldx, float* ws, ResidSplit* fold, hipStream_t st,
+                             int ldx, float* ws, size_t ws_floats, ResidSplit* fold, hipStream_t st,
                              const float* wscale = nullptr);
 
 // LM head: per-row softmax statistics over the vocabulary of

@@ -38,7 +38,10 @@ class GpuTrace:
 
 
 def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=None, logit_steps=None,
-                      progress=None, tau_semi=None, tau_add=0.0, skip_masked=False):
+                      progress=None, tau_semi=None, tau_add=0.0, skip_masked=False, logit_every=1):
+    """Decode the batch step by step; logits of the sequences in
+    ``logits_for`` are kept on every ``logit_every``-th step (and only on the
+    first ``logit_steps`` steps when that is given)."""
     import torch
     from paper_2609_33887_amd import bd
     st = bd.State(model, prompts, G, tau, nb, B, tau_semi, tau_add, skip_masked)
@@ -53,7 +56,8 @@ def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=No
     for s in range(limit):
         conf.fill_(-1.0)
         tok.fill_(-1)
-        want_logits = logits is not None and (logit_steps is None or s < logit_steps)
+        want_logits = (logits is not None and (logit_steps is None or s < logit_steps)
+                       and s % logit_every == 0)
         st.step(conf, tok, logits if want_logits else None)
         done = st.commit(want_done=True)
         c = conf.cpu().numpy()
@@ -91,19 +95,44 @@ class Report:
     complete: bool = True            # every replayed sequence ran to its end
 
 
+def prefilled(oracle_model, prompt, G, B, nb, tau, tau_semi=None, tau_add=0.0, skip_masked=False,
+              cache=None, key=None):
+    """An oracle decoder of one sequence after its prefill.  The prefill (the
+    prompt's forward) depends only on the prompt and the block grid, so with
+    a ``cache`` dict the prefilled KV cache is kept under ``key`` and copied
+    into later decoders of the same prompt and block size, whatever their
+    thresholds and in-flight count."""
+    import copy
+    from oracle.decode import SeqDecoder
+    d = SeqDecoder(oracle_model, prompt, G, B, nb, tau, tau_semi, tau_add, skip_masked)
+    if cache is None or key is None:
+        d.prefill()
+        return d
+    if key not in cache:
+        d.prefill()
+        cache[key] = (copy.deepcopy(d.cache), d.cache_len)
+        return d
+    kv, clen = cache[key]
+    d.cache = copy.deepcopy(kv)
+    d.cache_len = clen
+    d._admit()
+    return d
+
+
 def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, conf_tol, logit_tol,
-             max_steps=None, progress=None, tau_semi=None, tau_add=0.0, skip_masked=False):
+             max_steps=None, progress=None, tau_semi=None, tau_add=0.0, skip_masked=False,
+             prefill_cache=None, cache_tag=None):
     """Replay the chosen sequences in the oracle against ``trace`` (the first
     ``max_steps`` steps of each when given)."""
-    from oracle.decode import SeqDecoder, PART_NAMES
+    from oracle.decode import PART_NAMES
     rep = Report()
     part = np.zeros(len(PART_NAMES), dtype=np.int64)
     tau32 = float(np.float32(tau))
     for i in seq_ids:
-        d = SeqDecoder(oracle_model, prompts[i], G, B, nb, tau, tau_semi, tau_add, skip_masked)
         if progress:
             progress(f"  oracle prefill of sequence {i}")
-        d.prefill()
+        d = prefilled(oracle_model, prompts[i], G, B, nb, tau, tau_semi, tau_add, skip_masked,
+                      prefill_cache, None if cache_tag is None else (cache_tag, i, B))
         P = d.P
         step = 0
         while not d.done and (max_steps is None or step < max_steps):

@@ -1,5 +1,12 @@
 """GPU parity of the HIP path against the oracle, through the C ABI.
 
+Oracles: the plain definition ("f64": every operand and operation in
+float64 on the same bf16 weights -- the block-causal forward of §2.1 and the
+mask-suppressed softmax of App. B.1 with no storage rounding at all) is the
+reference of every test; the bf16-storage model ("bf16": the same forward
+with each stored activation rounded to a bf16 high/low pair) is replayed as
+well on the small models and on the dense workload, to report both.
+
 Tolerances (stated numerically): bf16 models -- logits max-abs <= 3e-2,
 confidence <= 5e-3; fp32 models -- confidence <= 1e-4, logits <= 1e-3.
 Committed tokens, commit steps and forwards must be identical except at
@@ -8,6 +15,7 @@ probability gap <= 1e-3, or best-two confidences within 1e-3 for a forced
 commit), which are counted and printed.
 """
 import sys
+import time
 
 import numpy as np
 import pytest
@@ -48,6 +56,15 @@ SMALL = {
                      prompt_len=8, block_size=8, n_inflight=2, gen_len=48),
     "block1": small("block1", seed=93, batch=2, prompt_len=5, block_size=1, n_inflight=1, gen_len=12,
                     dtype="f32"),
+    # bf16 at block size 1 (one block in flight: ordinary causal decoding,
+    # and the V cache stored row by row) and at block size 2
+    "bf16_block1": small("bf16_block1", seed=100, batch=3, prompt_len=7, block_size=1, n_inflight=1,
+                         gen_len=24),
+    "bf16_block2": small("bf16_block2", seed=101, batch=2, prompt_len=10, block_size=2, n_inflight=2,
+                         gen_len=32),
+    # GQA at head_dim 64: four q-heads per kv head
+    "gqa64": small("gqa64", seed=102, n_heads=8, n_kv_heads=2, head_dim=64, batch=3, prompt_len=64,
+                   block_size=16, n_inflight=2, gen_len=64),
     # MoE: 8 experts, top-2, expert FFN 128, one shared expert
     "moe": small("moe", seed=96, n_heads=4, n_kv_heads=2, head_dim=128, ffn_dim=0, n_experts=8, top_k=2,
                  expert_ffn=128, n_shared=1, batch=3, prompt_len=64, block_size=16, n_inflight=2,
@@ -62,6 +79,8 @@ SMALL = {
 }
 
 _models = {}
+_oracles = {}
+_prefills = {}
 
 
 def get_model(w, wq=None):
@@ -70,6 +89,14 @@ def get_model(w, wq=None):
     from paper_2609_33887_amd import bd
     key = (w.name, w.seed, wq)
     if key not in _models:
+        if w.d_model >= 2048:
+            # one large workload at a time in host and device memory
+            for k in [k for k in _models if k[0] != w.name]:
+                _models.pop(k)[0].close()
+            for k in [k for k in _oracles if k[0] != w.name]:
+                del _oracles[k]
+            for k in [k for k in _prefills if k[0][0] != w.name]:
+                del _prefills[k]
         ws = make_weights(w)
         model = bd.Model(w, ws, wq=wq)
         if wq == "fp8":
@@ -79,41 +106,63 @@ def get_model(w, wq=None):
     return _models[key]
 
 
-def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None, tau_semi=None,
-               tau_add=0.0, skip_masked=False, wq=None):
+def get_oracle(w, mode, wq=None):
     from oracle.model import OracleModel
+    key = (w.name, w.seed, wq, mode)
+    if key not in _oracles:
+        _oracles[key] = OracleModel(w, get_model(w, wq)[1], mode)
+    return _oracles[key]
+
+
+def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=None, tau_semi=None,
+               tau_add=0.0, skip_masked=False, wq=None, modes=None, logit_every=1, n_inflight=None):
+    """GPU decode of the whole batch, then oracle replays of ``seq_ids`` (all
+    sequences by default) in each precision mode of ``modes`` (default: the
+    plain float64 definition)."""
     from tests.gpu_harness import capture_gpu_trace, lockstep
     _need_gpu()
+    nb = w.n_inflight if n_inflight is None else n_inflight
+    modes = modes or ("f64",)
     _say(f"[parity] {w.name} tau={tau} b={w.batch} P={w.prompt_len} G={w.gen_len} B={w.block_size} "
-         f"nb={w.n_inflight} tau_semi={tau_semi} tau_add={tau_add} skip={skip_masked} wq={wq}")
+         f"nb={nb} tau_semi={tau_semi} tau_add={tau_add} skip={skip_masked} wq={wq} oracle={modes}")
+    t0 = time.perf_counter()
     model, ws = get_model(w, wq)
     prompts = make_prompts(w)
     ids = list(range(w.batch)) if seq_ids is None else list(seq_ids)
-    tr = capture_gpu_trace(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size,
+    tr = capture_gpu_trace(model, prompts, w.gen_len, tau, nb, w.block_size,
                            logits_for=set(ids) if logits else (), logit_steps=logit_steps, progress=_say,
-                           tau_semi=tau_semi, tau_add=tau_add, skip_masked=skip_masked)
-    om = OracleModel(w, ws, "f64" if w.dtype == "f32" else "bf16")
-    rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, w.n_inflight, w.block_size, *TOL[w.dtype],
-                   max_steps=max_steps, progress=_say, tau_semi=tau_semi, tau_add=tau_add,
-                   skip_masked=skip_masked)
+                           tau_semi=tau_semi, tau_add=tau_add, skip_masked=skip_masked,
+                           logit_every=logit_every)
+    t1 = time.perf_counter()
     ctol, ltol = TOL[w.dtype]
-    _say(f"  positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} max|dlogit|={rep.max_logit_diff:.3g} "
-         f"near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} T4(steps)={rep.t4} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
-    assert not rep.failures, rep.failures[:5]
-    assert rep.max_conf_diff <= ctol
-    assert rep.max_logit_diff <= ltol
-    if rep.complete and len(ids) == w.batch:
-        # participation counters (App. B.3): bit-exact
-        gp = {k: tr.stats[k] for k in rep.participation}
-        _say(f"  participation GPU {gp}")
-        assert gp == rep.participation, (gp, rep.participation)
-    return tr, rep
+    reps = {}
+    for mode in modes:
+        om = get_oracle(w, "f64" if w.dtype == "f32" else mode, wq)
+        rep = lockstep(om, prompts, ids, tr, w.gen_len, tau, nb, w.block_size, ctol, ltol,
+                       max_steps=max_steps, progress=_say, tau_semi=tau_semi, tau_add=tau_add,
+                       skip_masked=skip_masked, prefill_cache=_prefills, cache_tag=(w.name, w.seed, wq, mode))
+        _say(f"  oracle {mode}: positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} "
+             f"max|dlogit|={rep.max_logit_diff:.3g} near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} "
+             f"T4(steps)={rep.t4} complete={rep.complete} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
+        assert not rep.failures, rep.failures[:5]
+        assert rep.max_conf_diff <= ctol
+        assert rep.max_logit_diff <= ltol
+        if rep.complete and len(ids) == w.batch:
+            # participation counters (App. B.3): bit-exact
+            gp = {k: tr.stats[k] for k in rep.participation}
+            _say(f"  participation GPU {gp}")
+            assert gp == rep.participation, (gp, rep.participation)
+        reps[mode] = rep
+    _say(f"  wall: GPU decode {t1 - t0:.1f} s, oracle replays {time.perf_counter() - t1:.1f} s")
+    return tr, reps[modes[0]]
 
 
 @pytest.mark.parametrize("name", list(SMALL))
 @pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
 def test_small_models(name, tau):
-    run_parity(SMALL[name], tau)
+    """Every small model at four thresholds against the plain float64
+    definition and (bf16 models) the bf16-storage model."""
+    run_parity(SMALL[name], tau, modes=("f64", "bf16") if SMALL[name].dtype == "bf16" else ("f64",))
 
 
 @pytest.mark.parametrize("tau", [0.0, 2.0])
@@ -265,7 +314,7 @@ def test_small_models_fp8(name, tau):
 def test_dense_1024_fp8_full_size():
     """Full-size dense model with fp8 layer weights at tau 0.9: the GPU
     decodes the batch, the oracle replays sequence 3."""
-    run_parity(workload(1), 0.9, seq_ids=[3], logits=True, logit_steps=3, wq="fp8")
+    run_parity(workload(1), 0.9, seq_ids=[3], logits=True, logit_every=8, wq="fp8")
 
 
 def test_precision_sweep_matches_oracle():
@@ -318,20 +367,35 @@ def test_tiny_256_f32():
 @pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
 def test_dense_1024_bf16_full_size(tau):
     """Full-size dense bf16 model (12 layers, d 1024, vocab 32768, batch 16,
-    prompts 512, 256 generated tokens); the oracle replays 2 of the 16
-    sequences (sequences are independent, so the subset is exact)."""
+    prompts 512, 256 generated tokens): the GPU decodes the batch; the plain
+    float64 oracle replays 2 of the 16 sequences to their end (sequences are
+    independent, so the subset is exact), logits compared on every 8th step;
+    at tau 0.9 the bf16-storage model replays them as well."""
     w = workload(1)
-    run_parity(w, tau, seq_ids=[0, 11], logits=True)
+    tr, rep = run_parity(w, tau, seq_ids=[0, 11], logit_every=8,
+                         modes=("f64", "bf16") if tau == 0.9 else ("f64",))
+    assert rep.complete
 
 
-@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
-def test_multiblock_2048_full_size(tau):
+def test_multiblock_2048_whole_trace():
     """Full-size multi-block GQA model (24 layers, d 2048, 16/4 heads x 128,
     vocab 152064, batch 32, prompts 1024, 3 blocks in flight, 1024 generated
-    tokens): the GPU decodes the whole batch; the oracle replays sequence 5
-    for its first 16 steps (logits compared on the first 3)."""
+    tokens) at tau 0.9: the GPU decodes the whole batch; the float64 oracle
+    replays sequence 5 to its end, logits on every 8th step."""
     w = workload(2)
-    tr, _ = run_parity(w, tau, seq_ids=[5], max_steps=16, logit_steps=3)
+    tr, rep = run_parity(w, 0.9, seq_ids=[5], logit_every=8)
+    assert rep.complete
+    _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.8, 0.7])
+def test_multiblock_2048_full_size(tau):
+    """The multi-block workload at the other thresholds: the oracle replays
+    sequence 5 for its first 16 steps (logits on steps 0 and 8); at tau 0.7
+    the bf16-storage model replays it too."""
+    w = workload(2)
+    tr, _ = run_parity(w, tau, seq_ids=[5], max_steps=16, logit_every=8,
+                       modes=("f64", "bf16") if tau == 0.7 else ("f64",))
     _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
 
 
@@ -346,20 +410,37 @@ def test_multiblock_2048_static_skip_full_size():
     assert tr.stats["static_saved"] == tr.stats["static_deferred"] == 0 and tr.stats["skipped"] > 0
 
 
-def test_long_prefix_8192_full_size():
+@pytest.mark.parametrize("tau", [0.8, 0.95, 0.9, 0.7])
+def test_long_prefix_8192_full_size(tau):
     """Full-size long-prefix model (prompts of 8192 tokens encoded by the
-    prefill, block 64, 2 blocks in flight, batch 8) at tau 0.8: the oracle
-    encodes one 8192-token prompt and replays sequence 3 for 8 steps."""
-    run_parity(workload(3), 0.8, seq_ids=[3], max_steps=8, logit_steps=2)
+    prefill, block 64, 2 blocks in flight, batch 8): the oracle encodes the
+    8192-token prompt of sequence 3 once and replays it -- to its end at
+    tau 0.8 (logits on every 8th step), for 8 steps at the other thresholds."""
+    w = workload(3)
+    whole = tau == 0.8
+    tr, rep = run_parity(w, tau, seq_ids=[3], max_steps=None if whole else 8, logit_every=8)
+    assert rep.complete or not whole
 
 
-@pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
-def test_moe_2048_full_size(tau):
+@pytest.mark.parametrize("nb", [1, 3])
+def test_moe_2048_whole_trace(nb):
     """Full-size MoE model (20 layers, d 2048, 64 experts top-8 with FFN 512
     plus a shared expert, vocab 152064, batch 64, prompts 256, 128 generated
-    tokens); the oracle replays sequence 17 for 12 steps."""
+    tokens) at tau 0.9 with 1 and 3 blocks in flight (two of the sweep's
+    candidates): the oracle replays sequence 17 to its end, logits on every
+    8th step."""
     w = workload(4)
-    tr, _ = run_parity(w, tau, seq_ids=[17], max_steps=12, logit_steps=2)
+    tr, rep = run_parity(w, 0.9, seq_ids=[17], logit_every=8, n_inflight=nb)
+    assert rep.complete
+    _check_participation_identities(tr, nb, w.gen_len, w.block_size)
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.8, 0.7])
+def test_moe_2048_full_size(tau):
+    """The MoE workload at the other thresholds (one block in flight): the
+    oracle replays sequence 17 for 12 steps."""
+    w = workload(4)
+    tr, _ = run_parity(w, tau, seq_ids=[17], max_steps=12, logit_every=8)
     _check_participation_identities(tr, w.n_inflight, w.gen_len, w.block_size)
 
 
