@@ -170,26 +170,33 @@ class OracleModel:
                   B: int) -> np.ndarray:
         """Block-causal attention (§2.1).  q: [W][H][hd] at positions qpos;
         K, V: [e][Hkv][hd] for keys at positions 0..e-1.  Query at p attends to
-        key j iff j // B <= p // B.  GQA: q-head h reads kv-head h // (H/Hkv)."""
-        e = K.shape[0]
-        kpos = np.arange(e)
+        key j iff j // B <= p // B, i.e. to the keys [0, (p // B + 1) B): every
+        query of one block sees the same keys, so each block's queries are
+        taken together over exactly those keys.  GQA: q-head h reads kv-head
+        h // (H/Hkv).  Scores, softmax (max, exponentials, normalisation) and
+        the weighted sum of values in float64; the element-wise steps run as
+        torch CPU operations, which use every host core."""
+        import torch
         group = self.H // self.Hkv
-        out = np.empty(q.shape, dtype=np.float64)
         scale = 1.0 / math.sqrt(self.hd)
-        Kd = K.astype(np.float64)
-        Vd = V.astype(np.float64)
-        # query rows are independent; chunks of rows only bound the memory of
-        # the score matrix
-        for r0 in range(0, q.shape[0], 1024):
-            r1 = min(q.shape[0], r0 + 1024)
-            kend = int((qpos[r1 - 1] // B + 1) * B)                   # keys any row here sees
-            visible = (kpos[None, :kend] // B) <= (qpos[r0:r1, None] // B)
-            for h in range(self.H):
-                kv = h // group
-                s = (q[r0:r1, h, :] @ Kd[:kend, kv, :].T) * scale
-                s = np.where(visible, s, -np.inf)
-                out[r0:r1, h, :] = _softmax_rows(s) @ Vd[:kend, kv, :]
-        return out
+        qd = torch.from_numpy(np.ascontiguousarray(q, dtype=np.float64))
+        Kd = torch.from_numpy(np.ascontiguousarray(K, dtype=np.float64))
+        Vd = torch.from_numpy(np.ascontiguousarray(V, dtype=np.float64))
+        out = torch.empty_like(qd)
+        blk = np.asarray(qpos) // B
+        for b in np.unique(blk):
+            rows = np.nonzero(blk == b)[0]
+            r0, r1 = int(rows[0]), int(rows[-1]) + 1
+            assert r1 - r0 == rows.size, "a block's queries are consecutive window rows"
+            kend = int((b + 1) * B)
+            for kv in range(self.Hkv):
+                hs = slice(kv * group, (kv + 1) * group)
+                qb = qd[r0:r1, hs, :].reshape(-1, self.hd)             # [rows * group][hd]
+                sc = (qb @ Kd[:kend, kv, :].T) * scale                  # [rows * group][kend]
+                e = torch.exp(sc - torch.amax(sc, dim=-1, keepdim=True))
+                p = e / torch.sum(e, dim=-1, keepdim=True)
+                out[r0:r1, hs, :] = (p @ Vd[:kend, kv, :]).reshape(r1 - r0, group, self.hd)
+        return out.numpy()
 
     def dense_ffn(self, a: np.ndarray, L) -> np.ndarray:
         act = self._operand(_silu(self._mm(a, L["w_gate"])) * self._mm(a, L["w_up"]))

@@ -31,8 +31,8 @@ def _need_gpu():
 
 
 def _say(*a):
-    print(*a, flush=True)
-    sys.stdout.flush()
+    from tests.conftest import progress
+    progress(" ".join(str(x) for x in a))
 
 
 from bd_synth import workload, make_weights, make_prompts, Workload   # noqa: E402
