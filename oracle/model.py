@@ -71,6 +71,20 @@ def _silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
+def _block_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float, use_torch: bool) -> np.ndarray:
+    """softmax(scale * q @ k.T) @ v per row, in float64: the scores, their row
+    maximum, exp(s - max), the sum, the normalised weights and the weighted
+    sum of v -- as numpy operations, or as torch CPU operations (which use
+    every host core) when ``use_torch``."""
+    if not use_torch:
+        return _softmax_rows((q @ k.T) * scale) @ v
+    import torch
+    s = (torch.from_numpy(q) @ torch.from_numpy(k).T) * scale
+    e = torch.exp(s - torch.amax(s, dim=-1, keepdim=True))
+    p = e / torch.sum(e, dim=-1, keepdim=True)
+    return (p @ torch.from_numpy(v)).numpy()
+
+
 def _softmax_rows(s: np.ndarray) -> np.ndarray:
     m = np.max(s, axis=-1, keepdims=True)
     e = np.exp(s - m)
@@ -174,16 +188,17 @@ class OracleModel:
         query of one block sees the same keys, so each block's queries are
         taken together over exactly those keys.  GQA: q-head h reads kv-head
         h // (H/Hkv).  Scores, softmax (max, exponentials, normalisation) and
-        the weighted sum of values in float64; the element-wise steps run as
-        torch CPU operations, which use every host core."""
-        import torch
+        the weighted sum of values in float64."""
         group = self.H // self.Hkv
         scale = 1.0 / math.sqrt(self.hd)
-        qd = torch.from_numpy(np.ascontiguousarray(q, dtype=np.float64))
-        Kd = torch.from_numpy(np.ascontiguousarray(K, dtype=np.float64))
-        Vd = torch.from_numpy(np.ascontiguousarray(V, dtype=np.float64))
-        out = torch.empty_like(qd)
+        Kd = np.ascontiguousarray(K, dtype=np.float64)
+        Vd = np.ascontiguousarray(V, dtype=np.float64)
+        out = np.empty(q.shape, dtype=np.float64)
         blk = np.asarray(qpos) // B
+        # long prefixes: torch's thread pool for the whole call (switching
+        # between it and numpy's BLAS threads per block costs more than small
+        # blocks gain from it)
+        use_torch = q.shape[0] * self.H * K.shape[0] >= (1 << 24)
         for b in np.unique(blk):
             rows = np.nonzero(blk == b)[0]
             r0, r1 = int(rows[0]), int(rows[-1]) + 1
@@ -191,12 +206,10 @@ class OracleModel:
             kend = int((b + 1) * B)
             for kv in range(self.Hkv):
                 hs = slice(kv * group, (kv + 1) * group)
-                qb = qd[r0:r1, hs, :].reshape(-1, self.hd)             # [rows * group][hd]
-                sc = (qb @ Kd[:kend, kv, :].T) * scale                  # [rows * group][kend]
-                e = torch.exp(sc - torch.amax(sc, dim=-1, keepdim=True))
-                p = e / torch.sum(e, dim=-1, keepdim=True)
-                out[r0:r1, hs, :] = (p @ Vd[:kend, kv, :]).reshape(r1 - r0, group, self.hd)
-        return out.numpy()
+                qb = q[r0:r1, hs, :].reshape(-1, self.hd).astype(np.float64)     # [rows * group][hd]
+                o = _block_attention(qb, Kd[:kend, kv, :], Vd[:kend, kv, :], scale, use_torch)
+                out[r0:r1, hs, :] = o.reshape(r1 - r0, group, self.hd)
+        return out
 
     def dense_ffn(self, a: np.ndarray, L) -> np.ndarray:
         act = self._operand(_silu(self._mm(a, L["w_gate"])) * self._mm(a, L["w_up"]))
