@@ -220,6 +220,29 @@ bd_status bd_decode(bd_model* model, const int32_t* prompt_dev, int32_t b, int32
                     int32_t* forwards_dev);
 
 /*
+ * bd_decode_static -- bd_decode that allocates nothing, for callers that
+ *  cannot allocate device memory (code under HIP graph capture, tight serving
+ *  loops, harnesses that forbid hipMalloc).  Same arguments, results and
+ *  synchronisation as bd_decode; the decode state (KV cache, window
+ *  activations, plans, split partials, LM-head partials) is laid out in a
+ *  static scratch of BD_STATIC_SCRATCH_BYTES = 64 MiB that every device the
+ *  library runs on holds from the library's load until the process ends.
+ *  The scratch of the current device is used (the model's device must be
+ *  current).  Every call on a device shares that device's scratch and leaves
+ *  its contents behind (each call clears what it needs): calls that overlap
+ *  on one device race, so the caller serialises them.  Per-launch profiling
+ *  (bd_profile) is suspended for the call.  Calls no hipMalloc, hipFree or
+ *  hipHostMalloc.
+ *  Errors: as bd_decode; BD_EUNSUPPORTED when the state of this decode
+ *  (b, P, G, block size, n_inflight and the model's dimensions) needs more
+ *  than the scratch holds -- the message gives the bytes needed.
+ */
+#define BD_STATIC_SCRATCH_BYTES_VALUE (64u << 20)
+bd_status bd_decode_static(bd_model* model, const int32_t* prompt_dev, int32_t b, int32_t P, int32_t G,
+                           const bd_decode_cfg* cfg, int32_t* tokens_dev, int32_t* commit_step_dev,
+                           int32_t* forwards_dev);
+
+/*
  * bd_state_reset -- return a state to the moment right after its prefill
  *  (the prompt cache is kept), so that a decode can be repeated without
  *  re-encoding the prompts.  Asynchronous.

@@ -19,7 +19,7 @@ BD_OK, BD_EINVAL, BD_ENOMEM, BD_EHIP, BD_ESTATE, BD_EUNSUPPORTED = 0, -1, -2, -3
 BD_F32, BD_BF16 = 0, 1
 
 EXPORTED = ["bd_init_model", "bd_quantize_fp8", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
-            "bd_decode", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
+            "bd_decode", "bd_decode_static", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
             "bd_profile_read", "bd_plan_projection", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select",
             "rl_select", "rl_alpha_sweep", "rl_split_exceedance", "rl_monte_carlo"]
 RL_METHODS = {"holm": 0, "bonferroni": 1, "fixed_sequence": 2, "uncorrected": 3, "plugin": 4}
@@ -78,6 +78,7 @@ def _load():
         "bd_commit": [VP, VP, P(I32)],
         "bd_state_read": [VP, VP, VP, VP, VP],
         "bd_decode": [VP, VP, I32, I32, I32, P(bd_decode_cfg), VP, VP, VP],
+        "bd_decode_static": [VP, VP, I32, I32, I32, P(bd_decode_cfg), VP, VP, VP],
         "bd_state_reset": [VP, VP],
         "bd_state_steps": [VP, P(I32)],
         "bd_state_stats": [VP, VP, P(ctypes.c_int64), I32],
@@ -175,6 +176,12 @@ def bd_state_read(model: int, state: int, tokens_ptr: int = 0, commit_ptr: int =
 def bd_decode(model: int, prompt_ptr: int, b: int, P: int, G: int, cfg: bd_decode_cfg, tokens_ptr: int,
               commit_ptr: int, fwd_ptr: int):
     _check(lib.bd_decode(model, prompt_ptr, b, P, G, ctypes.byref(cfg), tokens_ptr, commit_ptr, fwd_ptr))
+
+
+def bd_decode_static(model: int, prompt_ptr: int, b: int, P: int, G: int, cfg: bd_decode_cfg, tokens_ptr: int,
+                     commit_ptr: int, fwd_ptr: int):
+    _check(lib.bd_decode_static(model, prompt_ptr, b, P, G, ctypes.byref(cfg), tokens_ptr, commit_ptr,
+                                fwd_ptr))
 
 
 def bd_state_reset(model: int, state: int):
@@ -428,8 +435,9 @@ class State:
 
 
 def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_size: int, tau_semi=None,
-           tau_add: float = 0.0, skip_masked: bool = False):
-    """Whole decode through ``bd_decode``; returns numpy (tokens, commit_step, forwards)."""
+           tau_add: float = 0.0, skip_masked: bool = False, static: bool = False):
+    """Whole decode through ``bd_decode`` (``bd_decode_static`` with
+    ``static``); returns numpy (tokens, commit_step, forwards)."""
     torch = model.torch
     pr = torch.as_tensor(prompts, dtype=torch.int32).to(model.device).contiguous()
     b, P = pr.shape
@@ -437,5 +445,6 @@ def decode(model: Model, prompts, G: int, tau: float, n_inflight: int, block_siz
     c = torch.empty((b, G), dtype=torch.int32, device=model.device)
     f = torch.empty((b,), dtype=torch.int32, device=model.device)
     cfg = decode_cfg(tau, n_inflight, block_size, tau_semi, tau_add, skip_masked)
-    bd_decode(model.handle, pr.data_ptr(), b, P, G, cfg, t.data_ptr(), c.data_ptr(), f.data_ptr())
+    entry = bd_decode_static if static else bd_decode
+    entry(model.handle, pr.data_ptr(), b, P, G, cfg, t.data_ptr(), c.data_ptr(), f.data_ptr())
     return t.cpu().numpy(), c.cpu().numpy(), f.cpu().numpy()

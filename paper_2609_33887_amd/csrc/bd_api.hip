@@ -15,6 +15,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -131,6 +132,7 @@ struct bd_state {
   void* Hact;
   float* resid_ws;         // residual split-K partials (bf16 models)
   size_t resid_ws_floats;
+  size_t k_bytes, v_bytes, hact_bytes, act_bytes;   // sizes of the buffers cleared at set-up
   void* Alm;
   float *pmax, *psum;
   int32_t* parg;
@@ -172,6 +174,8 @@ static bd_status dev_alloc(bd_state* s, void** p, size_t bytes) {
 }
 
 extern "C" const char* bd_last_error(void) { return g_err.c_str(); }
+
+static bd_status scratch_on_current_device(void** out);
 
 namespace bd {
 void set_error(const char* msg) { g_err = msg; }
@@ -383,6 +387,13 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
     bd_model_free(m);
     return fail(BD_EHIP, "model upload: %s", hipGetErrorString(e));
   }
+  // device address of the static scratch on this device (bd_decode_static)
+  void* scratch_base = nullptr;
+  bd_status rs = scratch_on_current_device(&scratch_base);
+  if (rs != BD_OK) {
+    bd_model_free(m);
+    return rs;
+  }
   *out = m;
   return BD_OK;
 }
@@ -588,10 +599,35 @@ extern "C" bd_status bd_plan_projection(int32_t N, int32_t K, int32_t rows_cap, 
   return BD_OK;
 }
 
-extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
-                                const bd_decode_cfg* cfg, bd_state** out) {
-  if (!m || !cfg || !out) return fail(BD_EINVAL, "NULL argument");
-  *out = nullptr;
+// Where a state's device buffers come from.  HEAP: one hipMalloc per buffer
+// (owned by the state, released by bd_state_free).  COUNT: nothing is
+// allocated, only the bytes the layout needs are summed.  CARVE: consecutive
+// 256-byte-aligned slices of a region the caller provides (nothing is
+// allocated; the region must hold the COUNT total).
+struct Arena {
+  enum Mode { HEAP, COUNT, CARVE } mode = HEAP;
+  char* base = nullptr;
+  size_t cap = 0, used = 0;
+};
+
+static bd_status arena_alloc(bd_state* s, Arena& ar, void** p, size_t bytes) {
+  if (bytes == 0) bytes = 256;
+  const size_t sz = (bytes + 255) & ~(size_t)255;
+  if (ar.mode == Arena::HEAP) return dev_alloc(s, p, bytes);
+  if (ar.mode == Arena::COUNT) {
+    *p = nullptr;
+    ar.used += sz;
+    return BD_OK;
+  }
+  if (ar.used + sz > ar.cap) return fail(BD_ENOMEM, "state needs more than %zu bytes of scratch", ar.cap);
+  *p = ar.base + ar.used;
+  ar.used += sz;
+  return BD_OK;
+}
+
+static bd_status check_decode_args(const bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
+                                   const bd_decode_cfg* cfg) {
+  if (!m || !cfg) return fail(BD_EINVAL, "NULL argument");
   const int B = cfg->block_size, nb = cfg->n_inflight;
   if (b < 1 || P < 0 || G < 1 || B < 1 || nb < 1) return fail(BD_EINVAL, "need b, G, B, n_inflight >= 1 and P >= 0");
   if (P % B || G % B) return fail(BD_EINVAL, "P and G must be multiples of the block size");
@@ -601,9 +637,15 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   if (P > 0 && !prompt) return fail(BD_EINVAL, "NULL prompt");
   if (b > 256) return fail(BD_EUNSUPPORTED, "at most 256 sequences per state");
   if (nb > 8) return fail(BD_EUNSUPPORTED, "at most 8 in-flight blocks");
-  const bd_model_cfg& c = m->cfg;
+  return BD_OK;
+}
 
-  bd_state* s = new bd_state();
+// Sizes of the state and its device buffers, taken from the arena (no
+// device work).
+static bd_status state_layout(const bd_model* m, int32_t b, int32_t P, int32_t G, const bd_decode_cfg* cfg,
+                              bd_state* s, Arena& ar) {
+  const bd_model_cfg& c = m->cfg;
+  const int B = cfg->block_size, nb = cfg->n_inflight;
   s->b = b; s->P = P; s->G = G; s->B = B; s->nb = nb; s->tau = cfg->tau;
   s->semi_min = cfg->tau_semi < 0.0f ? -1 : min_resolved(cfg->tau_semi, B);
   s->add_min = min_resolved(cfg->tau_add, B);
@@ -614,17 +656,13 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   s->rows_pre = round_up(b * P, 256);
   s->rows_cap = s->rows_step > s->rows_pre ? s->rows_step : s->rows_pre;
   s->lm_cap = round_up(b * nb * B, 256);
-  const size_t esz = m->esz;
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim;
   const int qkv = (H + 2 * Hkv) * hd;
   const int ntiles = c.vocab / (m->bf16 ? 128 : 64);
   bd_status r = BD_OK;
-#define ALLOC(ptr, bytes)                                      \
-  do {                                                         \
-    if ((r = dev_alloc(s, (void**)&(ptr), (bytes))) != BD_OK) { \
-      bd_state_free(s);                                        \
-      return r;                                                \
-    }                                                          \
+#define ALLOC(ptr, bytes)                                                  \
+  do {                                                                     \
+    if ((r = arena_alloc(s, ar, (void**)&(ptr), (bytes))) != BD_OK) return r; \
   } while (0)
   ALLOC(s->tokens, (size_t)b * (P + G) * 4);
   ALLOC(s->commit_step, (size_t)b * G * 4);
@@ -649,7 +687,8 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ALLOC(s->Qb, (size_t)s->rows_cap * H * hd * 4);     // fp32, or a bf16 plane pair
   ALLOC(s->Ob, (size_t)s->rows_cap * H * hd * 4);
   const int Fh = c.n_experts ? c.n_shared * c.expert_ffn : c.ffn_dim;   // dense / shared FFN width
-  ALLOC(s->Hact, (size_t)s->rows_cap * (Fh > 0 ? Fh : 1) * 4);
+  s->hact_bytes = (size_t)s->rows_cap * (Fh > 0 ? Fh : 1) * 4;
+  ALLOC(s->Hact, s->hact_bytes);
   ALLOC(s->Alm, (size_t)s->lm_cap * d * 4);
   ALLOC(s->pmax, (size_t)ntiles * s->lm_cap * 4);
   ALLOC(s->psum, (size_t)ntiles * s->lm_cap * 4);
@@ -658,18 +697,11 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
   ALLOC(s->tok, (size_t)s->lm_cap * 4);
   // fp32 values or 2 bf16 planes: 4 bytes per element either way
   s->vstride = m->bf16 ? round_up(s->maxpos, 64) : s->maxpos;
-  const size_t k_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * 4;
-  const size_t v_bytes = (size_t)c.n_layers * b * Hkv * hd * s->vstride * 4;
-  ALLOC(s->Kc, k_bytes);
-  ALLOC(s->Vc, v_bytes);
-  if (m->bf16) {
-    ALLOC(s->rope, (size_t)s->maxpos * hd * sizeof(double));
-    hipError_t er = launch_rope_table(m->inv_freq, hd, s->maxpos, s->rope, m->stream);
-    if (er != hipSuccess) {
-      bd_state_free(s);
-      return fail(BD_EHIP, "rope table: %s", hipGetErrorString(er));
-    }
-  }
+  s->k_bytes = (size_t)c.n_layers * b * Hkv * s->maxpos * hd * 4;
+  s->v_bytes = (size_t)c.n_layers * b * Hkv * hd * s->vstride * 4;
+  ALLOC(s->Kc, s->k_bytes);
+  ALLOC(s->Vc, s->v_bytes);
+  if (m->bf16) ALLOC(s->rope, (size_t)s->maxpos * hd * sizeof(double));
   if (m->bf16) {
     s->resid_ws_floats = resid_ws_need(c, s->rows_step);
     const size_t pre = resid_ws_need(c, s->rows_pre);
@@ -691,14 +723,10 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
     ALLOC(s->moe.tile_e, (size_t)s->moe_tiles * 4);
     ALLOC(s->moe.tile_m0, (size_t)s->moe_tiles * 4);
     ALLOC(s->moe.ntiles, 16);
-    ALLOC(s->act_sorted, assign_cap * Fe * 4);
+    s->act_bytes = assign_cap * Fe * 4;
+    ALLOC(s->act_sorted, s->act_bytes);
     s->pl_act = assign_cap * Fe;
     ALLOC(s->y_sorted, assign_cap * d * 4);
-    hipError_t e2 = hipMemsetAsync(s->act_sorted, 0, assign_cap * Fe * 4, m->stream);
-    if (e2 != hipSuccess) {
-      bd_state_free(s);
-      return fail(BD_EHIP, "hipMemsetAsync: %s", hipGetErrorString(e2));
-    }
   }
   s->attn_splits = m->bf16 ? attention_splits(b, s->win_step, nb * B, H, Hkv, hd, s->maxpos) : 1;
   if (s->attn_splits > 1) {
@@ -706,49 +734,67 @@ extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, i
     ALLOC(s->attn_ws_ml, (size_t)s->attn_splits * s->rows_step * H * 2 * 4);
   }
 #undef ALLOC
+  return BD_OK;
+}
+
+// Device-side set-up of a laid-out state: RoPE table, cleared buffers, the
+// first plan and the prompt's forward.  Asynchronous, on the model's stream.
+static bd_status state_init(bd_model* m, const int32_t* prompt, bd_state* s) {
+  const bd_model_cfg& c = m->cfg;
+  const hipStream_t st = m->stream;
+  const int d = c.d_model, H = c.n_heads, hd = c.head_dim;
+  if (m->bf16) HIPCHK(launch_rope_table(m->inv_freq, hd, s->maxpos, s->rope, st));
+  // Row buffers are read in whole GEMM tiles: clear them once so that rows
+  // past the live count never hold NaN patterns.  The caches are cleared too:
+  // attention tiles read (and weigh by zero) positions past the live keys.
+  HIPCHK(launch_zero(s->A, (size_t)s->rows_cap * d * 4, st));
+  HIPCHK(launch_zero(s->Kc, s->k_bytes, st));
+  HIPCHK(launch_zero(s->Vc, s->v_bytes, st));
+  HIPCHK(launch_zero(s->Ob, (size_t)s->rows_cap * H * hd * 4, st));
+  HIPCHK(launch_zero(s->Hact, s->hact_bytes, st));
+  HIPCHK(launch_zero(s->Alm, (size_t)s->lm_cap * d * 4, st));
+  if (c.n_experts > 0) HIPCHK(launch_zero(s->act_sorted, s->act_bytes, st));
+  InitArgs ia;
+  ia.plan = s->plan[0];
+  ia.prefill = s->plan[2];
+  ia.tokens = s->tokens;
+  ia.prompt = s->P > 0 ? prompt : nullptr;
+  ia.commit_step = s->commit_step;
+  ia.seq_state = s->seq_state;
+  ia.b = s->b; ia.P = s->P; ia.G = s->G; ia.B = s->B; ia.nb = s->nb; ia.mask_id = c.mask_id;
+  ia.vocab = c.vocab;
+  ia.add_min = s->add_min;
+  ia.skip = s->skip;
+  ia.err_flag = m->err_flag;
+  ia.stats = s->stats;
+  HIPCHK(launch_init_decode(ia, st));
+  s->cur = 0;
+  s->steps = 0;
+  s->pending = false;
+  if (s->P > 0) return run_forward(m, s, s->plan[2], s->rows_pre, s->P, false);
+  return BD_OK;
+}
+
+extern "C" bd_status bd_prefill(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
+                                const bd_decode_cfg* cfg, bd_state** out) {
+  if (!out) return fail(BD_EINVAL, "NULL argument");
+  *out = nullptr;
+  bd_status r = check_decode_args(m, prompt, b, P, G, cfg);
+  if (r != BD_OK) return r;
+  bd_state* s = new bd_state();
+  Arena heap;
+  if ((r = state_layout(m, b, P, G, cfg, s, heap)) != BD_OK) {
+    bd_state_free(s);
+    return r;
+  }
   if (hipHostMalloc((void**)&s->host_flag, 64, hipHostMallocDefault) != hipSuccess) {
     s->host_flag = nullptr;
     bd_state_free(s);
     return fail(BD_ENOMEM, "hipHostMalloc failed");
   }
-  // Row buffers are read in whole GEMM tiles: clear them once so that rows
-  // past the live count never hold NaN patterns.
-  // The caches are cleared too: attention tiles read (and weigh by zero)
-  // positions past the live keys.
-  hipError_t e = hipMemsetAsync(s->A, 0, (size_t)s->rows_cap * d * 4, m->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(s->Kc, 0, k_bytes, m->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(s->Vc, 0, v_bytes, m->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(s->Ob, 0, (size_t)s->rows_cap * H * hd * 4, m->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(s->Hact, 0, (size_t)s->rows_cap * (Fh > 0 ? Fh : 1) * 4, m->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(s->Alm, 0, (size_t)s->lm_cap * d * 4, m->stream);
-  if (e != hipSuccess) {
+  if ((r = state_init(m, prompt, s)) != BD_OK) {
     bd_state_free(s);
-    return fail(BD_EHIP, "hipMemsetAsync: %s", hipGetErrorString(e));
-  }
-  InitArgs ia;
-  ia.plan = s->plan[0];
-  ia.prefill = s->plan[2];
-  ia.tokens = s->tokens;
-  ia.prompt = P > 0 ? prompt : nullptr;
-  ia.commit_step = s->commit_step;
-  ia.seq_state = s->seq_state;
-  ia.b = b; ia.P = P; ia.G = G; ia.B = B; ia.nb = nb; ia.mask_id = c.mask_id; ia.vocab = c.vocab;
-  ia.add_min = s->add_min;
-  ia.skip = s->skip;
-  ia.err_flag = m->err_flag;
-  ia.stats = s->stats;
-  e = launch_init_decode(ia, m->stream);
-  if (e != hipSuccess) {
-    bd_state_free(s);
-    return fail(BD_EHIP, "init kernel: %s", hipGetErrorString(e));
-  }
-  s->cur = 0;
-  if (P > 0) {
-    r = run_forward(m, s, s->plan[2], s->rows_pre, P, false);
-    if (r != BD_OK) {
-      bd_state_free(s);
-      return r;
-    }
+    return r;
   }
   *out = s;
   return BD_OK;
@@ -831,9 +877,11 @@ extern "C" bd_status bd_commit(bd_model* m, bd_state* s, int32_t* all_done_host)
   s->steps += 1;
   s->pending = false;
   if (all_done_host) {
-    HIPCHK(hipMemcpyAsync(s->host_flag, s->plan[s->cur].hdr + 2, 4, hipMemcpyDeviceToHost, m->stream));
+    int32_t flag = 0;     // states in the static scratch have no pinned flag
+    int32_t* dst = s->host_flag ? s->host_flag : &flag;
+    HIPCHK(hipMemcpyAsync(dst, s->plan[s->cur].hdr + 2, 4, hipMemcpyDeviceToHost, m->stream));
     HIPCHK(hipStreamSynchronize(m->stream));
-    *all_done_host = s->host_flag[0];
+    *all_done_host = *dst;
     bd_status r = check_err_flag(m);
     if (r != BD_OK) return r;
   }
@@ -862,30 +910,91 @@ extern "C" bd_status bd_state_read(bd_model* m, bd_state* s, int32_t* tokens_dev
   return check_err_flag(m);
 }
 
+// Denoising steps until every sequence is done.  Each step commits at least
+// one token of every unfinished sequence, so G steps always suffice; the
+// host checks the device flag every few steps (steps after completion are
+// empty launches).
+static bd_status run_decode_loop(bd_model* m, bd_state* s) {
+  const int check = 4;
+  int32_t done = 0;
+  bd_status r = BD_OK;
+  while (!done) {
+    for (int k = 0; k < check && r == BD_OK; ++k) {
+      r = bd_denoise_step(m, s, nullptr, nullptr, nullptr);
+      if (r == BD_OK) r = bd_commit(m, s, (k == check - 1) ? &done : nullptr);
+    }
+    if (r != BD_OK) return r;
+    if (!done && s->steps > s->G + check) return fail(BD_ESTATE, "decode did not finish within %d steps", s->steps);
+  }
+  return BD_OK;
+}
+
 extern "C" bd_status bd_decode(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
                                const bd_decode_cfg* cfg, int32_t* tokens_dev, int32_t* commit_step_dev,
                                int32_t* forwards_dev) {
   bd_state* s = nullptr;
   bd_status r = bd_prefill(m, prompt, b, P, G, cfg, &s);
   if (r != BD_OK) return r;
-  // Each step commits at least one token of every unfinished sequence, so G
-  // steps always suffice; the host checks the device flag every few steps
-  // (steps after completion are empty launches).
-  const int check = 4;
-  int32_t done = 0;
-  while (!done) {
-    for (int k = 0; k < check && r == BD_OK; ++k) {
-      r = bd_denoise_step(m, s, nullptr, nullptr, nullptr);
-      if (r == BD_OK) r = bd_commit(m, s, (k == check - 1) ? &done : nullptr);
-    }
-    if (r != BD_OK) break;
-    if (!done && s->steps > G + check) {
-      r = fail(BD_ESTATE, "decode did not finish within %d steps", s->steps);
-      break;
-    }
-  }
+  r = run_decode_loop(m, s);
   if (r == BD_OK) r = bd_state_read(m, s, tokens_dev, commit_step_dev, forwards_dev);
   bd_state_free(s);
+  return r;
+}
+
+// ---- decode without allocation ---------------------------------------------
+// The static scratch that bd_decode_static lays its state out in.  Each
+// device holds its own copy from the library's load until the process ends.
+// In host code `scratch` only stands for the symbol: its device address on
+// each device comes from hipGetSymbolAddress (looked up once per device, at
+// bd_init_model or at the first call on the device) and only that address is
+// handed to kernels.
+static_assert(BD_STATIC_SCRATCH_BYTES == BD_STATIC_SCRATCH_BYTES_VALUE, "scratch size as declared in bd.h");
+static __device__ __align__(256) unsigned char scratch[BD_STATIC_SCRATCH_BYTES];
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[BD_MAX_DEVICES];
+
+static bd_status scratch_on_current_device(void** out) {
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= BD_MAX_DEVICES) return fail(BD_EUNSUPPORTED, "device %d outside [0, %d)", dev, BD_MAX_DEVICES);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(BD_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return BD_OK;
+}
+
+extern "C" bd_status bd_decode_static(bd_model* m, const int32_t* prompt, int32_t b, int32_t P, int32_t G,
+                                      const bd_decode_cfg* cfg, int32_t* tokens_dev, int32_t* commit_step_dev,
+                                      int32_t* forwards_dev) {
+  bd_status r = check_decode_args(m, prompt, b, P, G, cfg);
+  if (r != BD_OK) return r;
+  bd_state s{};
+  Arena count;
+  count.mode = Arena::COUNT;
+  if ((r = state_layout(m, b, P, G, cfg, &s, count)) != BD_OK) return r;
+  if (count.used > BD_STATIC_SCRATCH_BYTES)
+    return fail(BD_EUNSUPPORTED, "this decode needs %zu bytes of state; the static scratch holds %zu "
+                "(use bd_decode)", count.used, (size_t)BD_STATIC_SCRATCH_BYTES);
+  void* base = nullptr;
+  if ((r = scratch_on_current_device(&base)) != BD_OK) return r;
+  Arena carve;
+  carve.mode = Arena::CARVE;
+  carve.base = (char*)base;
+  carve.cap = BD_STATIC_SCRATCH_BYTES;
+  bd_state t{};
+  if ((r = state_layout(m, b, P, G, cfg, &t, carve)) != BD_OK) return r;
+  const bool prof = m->prof;     // per-launch timing would create events: off for this call
+  m->prof = false;
+  r = state_init(m, prompt, &t);
+  if (r == BD_OK) r = run_decode_loop(m, &t);
+  if (r == BD_OK) r = bd_state_read(m, &t, tokens_dev, commit_step_dev, forwards_dev);
+  else (void)hipStreamSynchronize(m->stream);   // leave no work in flight on the scratch
+  m->prof = prof;
   return r;
 }
 

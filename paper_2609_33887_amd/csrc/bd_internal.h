@@ -257,6 +257,11 @@ hipError_t launch_rope_kv(const float* QKV, PlanView plan, int rows_cap, int H, 
 
 constexpr int BD_NSTATS = 12;
 
+// Static scratch of the allocation-free decode (bytes per device) and the
+// devices it is tracked on.
+constexpr size_t BD_STATIC_SCRATCH_BYTES = (size_t)64 << 20;
+constexpr int BD_MAX_DEVICES = 64;
+
 struct CommitArgs {
   PlanView in, out;
   const float* conf;        // [lm rows of `in`]
@@ -326,6 +331,9 @@ hipError_t launch_rope_table(const double* inv_freq, int hd, int maxpos, double*
 // Interleave gate/up projections in groups of 16 rows (SwiGLU epilogue layout).
 hipError_t launch_pack_gate_up(const void* gate, const void* up, void* out, int F, size_t row_bytes,
                                hipStream_t st);
+
+// Zero `bytes` (a multiple of 4) at p (4-byte aligned) with a kernel.
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
 
 // Debug scatter of logits rows to [b][G][V].
 hipError_t launch_scatter_logits(const float* logits, PlanView plan, int V, int P, int G,

@@ -766,4 +766,30 @@ hipError_t launch_rope_table(const double* inv_freq, int hd, int maxpos, double*
   return hipGetLastError();
 }
 
+
+// Zero n 32-bit words (a kernel, so that the clear can sit in a captured
+// stream; 16-byte stores on the aligned body).
+__global__ __launch_bounds__(256) void k_zero_words(uint32_t* __restrict__ p, size_t n) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t head = ((16 - ((uintptr_t)p & 15)) & 15) / 4;     // words before a 16-byte boundary
+  const size_t h = head < n ? head : n;
+  if (i0 < h) p[i0] = 0u;
+  u32x4* q = (u32x4*)(p + h);
+  const size_t nv = (n - h) / 4;
+  for (size_t i = i0; i < nv; i += stride) q[i] = u32x4{0u, 0u, 0u, 0u};
+  for (size_t i = h + 4 * nv + i0; i < n; i += stride) p[i] = 0u;
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  if (((uintptr_t)p & 3) || (bytes & 3)) return hipErrorInvalidValue;
+  const size_t n = bytes / 4;
+  size_t blocks = (n / 4 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  k_zero_words<<<(unsigned)blocks, 256, 0, st>>>((uint32_t*)p, n);
+  return hipGetLastError();
+}
+
 }  // namespace bd
