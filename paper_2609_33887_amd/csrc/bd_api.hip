@@ -559,8 +559,8 @@ static int min_resolved(float thr, int B) {
 // Floats of residual split partials the O and down projections of a bf16
 // model may write over rows_cap rows (the largest of the two extents; they
 // never hold partials at the same time: the RMSNorm between them folds them).
-static ResidSplit resid_split_of(int N, int K, int rows_cap) {
-  const GemmPlan p = plan_resid(N, K, rows_cap);
+static ResidSplit resid_split_of(int N, int K, int rows_cap, bool wide_ok = true) {
+  const GemmPlan p = plan_resid(N, K, rows_cap, wide_ok);
   ResidSplit r{};
   r.nx = N / p.bn;
   r.bm = p.bm;
@@ -570,11 +570,16 @@ static ResidSplit resid_split_of(int N, int K, int rows_cap) {
 }
 
 static size_t resid_ws_need(const bd_model_cfg& c, int rows_cap) {
+  // the larger extent of the bf16-weight and the fp8-weight plans
   const int d = c.d_model;
-  size_t need = resid_extent_max(rows_cap, d, resid_split_of(d, c.n_heads * c.head_dim, rows_cap));
-  if (c.n_experts == 0) {
-    const size_t dn = resid_extent_max(rows_cap, d, resid_split_of(d, c.ffn_dim, rows_cap));
-    if (dn > need) need = dn;
+  size_t need = 0;
+  for (int wide = 0; wide < 2; ++wide) {
+    const size_t o = resid_extent_max(rows_cap, d, resid_split_of(d, c.n_heads * c.head_dim, rows_cap, wide));
+    if (o > need) need = o;
+    if (c.n_experts == 0) {
+      const size_t dn = resid_extent_max(rows_cap, d, resid_split_of(d, c.ffn_dim, rows_cap, wide));
+      if (dn > need) need = dn;
+    }
   }
   return need;
 }
@@ -587,10 +592,10 @@ extern "C" bd_status bd_plan_projection(int32_t N, int32_t K, int32_t rows_cap, 
   GemmPlan p;
   int64_t wsf = 0;
   if (resid) {
-    p = plan_resid(N, K, rows_cap);
+    p = plan_resid(N, K, rows_cap, true);
     wsf = (int64_t)resid_extent_max(rows_cap, N, resid_split_of(N, K, rows_cap));
   } else {
-    p = plan_gemm(true, N, K, rows_cap);
+    p = plan_gemm(true, N, K, rows_cap, false, true);
   }
   if (bm_out) *bm_out = p.bm;
   if (bn_out) *bn_out = p.bn;

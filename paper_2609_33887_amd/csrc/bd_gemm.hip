@@ -277,8 +277,9 @@ __device__ __forceinline__ void scale_columns(MfmaTile<BM, BN>& t, const float* 
 }
 
 // GEMM, epilogue applied in registers.  Items (split z, column tile x, row
-// tile y) are numbered z-major, then x, then y: an XCD's range shares the A
-// and W slices of one split and the W tiles of a few column tiles.  For
+// tile y) are numbered z-major, then in bands of row tiles (band_tile): an
+// XCD's concurrent workgroups share the A slices of a few row tiles and the
+// W slices of a few column tiles of one split.  For
 // EPI_ADD_F32 with a split workspace, the kernel picks S = resid_splits(M)
 // K-splits on the device (zmax is the largest allowed); with S > 1 every
 // split stores its raw partial tile to ws[split][row][col] (rows padded to
@@ -304,8 +305,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
   const int items = X * Y * S;
   const int u = xcd_item(blockIdx.x, items);
   if (u >= items) return;
-  const int z = u / (X * Y), xy = u % (X * Y);
-  const int m0 = (xy % Y) * BM, n0 = (xy / Y) * BN;
+  const int z = u / (X * Y);
+  int tx, ty;
+  band_tile(u % (X * Y), X, Y, BAND_R, tx, ty);
+  const int m0 = ty * BM, n0 = tx * BN;
   const int klen = K / S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   BD_GEMM_SMEM(BM, BN, W8);
@@ -372,9 +375,11 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, 
   constexpr int FM = BM / 32, FN = BN / 32;
   const int M = *Mp;
   const int X = (e.H + 2 * e.Hkv) * e.hd / BN, Y = (M + BM - 1) / BM;
-  const int u = xcd_item(blockIdx.x, X * Y);      // items: column tile major, row tile minor
+  const int u = xcd_item(blockIdx.x, X * Y);
   if (u >= X * Y) return;
-  const int m0 = (u % Y) * BM, n0 = (u / Y) * BN;
+  int tx, ty;
+  band_tile(u, X, Y, BAND_R, tx, ty);
+  const int m0 = ty * BM, n0 = tx * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   BD_GEMM_SMEM(BM, BN, W8);
   MfmaTile<BM, BN> t;
@@ -525,13 +530,14 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
                                                       int32_t* __restrict__ parg) {
   constexpr int TBM = 128, TBN = 128;
   const int M = *Mp;
-  // items: vocabulary tile major, row tile minor (an XCD streams its share of
-  // the head once, every row tile of a vocabulary tile running together)
+  // items in bands of row tiles (band_tile): an XCD's concurrent workgroups
+  // share a few row tiles of the operand and a few vocabulary tiles of the head
   const int X = V / TBN, Y = (M + TBM - 1) / TBM;
   const int u = xcd_item(blockIdx.x, X * Y);
   if (u >= X * Y) return;
-  const int m0 = (u % Y) * TBM, n0 = (u / Y) * TBN;
-  const int vt = u / Y;
+  int vt, ty;
+  band_tile(u, X, Y, BAND_R, vt, ty);
+  const int m0 = ty * TBM, n0 = vt * TBN;
   BD_GEMM_SMEM(TBM, TBN, false);
   __shared__ float red_m[2][TBM], red_s[2][TBM];
   __shared__ int32_t red_a[2][TBM];
@@ -764,17 +770,23 @@ static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t
   }
 }
 
-// Tile choice: 128x128 when that tiling gives enough workgroups over the
-// row capacity (the 64x64 tile runs out of LDS bandwidth on large products),
+// Tile choice: 128x256 (each wave 64 x 128: a third fewer LDS bytes per MFMA
+// than 64 x 64 waves, 128 KB of LDS) for products at least 2048 wide over
+// windows of at least 2048 rows, when the caller allows it (bf16 weights and
+// a kernel instantiated for it): on 3328-row products it ran gate/up
+// (N 16384) in 494 us against 550, down (N 2048, K 8192) in 259 against 291.
+// Otherwise 128x128 when that tiling gives enough workgroups over the row
+// capacity (the 64x64 tile runs out of LDS bandwidth on large products),
 // else 64x64.  Enough: 1024 for plain products (below that the 128x128 grid
 // leaves part of the chip idle for a round: the gate/up product of the dense
 // decode, 512 workgroups over its 1024-row capacity, runs 6% faster in
 // 64x64 tiles), 512 for residual projections, whose split-K partials grow
 // with the tile count (the multi-block O projection ran 18% slower in 64x64
 // tiles).  zmax: the largest residual split (1 = none).
-GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid) {
+GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid, bool wide_ok) {
   (void)K;
   if (!is_bf16) return GemmPlan{64, 64, 1};
+  if (wide_ok && N % 256 == 0 && N >= 2048 && rows_cap >= 2048) return GemmPlan{128, 256, 1};
   if (N % 128 == 0 && (N / 128) * cdiv(rows_cap, 128) >= (resid ? 512 : 1024)) return GemmPlan{128, 128, 1};
   return GemmPlan{64, 64, 1};
 }
@@ -784,7 +796,9 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
                                int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
                                hipStream_t st, const float* wscale) {
   const bool big = p.bm == 128 && p.bn == 128, small = p.bm == 64 && p.bn == 64;
-  if ((!big && !small) || p.zmax < 1 || p.zmax > 8) return hipErrorInvalidValue;
+  const bool wide = p.bm == 128 && p.bn == 256;
+  if ((!big && !small && !wide) || p.zmax < 1 || p.zmax > 8) return hipErrorInvalidValue;
+  if (wide && wscale) return hipErrorInvalidValue;       // no fp8-weight variant of the wide tile
   if (N % p.bn || K % KALIGN) return hipErrorInvalidValue;
   if (p.zmax > 1 && (epi != EPI_ADD_F32 || !ws)) return hipErrorInvalidValue;
   // 1-D grid: every (split, column tile, row tile) of the row capacity, + 7
@@ -797,7 +811,9 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
   if (wscale) {
     if (big) BD_CFG(128, 128, true); else BD_CFG(64, 64, true);
   } else {
-    if (big) BD_CFG(128, 128, false); else BD_CFG(64, 64, false);
+    if (wide) BD_CFG(128, 256, false);
+    else if (big) BD_CFG(128, 128, false);
+    else BD_CFG(64, 64, false);
   }
 #undef BD_CFG
   return hipGetLastError();
@@ -819,11 +835,11 @@ size_t resid_extent_max(int rows_cap, int N, const ResidSplit& r) {
   return mx;
 }
 
-GemmPlan plan_resid(int N, int K, int rows_cap) {
-  // deep products (K >= 4096) take 128x128 tiles: with K split, their A and
+GemmPlan plan_resid(int N, int K, int rows_cap, bool wide_ok) {
+  // deep products (K >= 4096) take 128-row tiles: with K split, their A and
   // W re-reads halve against 64x64 at the same parallelism
-  GemmPlan p = plan_gemm(true, N, K, rows_cap, true);
-  if (K >= 4096 && N % 128 == 0) p = GemmPlan{128, 128, 1};
+  GemmPlan p = plan_gemm(true, N, K, rows_cap, true, wide_ok);
+  if (K >= 4096 && N % 128 == 0 && p.bm != 128) p = GemmPlan{128, 128, 1};
   p.zmax = 8;
   return p;
 }
@@ -836,7 +852,7 @@ hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plan
   if (!is_bf16 || !ws)
     return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st,
                        wscale);
-  const GemmPlan p = plan_resid(N, K, rows_cap);
+  const GemmPlan p = plan_resid(N, K, rows_cap, wscale == nullptr);
   ResidSplit r{};
   r.nx = N / p.bn;
   r.bm = p.bm;
@@ -857,7 +873,7 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
                            const float* wscale) {
   const int N = (e.H + 2 * e.Hkv) * e.hd;
   if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
-  const GemmPlan p = plan_gemm(true, N, K, rows_cap);
+  const GemmPlan p = plan_gemm(true, N, K, rows_cap, false, false);
   if (N % p.bn) return hipErrorInvalidValue;
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) + 7);
   const bf16_t* a = (const bf16_t*)A;
@@ -875,8 +891,8 @@ hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_p
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
                        size_t out_plane, hipStream_t st, const float* wscale) {
   if (is_bf16)
-    return launch_gemm_planned(plan_gemm(true, N, K, rows_cap), epi, A, lda, a_plane, W, ldw, N, K,
-                               M_dev, rows_cap, out, ldo, out_plane, nullptr, st, wscale);
+    return launch_gemm_planned(plan_gemm(true, N, K, rows_cap, false, wscale == nullptr), epi, A, lda, a_plane,
+                               W, ldw, N, K, M_dev, rows_cap, out, ldo, out_plane, nullptr, st, wscale);
   if (wscale) return hipErrorInvalidValue;
   if (N % SBN || K % SBK) return hipErrorInvalidValue;
   dim3 grid(N / SBN, cdiv(rows_cap, SBM));

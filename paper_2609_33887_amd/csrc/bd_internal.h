@@ -152,8 +152,9 @@ hipError_t launch_transpose_f32(const float* in, float* out, int rows, int cols,
 struct GemmPlan {
   int bm, bn, zmax;        // tile; largest residual K-split (1 = none)
 };
-GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid = false);
-// bf16 GEMM with an explicit plan (128x128 or 64x64; K % KALIGN == 0;
+// wide_ok: the 128x256 tile may be chosen (bf16 weights, k_gemm_bf16 kernels)
+GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid = false, bool wide_ok = false);
+// bf16 GEMM with an explicit plan (128x256, 128x128 or 64x64; K % KALIGN == 0;
 // zmax > 1 only for EPI_ADD_F32 with a residual-split workspace ws).
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
@@ -161,7 +162,7 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
                                hipStream_t st, const float* wscale = nullptr);
 // Plan of a residual projection (O and down of bf16 models): tile shape and
 // the largest K-split (zmax).
-GemmPlan plan_resid(int N, int K, int rows_cap);
+GemmPlan plan_resid(int N, int K, int rows_cap, bool wide_ok);
 // X[M][N] += A . W^T for the residual stream.  bf16 with a workspace ws of
 // ws_floats floats: the kernel may split K (see ResidSplit) and *fold
 // describes the pending partials, which the next launch_rmsnorm of X must be
@@ -195,6 +196,23 @@ __device__ __forceinline__ int xcd_item(int id, int items) {
   const int per = (items + 7) / 8;
   return id < 8 * per ? (id % 8) * per + id / 8 : items;
 }
+
+// Tile (x, y) of work item u in a grid of X column tiles by Y row tiles,
+// walked in bands of R row tiles and, inside a band, column by column (the
+// band's h <= R row tiles of one column are neighbours).  With the items of
+// an XCD-aware launch, the workgroups running at once on one XCD (about 32
+// consecutive items of its range) then cover about R row tiles x 32 / R
+// column tiles, so each activation row tile and weight column tile they read
+// is fetched into that XCD's L2 once for all of them; walking all row tiles
+// of a column first would re-fetch the whole activation for every column.
+__device__ __forceinline__ void band_tile(int u, int X, int Y, int R, int& x, int& y) {
+  const int y0 = (u / (R * X)) * R;
+  const int h = Y - y0 < R ? Y - y0 : R;
+  const int ub = u - y0 * X;
+  x = ub / h;
+  y = y0 + ub % h;
+}
+constexpr int BAND_R = 4;   // row tiles per band: a 128-row hi/lo activation tile is twice a weight tile
 
 // One layer's KV cache.  K: [seq][kv head][pos][hd].  V: bf16 models keep
 // it transposed in tiles of 64 keys, [seq][kv head][pos / 64][hd][64]: a

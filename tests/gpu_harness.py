@@ -12,8 +12,11 @@ excused only when the oracle's numbers make it a near-tie:
   T3  a forced commit (of the sequence, or of one block under semi-completion)
       whose two best confidences are within 1e-3;
   T4  (MoE) a step whose forward, in the oracle, routed some row with a gap of
-      at most 1e-5 between its k-th and (k+1)-th router logits: expert choice
-      there can differ, so that step's statistics and decisions are excused.
+      at most 1e-4 between its k-th and (k+1)-th router logits: expert choice
+      there can differ from the GPU's (float32 router logits of 16-bit
+      activations carry errors of order 1e-5), so when such a step differs,
+      its statistics and decisions are excused as a whole; such a step that
+      agrees is counted like any other.
 
 After an excused difference the oracle adopts the GPU's decision, so that the
 rest of the trace stays comparable.  Any other difference is a failure.
@@ -25,7 +28,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 NEAR = 1e-3
-ROUTER_NEAR = 1e-5
+ROUTER_NEAR = 1e-4
 
 
 @dataclass
@@ -148,22 +151,21 @@ def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, con
                 rep.failures.append((i, step, "masked position sets differ"))
                 break
             gaps = oracle_model.router_gaps
-            if gaps and min(float(np.min(g)) for g in gaps) <= ROUTER_NEAR:
-                rep.t4 += 1
-                gsel = trace.commit_step[i, masked - P] == step
-                d.count_participation(masked[gsel])
-                d.apply(masked[gsel], trace.tokens[i, masked - P][gsel], step)
-                step += 1
-                continue
-            rep.positions += len(masked)
-            rep.max_conf_diff = max(rep.max_conf_diff, float(np.max(np.abs(conf - gconf))))
+            near_route = bool(gaps) and min(float(np.min(g)) for g in gaps) <= ROUTER_NEAR
+            # the step's comparison; a step whose routing had a near-tie is
+            # excused (T4) only when it differs, and then as a whole
+            fails, t1, t2, t3 = [], 0, 0, 0
+            cdiff = float(np.max(np.abs(conf - gconf)))
+            ldiff = 0.0
             if glog is not None:
                 fin = np.isfinite(z)
                 if not np.array_equal(fin, np.isfinite(glog)):
-                    rep.failures.append((i, step, "suppressed logit columns differ"))
-                rep.max_logit_diff = max(rep.max_logit_diff, float(np.max(np.abs(z[fin] - glog[fin]))))
-            if np.any(np.abs(conf - gconf) > conf_tol):
-                rep.failures.append((i, step, f"confidence differs by {np.max(np.abs(conf - gconf)):.3g}"))
+                    fails.append((i, step, "suppressed logit columns differ"))
+                ldiff = float(np.max(np.abs(z[fin] - glog[fin])))
+                if ldiff > logit_tol:
+                    fails.append((i, step, f"logits differ by {ldiff:.3g}"))
+            if cdiff > conf_tol:
+                fails.append((i, step, f"confidence differs by {cdiff:.3g}"))
             # decisions
             own, forced = d.decision(masked, conf)
             gsel = trace.commit_step[i, masked - P] == step
@@ -178,19 +180,29 @@ def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, con
 
             for k in np.nonzero(own != gsel)[0]:
                 if abs(conf[k] - tau32) <= NEAR:
-                    rep.t1 += 1
+                    t1 += 1
                 elif forced_near(k):
-                    rep.t3 += 1
+                    t3 += 1
                 else:
-                    rep.failures.append((i, step, f"commit decision differs at position {masked[k] - P} "
-                                                  f"(oracle conf {conf[k]:.6f}, GPU conf {gconf[k]:.6f})"))
+                    fails.append((i, step, f"commit decision differs at position {masked[k] - P} "
+                                           f"(oracle conf {conf[k]:.6f}, GPU conf {gconf[k]:.6f})"))
             both = own & gsel
             gtoks = trace.tokens[i, masked - P]
             for k in np.nonzero(both & (tok != gtoks))[0]:
                 if conf[k] - p2[k] <= NEAR:
-                    rep.t2 += 1
+                    t2 += 1
                 else:
-                    rep.failures.append((i, step, f"token differs at position {masked[k] - P}"))
+                    fails.append((i, step, f"token differs at position {masked[k] - P}"))
+            if fails and near_route:
+                rep.t4 += 1
+            else:
+                rep.failures += fails
+                rep.t1 += t1
+                rep.t2 += t2
+                rep.t3 += t3
+                rep.positions += len(masked)
+                rep.max_conf_diff = max(rep.max_conf_diff, cdiff)
+                rep.max_logit_diff = max(rep.max_logit_diff, ldiff)
             d.count_participation(masked[gsel])
             d.apply(masked[gsel], gtoks[gsel], step)
             step += 1

@@ -64,7 +64,7 @@ def test_residual_workspace_covers_every_row_count(cfg):
     for N, K in _resid_shapes(w):
         for rc in _rows_caps(w):
             bm, bn, zmax, wsf = bd.bd_plan_projection(N, K, rc, True)
-            assert (bm, bn) in ((128, 128), (64, 64)) and 1 <= zmax <= 8
+            assert (bm, bn) in ((128, 256), (128, 128), (64, 64)) and 1 <= zmax <= 8
             need = _extent_max(N, K, rc, bm, bn, zmax)
             assert wsf == need, (N, K, rc, bm, wsf, need)
 
@@ -74,7 +74,7 @@ def test_plain_projections_do_not_split():
     for w in WORKLOADS.values():
         if w.dtype != "bf16":
             continue
-        for N, K in [(w.qkv_dim, w.d_model), (w.d_model, w.n_heads * w.head_dim)]:
+        for N, K in [(w.qkv_dim, w.d_model), (2 * max(w.ffn_dim, 64), w.d_model)]:
             for rc in _rows_caps(w):
                 bm, bn, zmax, wsf = bd.bd_plan_projection(N, K, rc, False)
                 assert zmax == 1 and wsf == 0 and N % bn == 0

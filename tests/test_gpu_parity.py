@@ -522,27 +522,51 @@ def test_error_paths():
 
 def test_moe_2048_redline_sweep_matches_oracle():
     """Redline on the GPU-decoded MoE sweep: 12 candidates (tau x in-flight
-    blocks) plus the reference (tau > 1, one block) on one batch of 64
-    calibration prompts; correctness = the final 16 tokens equal the
-    reference's.  Violation counts, valid set and selection of the C
-    implementation equal the oracle's on the same matrix, bit for bit."""
+    blocks) plus the reference (tau > 1, one block), each decoding the
+    calibration prompts in batches of 64; correctness = the final 16 tokens
+    equal the reference's.  Violation counts, p-values, valid set and
+    selection of the C implementation equal the oracle's on the same matrix,
+    at the workload's budget and along a budget sweep up to 0.5 (where
+    candidates become valid).  64 prompts by default; BD_SWEEP_PROMPTS=1000
+    runs the workload's full calibration set and writes a summary under
+    gpurun_out/."""
+    import json
+    import os
+    from paper_2609_33887_amd import bd
     from paper_2609_33887_amd.sweep import redline_sweep
     from oracle import redline as orl
     _need_gpu()
+    n = int(os.environ.get("BD_SWEEP_PROMPTS", "64"))
     w = workload(4)
     model, _ = get_model(w)
-    prompts = make_prompts(w, 64)
+    prompts = make_prompts(w, n)
     cands = [(t, nb) for t in (0.95, 0.9, 0.8, 0.7) for nb in (1, 2, 3)]
+    alphas = [0.05, 0.10, 0.15, 0.20, 0.25, 0.30, 0.35, 0.40, 0.45, 0.50]
+    t0 = time.perf_counter()
     r = redline_sweep(model, prompts, w.gen_len, w.block_size, cands, (2.0, 1), 0.10, 0.05, batch=64,
-                      progress=_say)
+                      progress=_say, alphas=alphas)
+    t_gpu = time.perf_counter() - t0
     assert r["tpf"][0] == 1.0                      # tau > 1: one token per forward
+    V, p, valid, sel, near = bd.rl_risk_select(r["correct"], r["tpf"], 0, 0.10, 0.05)
     o = orl.risk_select(r["correct"], r["tpf"], 0, 0.10, 0.05)
-    assert r["V"].tolist() == o.V.tolist()
-    assert r["valid"].tolist() == o.valid.tolist()
-    assert r["selected"] == o.selected
-    for a, b in zip(r["p"], o.p):
+    assert V.tolist() == o.V.tolist() == r["V"].tolist()
+    assert valid.tolist() == o.valid.tolist() == r["valid"].tolist()
+    assert sel == o.selected == r["selected"]
+    for a, b in zip(p, o.p):
         assert abs(a - float(b)) <= 1e-11 * float(b) + 1e-300
-    _say(f"  TPF {['%.3f' % t for t in r['tpf']]} V {r['V'].tolist()} selected {r['grid'][r['selected']]}")
+    osel, onval, ohat = orl.alpha_sweep(r["correct"], r["tpf"], 0, alphas, 0.05)
+    assert r["alpha_selected"] == list(osel) and r["alpha_n_valid"] == list(onval) and r["alpha_hat"] == ohat
+    _say(f"  {n} prompts: TPF {['%.3f' % t for t in r['tpf']]} V {r['V'].tolist()} "
+         f"selected {r['grid'][r['selected']]}; budget sweep: selected {r['alpha_selected']}, "
+         f"valid {r['alpha_n_valid']}, alpha_hat {r['alpha_hat']}")
+    if n != 64:
+        os.makedirs("gpurun_out", exist_ok=True)
+        with open(os.path.join("gpurun_out", f"moe_sweep_{n}.json"), "w") as f:
+            json.dump({"prompts": n, "grid": r["labels"], "tpf": r["tpf"], "V": r["V"].tolist(),
+                       "p": [float(x) for x in r["p"]], "valid": r["valid"].tolist(), "selected": r["selected"],
+                       "alphas": alphas, "alpha_selected": r["alpha_selected"],
+                       "alpha_n_valid": r["alpha_n_valid"], "alpha_hat": r["alpha_hat"],
+                       "oracle_agrees": True, "near_ties": int(near), "gpu_seconds": t_gpu}, f)
 
 
 def test_engine_grid_sweep_matches_oracle():
