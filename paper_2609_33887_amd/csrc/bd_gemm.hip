@@ -53,13 +53,14 @@ __device__ __forceinline__ void store_pair(bf16_t* p, size_t plane, float x) {
 // consumed, and one barrier per stage both publishes the stage and retires
 // the one the next loads overwrite.  A wave's load instruction writes 1 KiB of
 // LDS = 16 rows x 64 B, lane l at byte 16 l; in LDS the 16-byte chunk c of row r
-// sits at position c ^ swz(r), swz(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1), so
-// that the rows read together for one MFMA fragment fall on distinct bank
-// groups whether the LDS serves 8 lanes from 32 banks or 16 lanes from 64
-// banks per cycle.
+// sits at position c ^ swz(r), swz(r) = (r >> 1) & 3.  A fragment read (lane
+// l: row l & 15, chunk l >> 4) is then free of bank conflicts: measured with
+// the LDS bank-conflict counter on gfx950, this pattern reads 141 B/clk per CU
+// with no conflict cycles, where the earlier (r >> 1) & 3 ^ (r >> 3) & 1 had
+// two-way conflicts (106 B/clk) and unswizzled rows 114 B/clk.
 constexpr int SK = 32;       // K per pipeline stage (KALIGN = 4 stages)
 
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 3) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -92,9 +93,11 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint2 v) {
   return o;
 }
 
-template <int BM, int BN>
+// NW waves per workgroup in a 2 x (NW / 2) arrangement: each wave owns
+// (BM / 2) x (2 BN / NW) of the tile.
+template <int BM, int BN, int NW = 4>
 struct MfmaTile {
-  floatx4 acc[BM / 32][BN / 32];
+  floatx4 acc[BM / 32][BN / (8 * NW)];
 };
 
 // s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding)
@@ -106,19 +109,20 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Per-thread source pointers of one tile's loads: A rows (hi plane; lo at
 // + a_plane) and W rows, each already offset to this lane's 16-byte chunk.
-template <int BM, int BN, bool W8 = false>
+template <int BM, int BN, bool W8 = false, int NW = 4>
 struct TileSrc {
-  const bf16_t* a[BM / 64];
-  const bf16_t* w[W8 ? 1 : BN / 64];
+  const bf16_t* a[BM / (16 * NW)];
+  const bf16_t* w[W8 ? 1 : BN / (16 * NW)];
   const uint8_t* w8[W8 ? W8Load<BN>::loads : 1];
 };
 
-template <int BM, int BN, bool W8>
-__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8>& src, size_t a_plane, int k,
+template <int BM, int BN, bool W8, int NW = 4>
+__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8, NW>& src, size_t a_plane, int k,
                                             GemmStage<BM, BN, W8>& s, int wave) {
+  static_assert(!W8 || NW == 4, "fp8 weights take four waves");
 #pragma unroll
-  for (int i = 0; i < BM / 64; ++i) {
-    const int r = (i * 4 + wave) * 16;
+  for (int i = 0; i < BM / (16 * NW); ++i) {
+    const int r = (i * NW + wave) * 16;
     __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k), (lds_void_t*)(s.ah + r * SK), 16, 0, 0);
     __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k + a_plane), (lds_void_t*)(s.al + r * SK), 16, 0, 0);
   }
@@ -132,20 +136,20 @@ __device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8>& src, size
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < BN / 64; ++i) {
-      const int r = (i * 4 + wave) * 16;
+    for (int i = 0; i < BN / (16 * NW); ++i) {
+      const int r = (i * NW + wave) * 16;
       __builtin_amdgcn_global_load_lds((const void*)(src.w[i] + k), (lds_void_t*)(s.b + r * SK), 16, 0, 0);
     }
   }
 }
 
-// One stage of MFMAs: 4 waves in a 2x2 arrangement, each accumulating a
-// (BM/2)x(BN/2) sub-tile of (BM/32)x(BN/32) MFMA 16x16x32 tiles.
-template <int BM, int BN, bool W8>
-__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaTile<BM, BN>& t, int wave) {
-  constexpr int FM = BM / 32, FN = BN / 32;
+// One stage of MFMAs: NW waves in a 2 x (NW/2) arrangement, each
+// accumulating a (BM/2) x (2BN/NW) sub-tile of MFMA 16x16x32 tiles.
+template <int BM, int BN, bool W8, int NW = 4>
+__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaTile<BM, BN, NW>& t, int wave) {
+  constexpr int FM = BM / 32, FN = BN / (8 * NW), WCOL = 2 * BN / NW;
   const int lane = threadIdx.x & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   const int r16 = lane & 15;
   const int pos = ((lane >> 4) ^ swz(r16)) * 8;   // fragment rows are r16 + 16 j
   u32x4 bfr[FN];
@@ -154,12 +158,12 @@ __device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaT
     const uint8_t* b8 = (const uint8_t*)s.b;
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const uint2 raw = *(const uint2*)(b8 + (wn * (BN / 2) + j * 16 + r16) * SK + (lane >> 4) * 8);
+      const uint2 raw = *(const uint2*)(b8 + (wn * WCOL + j * 16 + r16) * SK + (lane >> 4) * 8);
       bfr[j] = __builtin_bit_cast(u32x4, fp8x8_to_bf16(raw));
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&s.b[(wn * (BN / 2) + j * 16 + r16) * SK + pos]);
+    for (int j = 0; j < FN; ++j) bfr[j] = *(const u32x4*)(&s.b[(wn * WCOL + j * 16 + r16) * SK + pos]);
   }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
@@ -182,22 +186,22 @@ __device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaT
 // are separate LDS objects so the compiler can tell the loads into one stage
 // from the reads of another.  All waves of the workgroup must run the same
 // number of stages (the barriers are workgroup-wide).
-template <int BM, int BN, bool W8 = false>
+template <int BM, int BN, bool W8 = false, int NW = 4>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int lda, size_t a_plane,
                                               const void* __restrict__ Wv, int ldw, int k0,
-                                              int klen, int m0, int n0, MfmaTile<BM, BN>& t,
+                                              int klen, int m0, int n0, MfmaTile<BM, BN, NW>& t,
                                               GemmStage<BM, BN, W8>& s0, GemmStage<BM, BN, W8>& s1,
                                               GemmStage<BM, BN, W8>& s2, GemmStage<BM, BN, W8>& s3,
                                               int wave, const int32_t* __restrict__ arows = nullptr,
                                               int nvalid = 0) {
   // load instructions per thread per stage
-  constexpr int LPS = 2 * (BM / 64) + (W8 ? W8Load<BN>::loads : BN / 64);
+  constexpr int LPS = 2 * (BM / (16 * NW)) + (W8 ? W8Load<BN>::loads : BN / (16 * NW));
   const int lane = threadIdx.x & 63;
   const int rsub = lane >> 2, chunk = (lane & 3) ^ swz(rsub);
-  TileSrc<BM, BN, W8> src;
+  TileSrc<BM, BN, W8, NW> src;
 #pragma unroll
-  for (int i = 0; i < BM / 64; ++i) {
-    const int r = (i * 4 + wave) * 16 + rsub;
+  for (int i = 0; i < BM / (16 * NW); ++i) {
+    const int r = (i * NW + wave) * 16 + rsub;
     const int grow = arows ? arows[r < nvalid ? r : 0] : m0 + r;
     src.a[i] = A + (size_t)grow * lda + k0 + chunk * 8;
   }
@@ -213,18 +217,18 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
   } else {
     const bf16_t* W = (const bf16_t*)Wv;
 #pragma unroll
-    for (int i = 0; i < BN / 64; ++i)
-      src.w[i] = W + (size_t)(n0 + (i * 4 + wave) * 16 + rsub) * ldw + k0 + chunk * 8;
+    for (int i = 0; i < BN / (16 * NW); ++i)
+      src.w[i] = W + (size_t)(n0 + (i * NW + wave) * 16 + rsub) * ldw + k0 + chunk * 8;
   }
 #pragma unroll
   for (int i = 0; i < BM / 32; ++i)
 #pragma unroll
-    for (int j = 0; j < BN / 32; ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < BN / (8 * NW); ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = klen / SK;     // multiple of 4, >= 4
-  stage_issue<BM, BN, W8>(src, a_plane, 0, s0, wave);
-  stage_issue<BM, BN, W8>(src, a_plane, SK, s1, wave);
-  stage_issue<BM, BN, W8>(src, a_plane, 2 * SK, s2, wave);
+  stage_issue<BM, BN, W8, NW>(src, a_plane, 0, s0, wave);
+  stage_issue<BM, BN, W8, NW>(src, a_plane, SK, s1, wave);
+  stage_issue<BM, BN, W8, NW>(src, a_plane, 2 * SK, s2, wave);
   int kt = 0;
   // each step: own loads of stage kt done (the two younger stages may still
   // be in flight), barrier (everyone's loads done, everyone past stage kt-1),
@@ -232,8 +236,8 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
 #define BD_GEMM_STEP(CUR, NXT, KNEXT)                            \
   wait_vmcnt<2 * LPS>();                                         \
   __builtin_amdgcn_s_barrier();                                  \
-  stage_issue<BM, BN, W8>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
-  stage_mfma<BM, BN, W8>(CUR, t, wave);
+  stage_issue<BM, BN, W8, NW>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
+  stage_mfma<BM, BN, W8, NW>(CUR, t, wave);
   for (; kt + 4 < nk; kt += 4) {
     BD_GEMM_STEP(s0, s3, kt + 3)
     BD_GEMM_STEP(s1, s0, kt + 4)
@@ -244,17 +248,17 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
   // the last four stages (kt + 3 == nk - 1)
   wait_vmcnt<2 * LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_issue<BM, BN, W8>(src, a_plane, (kt + 3) * SK, s3, wave);
-  stage_mfma<BM, BN, W8>(s0, t, wave);
+  stage_issue<BM, BN, W8, NW>(src, a_plane, (kt + 3) * SK, s3, wave);
+  stage_mfma<BM, BN, W8, NW>(s0, t, wave);
   wait_vmcnt<2 * LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN, W8>(s1, t, wave);
+  stage_mfma<BM, BN, W8, NW>(s1, t, wave);
   wait_vmcnt<LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN, W8>(s2, t, wave);
+  stage_mfma<BM, BN, W8, NW>(s2, t, wave);
   wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN, W8>(s3, t, wave);
+  stage_mfma<BM, BN, W8, NW>(s3, t, wave);
 }
 
 #define BD_GEMM_SMEM(BM, BN, W8)                                                 \
@@ -285,15 +289,15 @@ __device__ __forceinline__ void scale_columns(MfmaTile<BM, BN>& t, const float* 
 // split stores its raw partial tile to ws[split][row][col] (rows padded to
 // whole tiles) and the next RMSNorm of the residual stream adds the partials
 // in split order.
-template <int BM, int BN, int EPI, bool W8>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
+template <int BM, int BN, int EPI, bool W8, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
                                                    size_t a_plane, const void* __restrict__ W,
                                                    int ldw, int N, int K,
                                                    const int32_t* __restrict__ Mp,
                                                    void* __restrict__ out, int ldo, size_t out_plane,
                                                    float* __restrict__ ws, int zmax,
                                                    const float* __restrict__ wscale) {
-  constexpr int FM = BM / 32, FN = BN / 32;
+  constexpr int FM = BM / 32, FN = BN / (8 * NW), WCOL = 2 * BN / NW;
   const int M = *Mp;
   const int X = N / BN, Y = (M + BM - 1) / BM;
   int S = 1;
@@ -312,11 +316,11 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
   const int klen = K / S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   BD_GEMM_SMEM(BM, BN, W8);
-  MfmaTile<BM, BN> t;
-  mfma_mainloop<BM, BN, W8>(A, lda, a_plane, W, ldw, z * klen, klen, m0, n0, t, gs0, gs1, gs2,
-                            gs3, wave);
+  MfmaTile<BM, BN, NW> t;
+  mfma_mainloop<BM, BN, W8, NW>(A, lda, a_plane, W, ldw, z * klen, klen, m0, n0, t, gs0, gs1, gs2,
+                                gs3, wave);
   if constexpr (W8) scale_columns<BM, BN>(t, wscale, n0, wave);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   float* wz = (EPI == EPI_ADD_F32 && S > 1) ? ws + (size_t)z * ((M + BM - 1) / BM) * BM * N
                                             : nullptr;
 #pragma unroll
@@ -328,7 +332,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
       if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll
         for (int j = 0; j < FN; j += 2) {
-          const int pb = n0 + wn * (BN / 2) + j * 16;    // packed column of the gate group
+          const int pb = n0 + wn * WCOL + j * 16;        // packed column of the gate group
           const int col = (pb >> 5) * 16 + (lane & 15);  // output feature
           const float g = t.acc[i][j][r], u = t.acc[i][j + 1][r];
           store_pair((bf16_t*)out + (size_t)m * ldo + col, out_plane, silu(g) * u);
@@ -336,7 +340,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t* __restrict__ A,
       } else {
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          const int n = n0 + wn * (BN / 2) + j * 16 + (lane & 15);
+          const int n = n0 + wn * WCOL + j * 16 + (lane & 15);
           const float v = t.acc[i][j][r];
           if (EPI == EPI_ADD_F32 && S > 1) wz[(size_t)m * N + n] = v;
           else if (EPI == EPI_ADD_F32) ((float*)out)[(size_t)m * ldo + n] += v;
@@ -750,31 +754,34 @@ __global__ __launch_bounds__(256) void k_lm_merge(const float* __restrict__ pmax
 
 // ------------------------------------------------------------------ launchers
 
-template <int BM, int BN, bool W8>
+template <int BM, int BN, bool W8, int NW = 4>
 static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const void* w,
                             int ldw, int N, int K, const int32_t* M_dev, void* o, int ldo, size_t op,
                             float* ws, int zmax, const float* wscale, hipStream_t st) {
   switch (epi) {
     case EPI_ADD_F32:
-      k_gemm_bf16<BM, BN, EPI_ADD_F32, W8><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws,
+      k_gemm_bf16<BM, BN, EPI_ADD_F32, W8, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws,
                                                                  zmax, wscale);
       break;
     case EPI_SWIGLU:
-      k_gemm_bf16<BM, BN, EPI_SWIGLU, W8><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
+      k_gemm_bf16<BM, BN, EPI_SWIGLU, W8, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
                                                                 nullptr, 1, wscale);
       break;
     default:
-      k_gemm_bf16<BM, BN, EPI_STORE_F32, W8><<<grid, 256, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
+      k_gemm_bf16<BM, BN, EPI_STORE_F32, W8, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
                                                                    nullptr, 1, wscale);
       break;
   }
 }
 
 // Tile choice: 128x256 (each wave 64 x 128: a third fewer LDS bytes per MFMA
-// than 64 x 64 waves, 128 KB of LDS) for products at least 2048 wide over
-// windows of at least 2048 rows, when the caller allows it (bf16 weights and
-// a kernel instantiated for it): on 3328-row products it ran gate/up
-// (N 16384) in 494 us against 550, down (N 2048, K 8192) in 259 against 291.
+// than 64 x 64 waves, 128 KB of LDS) over windows of at least 2048 rows for
+// wide plain products (N >= 8192) and deep residual ones (K >= 4096), when the
+// caller allows it (bf16 weights and a kernel instantiated for it): on
+// 3328-row products it ran gate/up (N 16384) in 494 us against 550 and down
+// (N 2048, K 8192) in 259 against 291; a shallower residual product over
+// fewer live rows (the MoE O projection, K 2048, about 2300 rows) ran slower
+// in it (37 us against 30), its grid leaving half the chip idle.
 // Otherwise 128x128 when that tiling gives enough workgroups over the row
 // capacity (the 64x64 tile runs out of LDS bandwidth on large products),
 // else 64x64.  Enough: 1024 for plain products (below that the 128x128 grid
@@ -784,9 +791,9 @@ static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t
 // with the tile count (the multi-block O projection ran 18% slower in 64x64
 // tiles).  zmax: the largest residual split (1 = none).
 GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid, bool wide_ok) {
-  (void)K;
   if (!is_bf16) return GemmPlan{64, 64, 1};
-  if (wide_ok && N % 256 == 0 && N >= 2048 && rows_cap >= 2048) return GemmPlan{128, 256, 1};
+  if (wide_ok && N % 256 == 0 && rows_cap >= 2048 && (N >= 8192 || (resid && K >= 4096)))
+    return GemmPlan{128, 256, 1};
   if (N % 128 == 0 && (N / 128) * cdiv(rows_cap, 128) >= (resid ? 512 : 1024)) return GemmPlan{128, 128, 1};
   return GemmPlan{64, 64, 1};
 }
@@ -811,7 +818,8 @@ hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int ld
   if (wscale) {
     if (big) BD_CFG(128, 128, true); else BD_CFG(64, 64, true);
   } else {
-    if (wide) BD_CFG(128, 256, false);
+    if (wide) launch_bf16_cfg<128, 256, false, 8>(epi, grid, a, lda, a_plane, W, ldw, N, K, M_dev, out, ldo,
+                                                   out_plane, ws, p.zmax, wscale, st);
     else if (big) BD_CFG(128, 128, false);
     else BD_CFG(64, 64, false);
   }
