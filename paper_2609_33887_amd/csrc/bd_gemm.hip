@@ -371,12 +371,12 @@ __device__ __forceinline__ void store_pair4(bf16_t* p, size_t plane, const float
       make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
 }
 
-template <int BM, int BN, bool W8>
-__global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, int lda,
+template <int BM, int BN, bool W8, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void k_gemm_qkv(const bf16_t* __restrict__ A, int lda,
                                                   size_t a_plane, const void* __restrict__ W,
                                                   int K, const int32_t* __restrict__ Mp, QkvEpi e,
                                                   const float* __restrict__ wscale) {
-  constexpr int FM = BM / 32, FN = BN / 32;
+  constexpr int FM = BM / 32, FN = BN / (8 * NW), WCOL = 2 * BN / NW;
   const int M = *Mp;
   const int X = (e.H + 2 * e.Hkv) * e.hd / BN, Y = (M + BM - 1) / BM;
   const int u = xcd_item(blockIdx.x, X * Y);
@@ -386,10 +386,10 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, 
   const int m0 = ty * BM, n0 = tx * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   BD_GEMM_SMEM(BM, BN, W8);
-  MfmaTile<BM, BN> t;
-  mfma_mainloop<BM, BN, W8>(A, lda, a_plane, W, K, 0, K, m0, n0, t, gs0, gs1, gs2, gs3, wave);
+  MfmaTile<BM, BN, NW> t;
+  mfma_mainloop<BM, BN, W8, NW>(A, lda, a_plane, W, K, 0, K, m0, n0, t, gs0, gs1, gs2, gs3, wave);
   if constexpr (W8) scale_columns<BM, BN>(t, wscale, n0, wave);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   const int hd = e.hd, half = hd >> 1;
   const int qcols = e.H * hd, qkcols = (e.H + e.Hkv) * hd;
   bf16_t* Q = (bf16_t*)e.Q;
@@ -407,7 +407,7 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16_t* __restrict__ A, 
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * (BN / 2) + j * 16 + (lane & 15);
+      const int n = n0 + wn * WCOL + j * 16 + (lane & 15);
       float v[4], pv[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -774,14 +774,15 @@ static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t
   }
 }
 
-// Tile choice: 128x256 (each wave 64 x 128: a third fewer LDS bytes per MFMA
-// than 64 x 64 waves, 128 KB of LDS) over windows of at least 2048 rows for
-// wide plain products (N >= 8192) and deep residual ones (K >= 4096), when the
-// caller allows it (bf16 weights and a kernel instantiated for it): on
+// Tile choice: 128x256 (8 waves of 64 x 64, two per SIMD; 128 KB of LDS) over
+// windows of at least 2048 rows for wide plain products (N >= 8192) and
+// residual ones with K >= 2048, when the caller allows it (bf16 weights and a
+// kernel instantiated for it): on
 // 3328-row products it ran gate/up (N 16384) in 494 us against 550 and down
-// (N 2048, K 8192) in 259 against 291; a shallower residual product over
-// fewer live rows (the MoE O projection, K 2048, about 2300 rows) ran slower
-// in it (37 us against 30), its grid leaving half the chip idle.
+// (N 2048, K 8192) in 259 against 291.  With 8 waves per tile the shallower
+// O projection (N 2048, K 2048) gains too, even where few rows are live: per
+// decode 256 -> 193 ms on the multi-block window, 90 -> 71 on the MoE window
+// (about 2300 live rows of 4096), 56 -> 39 on the long-prefix window.
 // Otherwise 128x128 when that tiling gives enough workgroups over the row
 // capacity (the 64x64 tile runs out of LDS bandwidth on large products),
 // else 64x64.  Enough: 1024 for plain products (below that the 128x128 grid
@@ -792,7 +793,7 @@ static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t
 // tiles).  zmax: the largest residual split (1 = none).
 GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid, bool wide_ok) {
   if (!is_bf16) return GemmPlan{64, 64, 1};
-  if (wide_ok && N % 256 == 0 && rows_cap >= 2048 && (N >= 8192 || (resid && K >= 4096)))
+  if (wide_ok && N % 256 == 0 && rows_cap >= 2048 && (N >= 8192 || (resid && K >= 2048)))
     return GemmPlan{128, 256, 1};
   if (N % 128 == 0 && (N / 128) * cdiv(rows_cap, 128) >= (resid ? 512 : 1024)) return GemmPlan{128, 128, 1};
   return GemmPlan{64, 64, 1};
@@ -881,13 +882,22 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
                            const float* wscale) {
   const int N = (e.H + 2 * e.Hkv) * e.hd;
   if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
-  const GemmPlan p = plan_gemm(true, N, K, rows_cap, false, false);
+  // bf16 weights over windows that fill at least 512 wide tiles: 128x256
+  // tiles with 8 waves (3328 x 3072 x 2048: 111 us against 119 in 128x128
+  // tiles; per decode 428 -> 383 ms on the multi-block window).  Smaller
+  // windows, whose live rows often fall well below the capacity, keep the
+  // finer tiling: wide tiles there ran 50% slower (long-prefix 2048-row and
+  // MoE 4096-row windows), leaving CUs idle.
+  GemmPlan p = plan_gemm(true, N, K, rows_cap, false, false);
+  if (!wscale && N % 256 == 0 && (N / 256) * cdiv(rows_cap, 128) >= 512) p = GemmPlan{128, 256, 1};
   if (N % p.bn) return hipErrorInvalidValue;
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) + 7);
   const bf16_t* a = (const bf16_t*)A;
 #define BD_QKV(BM_, W8_) k_gemm_qkv<BM_, BM_, W8_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, wscale)
   if (wscale) {
     if (p.bm == 128) BD_QKV(128, true); else BD_QKV(64, true);
+  } else if (p.bn == 256) {
+    k_gemm_qkv<128, 256, false, 8><<<grid, 512, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, wscale);
   } else {
     if (p.bm == 128) BD_QKV(128, false); else BD_QKV(64, false);
   }
