@@ -35,6 +35,17 @@ __device__ __forceinline__ bf16_t f2bf_a(float f) {
 
 constexpr int AK = 64;    // keys per tile
 
+typedef __bf16 bf16x2_a __attribute__((ext_vector_type(2)));
+typedef float floatx2_a __attribute__((ext_vector_type(2)));
+
+// (x0, x1) -> the hi bf16 pair (round to nearest even, one v_cvt_pk_bf16_f32)
+// in hi and the lo pair, the rounded remainders x - hi (exact in fp32), in lo
+__device__ __forceinline__ void split_pair2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  hi = __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_a){x0, x1}, bf16x2_a));
+  const float h0 = __uint_as_float(hi << 16), h1 = __uint_as_float(hi & 0xFFFF0000u);
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_a){x0 - h0, x1 - h1}, bf16x2_a));
+}
+
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict__ Q, size_t q_plane,
                                                    const bf16_t* __restrict__ Kc, size_t k_plane,
@@ -92,6 +103,11 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict_
   const int qrow = row_start + (qvalid ? qi / G : 0);        // its row in the step
   const int h = kv * G + (qvalid ? qi % G : 0);              // its q-head
   const int qend = ((win_start + (qvalid ? qi / G : 0)) / B + 1) * B;   // its key bound
+  // the wave's smallest key bound (query index and bound rise together) and
+  // whether every lane holds a query: tiles below the bound skip the mask
+  const int q0w = qt * AQ + wave * 16;
+  const int qend_w = ((win_start + min(q0w, QG - 1) / G) / B + 1) * B;
+  const bool full_w = q0w + 16 <= QG;
 
   // Q^T fragments (B operand of S^T = K Q^T): dims [32 kc + 8 g, +8) of query c,
   // hi and lo halves.
@@ -113,22 +129,20 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict_
   float m_run = -INFINITY, l_part = 0.f;
 
   // register prefetch of the next K/V tile (both planes) overlaps the loads
-  // with the MFMAs of the current tile.  K: chunk ci = (key, 8 dims), keys
-  // >= kend read as zero.  V^T: chunk ci = (dim, 8 keys); a tile never
-  // reaches past vstride and the keys past kend there are finite cache
-  // contents that meet zero probabilities.
+  // with the MFMAs of the current tile.  K: chunk ci = (key, 8 dims); keys
+  // >= kend (past the slice's written rows, possibly past the slice) read
+  // row kend - 1 instead, whose finite score every query masks.  V^T: chunk
+  // ci = (dim, 8 keys); a tile never reaches past vstride and the keys past
+  // kend there are finite cache contents that meet zero probabilities.
   u32x4 pkh[NCH], pkl[NCH], pvh[NCH], pvl[NCH];
 #define BD_FETCH(K0)                                                            \
   do {                                                                          \
     _Pragma("unroll") for (int it = 0; it < NCH; ++it) {                        \
       const int ci = tid + NT * it;                                             \
       const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;                  \
-      pkh[it] = pkl[it] = u32x4{0u, 0u, 0u, 0u};                                \
-      if ((K0) + key < kend) {                                                  \
-        const size_t o = (size_t)((K0) + key) * HD + dc;                        \
-        pkh[it] = *(const u32x4*)(Kp + o);                                      \
-        pkl[it] = *(const u32x4*)(Kp + o + k_plane);                            \
-      }                                                                         \
+      const size_t o = (size_t)min((K0) + key, kend - 1) * HD + dc;             \
+      pkh[it] = *(const u32x4*)(Kp + o);                                        \
+      pkl[it] = *(const u32x4*)(Kp + o + k_plane);                              \
       const int dim = ci / (AK / 8), kc8 = (ci % (AK / 8)) * 8;                 \
       const size_t ov = vt_row((K0), dim, HD) + kc8;                            \
       pvh[it] = *(const u32x4*)(Vp + ov);                                       \
@@ -171,42 +185,56 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict_
       for (int r = 0; r < 4; ++r) sv[st][r] = a[r];
     }
     // In this lane, score (st, r) belongs to key k0 + st*16 + 4g + r of query c.
-    const bool need_mask = (k0 + AK > qend) || !qvalid;
+    // Scores stay unscaled until the exponent: the max of the raw scores
+    // times the (positive) scale is the max of the scaled ones.  The mask
+    // branch is wave-uniform.
+    if (k0 + AK > qend_w || !full_w) {
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = k0 + st * 16 + 4 * g + r;
+          if (!qvalid || key >= qend) sv[st][r] = -INFINITY;
+        }
+    }
     float tmax = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float x = sv[st][r] * scale_log2;
-        if (need_mask) {
-          const int key = k0 + st * 16 + 4 * g + r;
-          if (!qvalid || key >= qend) x = -INFINITY;
-        }
-        sv[st][r] = x;
-        tmax = fmaxf(tmax, x);
-      }
+      for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, sv[st][r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float m_new = fmaxf(m_run, tmax);
+    const float m_new = fmaxf(m_run, tmax * scale_log2);
     const float m_ref = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_ref);
-    m_run = m_new;
-    l_part *= alpha;
+    // rescale only when some lane's running max moved (alpha = 1 elsewhere);
+    // v_exp_f32 is exp2 without the denormal-range scaling: terms below
+    // 2^-126 of the row max contribute nothing at fp32 precision anyway
+    if (__any(m_new != m_run)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+      l_part *= alpha;
 #pragma unroll
-    for (int t = 0; t < HD / 16; ++t) oacc[t] *= alpha;
-    // P^T as a hi/lo bf16 pair
-    bf16x8 ph[2], pl[2];
+      for (int t = 0; t < HD / 16; ++t) oacc[t] *= alpha;
+    }
+    m_run = m_new;
+    // P^T as a hi/lo bf16 pair: keys 4g + r of sub-tile st take slots
+    // (st & 1) * 4 + r of chunk st >> 1, two slots per 32-bit word
+    uint32_t hw[4][2], lw[4][2];
 #pragma unroll
     for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(sv[st][r] - m_ref);
-        l_part += p;
-        const bf16_t hb = f2bf_a(p);
-        const bf16_t lb = f2bf_a(p - bf2f_a(hb));
-        ph[st >> 1][(st & 1) * 4 + r] = __builtin_bit_cast(__bf16, hb);
-        pl[st >> 1][(st & 1) * 4 + r] = __builtin_bit_cast(__bf16, lb);
+      for (int r2 = 0; r2 < 2; ++r2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[st][2 * r2], scale_log2, -m_ref));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[st][2 * r2 + 1], scale_log2, -m_ref));
+        l_part += p0;
+        l_part += p1;
+        split_pair2(p0, p1, hw[st][r2], lw[st][r2]);
       }
+    bf16x8 ph[2], pl[2];
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      ph[kc] = __builtin_bit_cast(bf16x8, u32x4{hw[2 * kc][0], hw[2 * kc][1], hw[2 * kc + 1][0], hw[2 * kc + 1][1]});
+      pl[kc] = __builtin_bit_cast(bf16x8, u32x4{lw[2 * kc][0], lw[2 * kc][1], lw[2 * kc + 1][0], lw[2 * kc + 1][1]});
+    }
     // O^T += V^T P^T over 2 chunks of 32 keys; k-slot 8g+r <-> key 32kc+4g+r,
     // k-slot 8g+4+r <-> key 32kc+16+4g+r (same permutation as the scores),
     // which the V^T slot order (vt_slot) stores as slots 32kc+8g..+7: one
