@@ -50,7 +50,7 @@ struct LayerW {
   void* w_gu;           // dense: packed gate/up (library-owned)
   const void* w_down;
   // MoE
-  float* wr_t;          // router weights transposed [d][E] (library-owned)
+  const float* wr;      // router weights [E][d] (the caller's)
   void* w_gu_e;         // packed gate/up per expert [E][2 Fe][d] (library-owned)
   const void* w_down_e; // [E][d][Fe]
   void* w_gu_s;         // packed shared-expert gate/up [2 Fs][d] (library-owned)
@@ -338,11 +338,8 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
       const void* gate_s = w[t++];
       const void* up_s = w[t++];
       L.w_down_s = w[t++];
-      L.wr_t = (float*)owned_alloc((size_t)E * c.d_model * sizeof(float));
-      if (!L.wr_t) r = fail(BD_ENOMEM, "hipMalloc for the router failed");
-      else if (launch_transpose_f32(router, L.wr_t, E, c.d_model, m->stream) != hipSuccess)
-        r = fail(BD_EHIP, "router transpose failed");
-      if (r == BD_OK) {
+      L.wr = router;
+      {
         L.w_gu_e = owned_alloc((size_t)E * 2 * Fe * row_bytes);
         if (!L.w_gu_e) r = fail(BD_ENOMEM, "hipMalloc for packed experts failed");
         for (int e = 0; e < E && r == BD_OK; ++e) {
@@ -435,7 +432,7 @@ static bd_status run_moe(bd_model* m, bd_state* s, const LayerW& L, const PlanVi
     LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, true, s->Hact, Fs, s->pl_H, L.w_down_s, Fs, d,
                                           Fs, plan.hdr, rows_cap, s->X, d, 0, st, L.s_down_s));
   }
-  LAUNCH(BD_PROF_MOE, launch_router(s->A, s->pl_A, d, L.wr_t, E, k, plan.hdr, rows_cap, s->top_e,
+  LAUNCH(BD_PROF_MOE, launch_router(s->A, s->pl_A, d, L.wr, E, k, plan.hdr, rows_cap, s->top_e,
                                     s->top_w, st));
   LAUNCH(BD_PROF_MOE, launch_moe_dispatch(s->top_e, k, E, plan.hdr, s->moe, st));
   GroupTiles g;

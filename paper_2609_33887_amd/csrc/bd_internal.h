@@ -126,9 +126,9 @@ hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, 
                                int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
                                int ldo, size_t out_plane, const float* wscale, hipStream_t st);
 
-// MoE routing: softmax over E router logits (fp32 weights, transposed
-// [d][E]), top_k experts (lowest id among equals), weights renormalised.
-hipError_t launch_router(const void* A, size_t a_plane, int d, const float* WrT, int E, int topk,
+// MoE routing: softmax over E router logits (fp32 weights [E][d]), top_k
+// experts (lowest id among equals), weights renormalised.
+hipError_t launch_router(const void* A, size_t a_plane, int d, const float* Wr, int E, int topk,
                          const int32_t* M_dev, int rows_cap, int32_t* top_e, float* top_w,
                          hipStream_t st);
 // Deterministic dispatch: expert-sorted assignment lists (token rows ascending
@@ -147,7 +147,6 @@ hipError_t launch_moe_dispatch(const int32_t* top_e, int topk, int E, const int3
 // X[row] += sum_j top_w[row][j] * Y[pos_of[row][j]] (fixed slot order).
 hipError_t launch_moe_combine(float* X, const float* Y, const int32_t* pos_of, const float* top_w,
                               int topk, int d, const int32_t* M_dev, int rows_cap, hipStream_t st);
-hipError_t launch_transpose_f32(const float* in, float* out, int rows, int cols, hipStream_t st);
 
 struct GemmPlan {
   int bm, bn, zmax;        // tile; largest residual K-split (1 = none)

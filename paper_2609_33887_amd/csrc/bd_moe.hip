@@ -9,83 +9,73 @@ namespace bd {
 
 __device__ __forceinline__ float bf2f_e(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// Router.  A workgroup takes 16 rows: thread t accumulates the logits of
-// experts 4 (t % 16) + [0, 4) of row t / 16 over d in chunks of RC = 128,
-// the row's activation pair (hi + lo, summed in fp32) and the transposed fp32
-// router weights staged in LDS (the weights are read once per workgroup, not
-// once per row; the next chunk's loads are in flight, in registers, while
-// the current chunk is computed); every logit is the FMA chain over
-// k = 0 .. d-1 in order.  Then one wave per row: softmax over the E lanes,
-// top_k selection by repeated wave argmax (lowest expert id among equal
+// Router.  A workgroup takes 16 rows and wave w the logits of experts
+// 16 w .. 16 w + 15 on the fp32 matrix cores (v_mfma_f32_16x16x4_f32: fp32
+// operands, fp32 accumulation): the A operand is the row's activation pair
+// summed in fp32 (hi + lo), the B operand the fp32 router weights [E][d]
+// read straight from global memory (one 64-byte run per lane and block; the
+// next block's loads are in flight while the current one is multiplied).
+// In MFMA step s of the 64-deep block at k0, lane group g feeds depth
+// k0 + 16 g + s; four accumulators take the steps s mod 4 and are summed at
+// the end (an fp32 sum of the same products in another order than the plain
+// dot product).  Then one wave per row: softmax over the E lanes, top_k
+// selection by repeated wave argmax (lowest expert id among equal
 // probabilities), and weights renormalised over the chosen experts.
-// Needs E <= 64 and d % 128 == 0.
+// Needs E <= 64 and d % 64 == 0.
 constexpr int RR = 16;     // rows per workgroup
-constexpr int RC = 128;    // k per LDS chunk
+constexpr int RKB = 64;    // depth per block
 __global__ __launch_bounds__(256) void k_router(const bf16_t* __restrict__ A, size_t a_plane, int d,
-                                                const float* __restrict__ WrT, int E, int topk,
+                                                const float* __restrict__ Wr, int E, int topk,
                                                 const int32_t* __restrict__ Mp,
                                                 int32_t* __restrict__ top_e, float* __restrict__ top_w) {
-  __shared__ float sA[RR][RC + 4];
-  __shared__ __attribute__((aligned(16))) float sW[RC][64];
   __shared__ float sL[RR][65];
   const int M = *Mp;
   const int row0 = blockIdx.x * RR;
   if (row0 >= M) return;
-  const int t = threadIdx.x;
-  const int r = t / 16, e0 = (t % 16) * 4;
-  // staging assignment: A -- row t / 16, k = 8 (t % 16) + [0, 8) (one 16-byte
-  // load per plane); W -- float4 i of the chunk's RC x 64 block for
-  // i = t + 256 j, j < 8 (k = i / 16, experts 4 (i % 16) + [0, 4))
-  const int ar = t / 16, ak = (t % 16) * 8;
-  const bool arow = row0 + ar < M;
-  const bf16_t* ap = A + (size_t)(arow ? row0 + ar : row0) * d + ak;
-  u32x4 ah, al;
-  float4 wv[8];
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int g = lane >> 4, c = lane & 15;
+  const bool rv = row0 + c < M;               // this lane's A row is live
+  const int e = wave * 16 + c;
+  const bool ev = e < E;                      // this lane's expert exists
+  const bf16_t* ap = A + (size_t)(rv ? row0 + c : row0) * d + 16 * g;
+  const float* wp = Wr + (size_t)(ev ? e : 0) * d + 16 * g;
+  u32x4 ah[2], al[2];
+  float4 wv[4];
   auto fetch = [&](int k0) {
-    ah = *(const u32x4*)(ap + k0);
-    al = *(const u32x4*)(ap + k0 + a_plane);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int i = t + 256 * j, kk = i / 16, e = (i % 16) * 4;
-      if (E == 64) {
-        wv[j] = *(const float4*)(WrT + (size_t)(k0 + kk) * 64 + e);
-      } else {
-        float v[4];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) v[x] = e + x < E ? WrT[(size_t)(k0 + kk) * E + e + x] : 0.f;
-        wv[j] = make_float4(v[0], v[1], v[2], v[3]);
-      }
+    for (int x = 0; x < 2; ++x) {
+      ah[x] = *(const u32x4*)(ap + k0 + 8 * x);
+      al[x] = *(const u32x4*)(ap + k0 + 8 * x + a_plane);
     }
+#pragma unroll
+    for (int x = 0; x < 4; ++x) wv[x] = *(const float4*)(wp + k0 + 4 * x);
   };
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  floatx4 acc[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
   fetch(0);
-  for (int k0 = 0; k0 < d; k0 += RC) {
-    const bf16_t* h = (const bf16_t*)&ah;
-    const bf16_t* l = (const bf16_t*)&al;
+  for (int k0 = 0; k0 < d; k0 += RKB) {
+    float a[16], w[16];
+    const bf16_t* h = (const bf16_t*)ah;
+    const bf16_t* l = (const bf16_t*)al;
 #pragma unroll
-    for (int x = 0; x < 8; ++x) sA[ar][ak + x] = arow ? bf2f_e(h[x]) + bf2f_e(l[x]) : 0.f;
+    for (int x = 0; x < 16; ++x) a[x] = rv ? bf2f_e(h[x]) + bf2f_e(l[x]) : 0.f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int i = t + 256 * j;
-      *(float4*)&sW[i / 16][(i % 16) * 4] = wv[j];
+    for (int x = 0; x < 4; ++x) {
+      w[4 * x] = ev ? wv[x].x : 0.f;
+      w[4 * x + 1] = ev ? wv[x].y : 0.f;
+      w[4 * x + 2] = ev ? wv[x].z : 0.f;
+      w[4 * x + 3] = ev ? wv[x].w : 0.f;
     }
-    __syncthreads();
-    if (k0 + RC < d) fetch(k0 + RC);
-#pragma unroll 8
-    for (int kk = 0; kk < RC; ++kk) {
-      const float a = sA[r][kk];
-      const float4 w = *(const float4*)&sW[kk][e0];
-      acc[0] = fmaf(a, w.x, acc[0]);
-      acc[1] = fmaf(a, w.y, acc[1]);
-      acc[2] = fmaf(a, w.z, acc[2]);
-      acc[3] = fmaf(a, w.w, acc[3]);
-    }
-    __syncthreads();
+    if (k0 + RKB < d) fetch(k0 + RKB);
+#pragma unroll
+    for (int s2 = 0; s2 < 16; ++s2)
+      acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s2], w[s2], acc[s2 & 3], 0, 0, 0);
   }
+  // lane (g, c) holds the logits of rows 4 g + i, expert 16 wave + c
 #pragma unroll
-  for (int j = 0; j < 4; ++j) sL[r][e0 + j] = acc[j];
+  for (int i = 0; i < 4; ++i) sL[4 * g + i][e] = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
   __syncthreads();
-  const int wave = t >> 6, lane = t & 63;
   for (int rr = wave; rr < RR; rr += 4) {
     const int row = row0 + rr;
     if (row >= M) break;
@@ -119,11 +109,11 @@ __global__ __launch_bounds__(256) void k_router(const bf16_t* __restrict__ A, si
   }
 }
 
-hipError_t launch_router(const void* A, size_t a_plane, int d, const float* WrT, int E, int topk,
+hipError_t launch_router(const void* A, size_t a_plane, int d, const float* Wr, int E, int topk,
                          const int32_t* M_dev, int rows_cap, int32_t* top_e, float* top_w,
                          hipStream_t st) {
-  if (E > 64 || topk > E || topk < 1 || d % RC) return hipErrorInvalidValue;
-  k_router<<<(rows_cap + RR - 1) / RR, 256, 0, st>>>((const bf16_t*)A, a_plane, d, WrT, E, topk, M_dev,
+  if (E > 64 || topk > E || topk < 1 || d % RKB) return hipErrorInvalidValue;
+  k_router<<<(rows_cap + RR - 1) / RR, 256, 0, st>>>((const bf16_t*)A, a_plane, d, Wr, E, topk, M_dev,
                                                      top_e, top_w);
   return hipGetLastError();
 }
@@ -215,20 +205,6 @@ hipError_t launch_moe_combine(float* X, const float* Y, const int32_t* pos_of, c
                               int topk, int d, const int32_t* M_dev, int rows_cap, hipStream_t st) {
   if (d % 4) return hipErrorInvalidValue;
   k_moe_combine<<<dim3((d / 4 + 255) / 256, rows_cap), 256, 0, st>>>(X, Y, pos_of, top_w, topk, d, M_dev);
-  return hipGetLastError();
-}
-
-__global__ void k_transpose_f32(const float* __restrict__ in, float* __restrict__ out, int rows,
-                                int cols) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (size_t)rows * cols) return;
-  const int r = (int)(i / cols), c = (int)(i % cols);
-  out[(size_t)c * rows + r] = in[i];
-}
-
-hipError_t launch_transpose_f32(const float* in, float* out, int rows, int cols, hipStream_t st) {
-  const size_t n = (size_t)rows * cols;
-  k_transpose_f32<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(in, out, rows, cols);
   return hipGetLastError();
 }
 
