@@ -139,7 +139,9 @@ typedef struct bd_state bd_state;
  *  BD_WQ_* value),
  *  BD_EUNSUPPORTED (MoE or BD_WQ_FP8 with the f32 dtype; shapes off the GEMM tiles: with
  *  bf16 every projection's output and input widths -- (H + 2 Hkv) hd, d,
- *  H hd, vocab, 2 ffn or 2 Fe, ffn or Fe -- must be multiples of 128),
+ *  H hd, vocab, 2 ffn or 2 Fe, ffn or Fe -- must be multiples of 128; an
+ *  MoE model's d_model a multiple of 256, for its router's four depth
+ *  quarters of 64-deep blocks),
  *  BD_ENOMEM, BD_EHIP.
  */
 bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev, int32_t n_weights,

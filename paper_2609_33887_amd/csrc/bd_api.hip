@@ -263,8 +263,8 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
     if (!bf16) return fail(BD_EUNSUPPORTED, "MoE layers need the bf16 dtype");
     if (c.n_experts > 64 || c.top_k < 1 || c.top_k > c.n_experts || c.expert_ffn < 1 || c.n_shared < 0)
       return fail(BD_EINVAL, "need 1 <= top_k <= n_experts <= 64, expert_ffn >= 1, n_shared >= 0");
-    if (c.expert_ffn % 128 || c.d_model % 128)
-      return fail(BD_EUNSUPPORTED, "expert_ffn and d_model must be multiples of 128");
+    if (c.expert_ffn % 128 || c.d_model % 256)
+      return fail(BD_EUNSUPPORTED, "MoE needs expert_ffn a multiple of 128 and d_model of 256");
   } else if (c.ffn_dim < 16 || c.ffn_dim % 16) {
     return fail(BD_EINVAL, "ffn_dim must be a positive multiple of 16");
   }

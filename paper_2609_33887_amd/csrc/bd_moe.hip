@@ -9,36 +9,40 @@ namespace bd {
 
 __device__ __forceinline__ float bf2f_e(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// Router.  A workgroup takes 16 rows and wave w the logits of experts
-// 16 w .. 16 w + 15 on the fp32 matrix cores (v_mfma_f32_16x16x4_f32: fp32
-// operands, fp32 accumulation): the A operand is the row's activation pair
-// summed in fp32 (hi + lo), the B operand the fp32 router weights [E][d]
-// read straight from global memory (one 64-byte run per lane and block; the
-// next block's loads are in flight while the current one is multiplied).
-// In MFMA step s of the 64-deep block at k0, lane group g feeds depth
-// k0 + 16 g + s; four accumulators take the steps s mod 4 and are summed at
-// the end (an fp32 sum of the same products in another order than the plain
-// dot product).  Then one wave per row: softmax over the E lanes, top_k
-// selection by repeated wave argmax (lowest expert id among equal
-// probabilities), and weights renormalised over the chosen experts.
-// Needs E <= 64 and d % 64 == 0.
-constexpr int RR = 16;     // rows per workgroup
+// Router.  A workgroup takes 16 rows with 16 waves: wave (q, w) multiplies
+// depth quarter q of the logits of experts 16 w .. 16 w + 15 on the fp32
+// matrix cores (v_mfma_f32_16x16x4_f32: fp32 operands, fp32 accumulation):
+// the A operand is the row's activation pair summed in fp32 (hi + lo), the
+// B operand the fp32 router weights [E][d] read straight from global memory
+// (one 64-byte run per lane and block; the next block's loads are in flight
+// while the current one is multiplied, and the workgroup's 16 waves cover
+// each other's load latency).  In MFMA step s of the 64-deep block at k0, lane group g feeds
+// depth k0 + 16 g + s; four accumulators take the steps s mod 4; the four
+// quarters are summed in LDS in a fixed order (an fp32 sum of the same
+// products in another order than the plain dot product).  Then one wave per
+// row: softmax over the E lanes, top_k selection by repeated wave argmax
+// (lowest expert id among equal probabilities), and weights renormalised
+// over the chosen experts.  Needs E <= 64 and d % 256 == 0.
+constexpr int RR = 16;     // rows per workgroup (one per wave in the tail)
 constexpr int RKB = 64;    // depth per block
-__global__ __launch_bounds__(256) void k_router(const bf16_t* __restrict__ A, size_t a_plane, int d,
-                                                const float* __restrict__ Wr, int E, int topk,
-                                                const int32_t* __restrict__ Mp,
-                                                int32_t* __restrict__ top_e, float* __restrict__ top_w) {
-  __shared__ float sL[RR][65];
+constexpr int RQ = 4;      // depth quarters
+__global__ __launch_bounds__(1024) void k_router(const bf16_t* __restrict__ A, size_t a_plane, int d,
+                                                 const float* __restrict__ Wr, int E, int topk,
+                                                 const int32_t* __restrict__ Mp,
+                                                 int32_t* __restrict__ top_e, float* __restrict__ top_w) {
+  __shared__ float sP[RQ][RR][65];
   const int M = *Mp;
   const int row0 = blockIdx.x * RR;
   if (row0 >= M) return;
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int wq = wave >> 2, we = wave & 3;
   const int g = lane >> 4, c = lane & 15;
   const bool rv = row0 + c < M;               // this lane's A row is live
-  const int e = wave * 16 + c;
+  const int e = we * 16 + c;
   const bool ev = e < E;                      // this lane's expert exists
-  const bf16_t* ap = A + (size_t)(rv ? row0 + c : row0) * d + 16 * g;
-  const float* wp = Wr + (size_t)(ev ? e : 0) * d + 16 * g;
+  const int kq = d / RQ, kbeg = wq * kq;
+  const bf16_t* ap = A + (size_t)(rv ? row0 + c : row0) * d + kbeg + 16 * g;
+  const float* wp = Wr + (size_t)(ev ? e : 0) * d + kbeg + 16 * g;
   u32x4 ah[2], al[2];
   float4 wv[4];
   auto fetch = [&](int k0) {
@@ -54,7 +58,7 @@ __global__ __launch_bounds__(256) void k_router(const bf16_t* __restrict__ A, si
 #pragma unroll
   for (int q = 0; q < 4; ++q) acc[q] = floatx4{0.f, 0.f, 0.f, 0.f};
   fetch(0);
-  for (int k0 = 0; k0 < d; k0 += RKB) {
+  for (int k0 = 0; k0 < kq; k0 += RKB) {
     float a[16], w[16];
     const bf16_t* h = (const bf16_t*)ah;
     const bf16_t* l = (const bf16_t*)al;
@@ -67,19 +71,20 @@ __global__ __launch_bounds__(256) void k_router(const bf16_t* __restrict__ A, si
       w[4 * x + 2] = ev ? wv[x].z : 0.f;
       w[4 * x + 3] = ev ? wv[x].w : 0.f;
     }
-    if (k0 + RKB < d) fetch(k0 + RKB);
+    if (k0 + RKB < kq) fetch(k0 + RKB);
 #pragma unroll
     for (int s2 = 0; s2 < 16; ++s2)
       acc[s2 & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s2], w[s2], acc[s2 & 3], 0, 0, 0);
   }
-  // lane (g, c) holds the logits of rows 4 g + i, expert 16 wave + c
+  // lane (g, c) holds quarter wq of the logits of rows 4 g + i, expert e
 #pragma unroll
-  for (int i = 0; i < 4; ++i) sL[4 * g + i][e] = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
+  for (int i = 0; i < 4; ++i) sP[wq][4 * g + i][e] = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
   __syncthreads();
-  for (int rr = wave; rr < RR; rr += 4) {
+  {
+    const int rr = wave;
     const int row = row0 + rr;
-    if (row >= M) break;
-    const float lg = sL[rr][lane];
+    if (row >= M) return;
+    const float lg = (sP[0][rr][lane] + sP[1][rr][lane]) + (sP[2][rr][lane] + sP[3][rr][lane]);
     float mx = lane < E ? lg : -INFINITY;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
@@ -112,8 +117,8 @@ __global__ __launch_bounds__(256) void k_router(const bf16_t* __restrict__ A, si
 hipError_t launch_router(const void* A, size_t a_plane, int d, const float* Wr, int E, int topk,
                          const int32_t* M_dev, int rows_cap, int32_t* top_e, float* top_w,
                          hipStream_t st) {
-  if (E > 64 || topk > E || topk < 1 || d % RKB) return hipErrorInvalidValue;
-  k_router<<<(rows_cap + RR - 1) / RR, 256, 0, st>>>((const bf16_t*)A, a_plane, d, Wr, E, topk, M_dev,
+  if (E > 64 || topk > E || topk < 1 || d % (RQ * RKB)) return hipErrorInvalidValue;
+  k_router<<<(rows_cap + RR - 1) / RR, 1024, 0, st>>>((const bf16_t*)A, a_plane, d, Wr, E, topk, M_dev,
                                                      top_e, top_w);
   return hipGetLastError();
 }
