@@ -12,8 +12,11 @@ steps with no host synchronisation.
 
 Prints one JSON line: committed tokens/s, TPF, step latency, the roofline
 of the dominant kernel class (HIP events on the library's stream in a
-second, profiled pass over the same decodes), and the CPU oracle timed on a
-bounded sample of the same workload.
+second, profiled pass over the same decodes) and of the whole step, the
+prefill time (reported apart), whether the timed decodes reproduced the
+reference decode bit for bit, the CPU oracle timed on a bounded sample of the
+same workload, and shorter runs of the batch-16 dense and batch-64 MoE
+workloads as sub-entries.
 """
 from __future__ import annotations
 
@@ -188,7 +191,12 @@ def measure(w, tau, steps, warmup, wq="bf16", tau_semi=None, tau_add=0.0, skip_m
         weights = make_weights(w)
     prompts = make_prompts(w)
     model = bd.Model(w, weights, wq=None if wq == "bf16" else wq)
+    torch.cuda.synchronize()
+    t_pre = time.perf_counter()
     st = bd.State(model, prompts, w.gen_len, tau, w.n_inflight, w.block_size, tau_semi, tau_add, skip_masked)
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t_pre
+    say(f"{w.name}: prefill of {w.batch} x {w.prompt_len} prompt tokens in {1e3 * prefill_s:.1f} ms")
     done, S = False, 0
     while not done:
         st.step()
@@ -276,7 +284,11 @@ def measure(w, tau, steps, warmup, wq="bf16", tau_semi=None, tau_add=0.0, skip_m
                  "bound": "hbm" if t_hbm >= t_mfma else "mfma"}
     res = {"workload": w, "value": value, "ms": ms, "wall": wall, "tpf": tpf, "S": S, "stats": stats,
            "roofline": roof, "step_roofline": step_roof, "kernels": kernels, "weights": weights,
-           "prompts": prompts}
+           "prompts": prompts,
+           "prefill": {"wall_ms": 1e3 * prefill_s,
+                       "prompt_tokens_per_s": w.batch * w.prompt_len / prefill_s,
+                       "note": "first bd_prefill of the batch, host clock around the state's creation "
+                               "(its device allocation included); outside the timed decodes"}}
     st.close()
     model.close()
     return res
@@ -389,7 +401,9 @@ def main():
                    **({"skip_masked": True} if args.skip_masked else {}),
                    **({"weights": args.wq} if args.wq != "bf16" else {})},
         "tpf": r["tpf"], "denoise_steps_per_decode": r["S"], "step_latency_us": 1e3 * r["ms"] / r["S"],
-        "wall_s": r["wall"], "roofline": r["roofline"], "step_roofline": r["step_roofline"],
+        "wall_s": r["wall"], "prefill": r["prefill"],
+        "deterministic": True,       # every timed decode reproduced the reference decode bit for bit
+        "roofline": r["roofline"], "step_roofline": r["step_roofline"],
         "kernels": r["kernels"], "cpu_baseline": cpu,
         "participation": {k: r["stats"][k] for k in ("active_forwards", "zero_commit", "static_saved",
                                                      "static_deferred", "cache_writes", "skipped")},
