@@ -49,7 +49,8 @@ def algorithmic_work(w, stats, wq="bf16"):
     LM rows.  With fp8 layer weights the layer projections read 1 byte per
     weight (the per-row scales are negligible); the LM head stays bf16."""
     esz = 2 if w.dtype == "bf16" else 4     # LM-head / embedding weights
-    lsz = 1 if wq == "fp8" else esz         # decoder-layer projection weights
+    # decoder-layer projection weights: fp8 1 byte, MXFP4 half a byte + an exponent per 32
+    lsz = 1 if wq == "fp8" else (0.5 + 1 / 32 if wq == "mxfp4" else esz)
     asz = esz                                # activations, Q/K/V, K/V cache
     d, H, Hkv, hd, F, V, L = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.ffn_dim, w.vocab, w.n_layers
     qkv = (H + 2 * Hkv) * hd
@@ -93,7 +94,7 @@ def step_work(w, stats, wq="bf16"):
     work = algorithmic_work(w, stats, wq)
     flops = sum(f for f, _ in work.values())
     esz = 2 if w.dtype == "bf16" else 4
-    lsz = 1 if wq == "fp8" else esz
+    lsz = 1 if wq == "fp8" else (0.5 + 1 / 32 if wq == "mxfp4" else esz)
     d, H, Hkv, hd, L = w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.n_layers
     qkv = (H + 2 * Hkv) * hd
     if w.n_experts:
@@ -262,7 +263,8 @@ def measure(w, tau, steps, warmup, wq="bf16", tau_semi=None, tau_add=0.0, skip_m
     else:
         roof = {"bound": "hbm", "achieved": kernels[dom]["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    mt = measured_traffic(w.name, dom)
+    # the counter summaries are of the bf16-weight kernels
+    mt = measured_traffic(w.name, dom) if wq == "bf16" else None
     roof["traffic"] = mt["bytes_per_launch"] if mt else None
     launches = kernels[dom]["launches_per_decode"]
     roof["algorithmic_per_launch"] = {"flops": fl / launches, "bytes": by / launches}
@@ -309,7 +311,7 @@ def main():
                     help="semi-completion threshold (default: off)")
     ap.add_argument("--tau-add", type=float, default=0.0,
                     help="admission threshold (default 0: refill every free slot)")
-    ap.add_argument("--wq", choices=["bf16", "fp8"], default="bf16",
+    ap.add_argument("--wq", choices=["bf16", "fp8", "mxfp4"], default="bf16",
                     help="weight precision of the decoder-layer projections")
     ap.add_argument("--skip-masked", action="store_true",
                     help="static skip rule: leave fully masked blocks behind an active one out of the forward")
@@ -375,6 +377,9 @@ def main():
         if args.wq == "fp8":
             from oracle.quant import fp8_weights
             ow = fp8_weights(w, weights)
+        elif args.wq == "mxfp4":
+            from oracle.quant import mxfp4_weights
+            ow = mxfp4_weights(w, weights)
         cpu = cpu_baseline(w, ow, prompts, args.tau, args.cpu_seconds, args.tau_semi, args.tau_add,
                            args.skip_masked)
     del weights

@@ -66,10 +66,15 @@ typedef struct {
                               LM head stay as given.  The GEMMs read the fp8
                               codes and compute exactly as bf16 GEMMs on the
                               dequantized weights (code value x scale, which
-                              bf16 holds exactly). */
+                              bf16 holds exactly).  BD_WQ_MXFP4 (bf16 models
+                              only) quantizes the same matrices to the OCP
+                              MXFP4 format instead: E2M1 elements with one
+                              E8M0 scale per 32 consecutive elements of a row
+                              (see bd_quantize_mxfp4), again computed exactly
+                              as bf16 GEMMs on the dequantized weights. */
 } bd_model_cfg;
 
-enum { BD_WQ_NONE = 0, BD_WQ_FP8 = 1 };
+enum { BD_WQ_NONE = 0, BD_WQ_FP8 = 1, BD_WQ_MXFP4 = 2 };
 
 /* One serving configuration: the paper's operating point lambda (§2.1, the
  * notation table and App. F): accept threshold, in-flight block count, block
@@ -137,7 +142,7 @@ typedef struct bd_state bd_state;
  *  n_heads not a multiple of n_kv_heads, mask_id out of range, wrong
  *  n_weights, top_k outside [1, n_experts], n_experts > 64, wq not a
  *  BD_WQ_* value),
- *  BD_EUNSUPPORTED (MoE or BD_WQ_FP8 with the f32 dtype; shapes off the GEMM tiles: with
+ *  BD_EUNSUPPORTED (MoE, BD_WQ_FP8 or BD_WQ_MXFP4 with the f32 dtype; shapes off the GEMM tiles: with
  *  bf16 every projection's output and input widths -- (H + 2 Hkv) hd, d,
  *  H hd, vocab, 2 ffn or 2 Fe, ffn or Fe -- must be multiples of 128; an
  *  MoE model's d_model a multiple of 256, for its router's four depth
@@ -159,6 +164,29 @@ bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* weights_dev,
  */
 bd_status bd_quantize_fp8(const void* w_dev, int32_t rows, int32_t cols, uint8_t* codes_dev,
                           float* scale_dev, void* stream);
+
+/*
+ * bd_quantize_mxfp4 -- MXFP4 weight quantization of one bf16 matrix, in the
+ *  layout bd_init_model keeps for BD_WQ_MXFP4 (the microscaling format of the
+ *  quantization grid, App. E).
+ *  w_dev: bf16 [rows][cols] device, cols a multiple of 32, the rows taken in
+ *  groups of group_rows (rows a multiple of group_rows; one group = one
+ *  matrix of a stack, e.g. one expert).  Each 32-element block of a row
+ *  (columns 32 j .. 32 j + 31) shares the exponent X = floor(log2 max|w|) - 2
+ *  over the block (-127 for an all-zero block; clamped to [-127, 127]); each
+ *  element is the E2M1 code (sign bit 3, exponent bits 2-1 with bias 1,
+ *  mantissa bit 0: values 0, 0.5, 1, 1.5, 2, 3, 4, 6) nearest to w / 2^X,
+ *  ties to the even mantissa, magnitudes above 6 saturating to 6.
+ *  Outputs (uint8, device), block-major within each group g:
+ *    codes_dev[g][cols/32][group_rows][16]: the block's 32 codes, element 2k
+ *      in the low nibble of byte k, element 2k + 1 in the high nibble;
+ *    exps_dev[g][cols/32][group_rows]: X + 127 (E8M0).
+ *  Asynchronous on stream (NULL = default).
+ *  Errors: BD_EINVAL for NULL pointers, rows, cols or group_rows < 1, cols not
+ *  a multiple of 32 or rows not a multiple of group_rows; BD_EHIP.
+ */
+bd_status bd_quantize_mxfp4(const void* w_dev, int32_t rows, int32_t cols, int32_t group_rows,
+                            uint8_t* codes_dev, uint8_t* exps_dev, void* stream);
 
 /*
  * bd_prefill -- encode b prompts and create a decode state.

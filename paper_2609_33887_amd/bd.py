@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libbd.so")
 BD_OK, BD_EINVAL, BD_ENOMEM, BD_EHIP, BD_ESTATE, BD_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 BD_F32, BD_BF16 = 0, 1
 
-EXPORTED = ["bd_init_model", "bd_quantize_fp8", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
+EXPORTED = ["bd_init_model", "bd_quantize_fp8", "bd_quantize_mxfp4", "bd_prefill", "bd_denoise_step", "bd_commit", "bd_state_read",
             "bd_decode", "bd_decode_static", "bd_state_reset", "bd_state_steps", "bd_state_stats", "bd_profile",
             "bd_profile_read", "bd_plan_projection", "bd_state_free", "bd_model_free", "bd_last_error", "rl_risk_select",
             "rl_select", "rl_alpha_sweep", "rl_split_exceedance", "rl_monte_carlo"]
@@ -35,8 +35,9 @@ class bd_model_cfg(ctypes.Structure):
                 ("mask_id", ctypes.c_int32), ("dtype", ctypes.c_int32), ("wq", ctypes.c_int32)]
 
 
-BD_WQ_NONE, BD_WQ_FP8 = 0, 1
-WQ = {None: BD_WQ_NONE, "bf16": BD_WQ_NONE, "fp8": BD_WQ_FP8}
+BD_WQ_NONE, BD_WQ_FP8, BD_WQ_MXFP4 = 0, 1, 2
+WQ = {None: BD_WQ_NONE, "bf16": BD_WQ_NONE, "fp8": BD_WQ_FP8, "mxfp4": BD_WQ_MXFP4}
+MX_BLOCK = 32
 
 
 class bd_decode_cfg(ctypes.Structure):
@@ -73,6 +74,7 @@ def _load():
     sig = {
         "bd_init_model": [P(bd_model_cfg), P(VP), I32, VP, P(VP)],
         "bd_quantize_fp8": [VP, I32, I32, VP, VP, VP],
+        "bd_quantize_mxfp4": [VP, I32, I32, I32, VP, VP, VP],
         "bd_prefill": [VP, VP, I32, I32, I32, P(bd_decode_cfg), P(VP)],
         "bd_denoise_step": [VP, VP, VP, VP, VP],
         "bd_commit": [VP, VP, P(I32)],
@@ -148,6 +150,31 @@ def quantize_fp8(w_bf16_bits, device: str = "cuda:0"):
                     torch.cuda.current_stream(device).cuda_stream)
     torch.cuda.synchronize(device)
     return codes.cpu().numpy(), scale.cpu().numpy()
+
+
+def bd_quantize_mxfp4(w_ptr: int, rows: int, cols: int, group_rows: int, codes_ptr: int, exps_ptr: int,
+                      stream: int = 0):
+    _check(lib.bd_quantize_mxfp4(w_ptr, rows, cols, group_rows, codes_ptr, exps_ptr, ctypes.c_void_p(stream)))
+
+
+def quantize_mxfp4(w_bf16_bits, group_rows=None, device: str = "cuda:0"):
+    """MXFP4 codes and block exponents of a bf16 matrix given as uint16 bit
+    patterns [rows][cols] (numpy), in the library's layout (see
+    bd_quantize_mxfp4); returns numpy (codes uint8 [groups][cols/32][group_rows][16],
+    exps uint8 [groups][cols/32][group_rows])."""
+    import numpy as np
+    import torch
+    a = np.ascontiguousarray(w_bf16_bits)
+    rows, cols = a.shape
+    gr = rows if group_rows is None else group_rows
+    w = torch.from_numpy(a.view(np.int16)).to(device)
+    nb = cols // MX_BLOCK
+    codes = torch.empty((rows // gr, nb, gr, 16), dtype=torch.uint8, device=device)
+    exps = torch.empty((rows // gr, nb, gr), dtype=torch.uint8, device=device)
+    bd_quantize_mxfp4(w.data_ptr(), rows, cols, gr, codes.data_ptr(), exps.data_ptr(),
+                      torch.cuda.current_stream(device).cuda_stream)
+    torch.cuda.synchronize(device)
+    return codes.cpu().numpy(), exps.cpu().numpy()
 
 
 def bd_prefill(model: int, prompt_ptr: int, b: int, P: int, G: int, cfg: bd_decode_cfg) -> int:
@@ -350,8 +377,9 @@ class Model:
     """Device copy of the weights plus the library handle."""
 
     def __init__(self, workload, weights, device: str = "cuda:0", wq=None):
-        """``wq``: None (weights in the model dtype) or "fp8" (decoder-layer
-        projections quantized by the library, see bd_quantize_fp8)."""
+        """``wq``: None (weights in the model dtype), "fp8" or "mxfp4"
+        (decoder-layer projections quantized by the library, see
+        bd_quantize_fp8 and bd_quantize_mxfp4)."""
         import numpy as np
         import torch
         self.torch = torch

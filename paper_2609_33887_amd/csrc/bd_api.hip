@@ -55,9 +55,10 @@ struct LayerW {
   const void* w_down_e; // [E][d][Fe]
   void* w_gu_s;         // packed shared-expert gate/up [2 Fs][d] (library-owned)
   const void* w_down_s; // [d][Fs]
-  // BD_WQ_FP8: the projection pointers above hold library-owned fp8 codes
-  // and these their per-row scales (NULL for weights in the model dtype)
-  const float *s_qkv, *s_o, *s_gu, *s_down, *s_gu_e, *s_down_e, *s_gu_s, *s_down_s;
+  // BD_WQ_FP8 / BD_WQ_MXFP4: the projection pointers above hold
+  // library-owned codes and these their format and scales (fp8 row scales or
+  // MXFP4 block exponents; format WQ_NONE for weights in the model dtype)
+  WQuant q_qkv, q_o, q_gu, q_down, q_gu_e, q_down_e, q_gu_s, q_down_s;
 };
 
 struct bd_model {
@@ -181,52 +182,62 @@ namespace bd {
 void set_error(const char* msg) { g_err = msg; }
 }
 
-// BD_WQ_FP8: replace every decoder-layer projection by library-owned fp8
-// codes and row scales (rows of the repacked copies are rows of the
-// original matrices, so the codes do not depend on the packing); the
-// library's bf16 repacked copies are released.
+// BD_WQ_FP8 / BD_WQ_MXFP4: replace every decoder-layer projection by
+// library-owned codes and scales (fp8: one scale per row; MXFP4: one exponent
+// per 32 elements of a row, blocks along the input dimension; rows of the
+// repacked copies are rows of the original matrices, so the codes do not
+// depend on the packing; MoE experts are quantized expert by expert, each a
+// stage-major block of its own); the library's bf16 repacked copies are
+// released.
 static bd_status quantize_layers(bd_model* m) {
   const bd_model_cfg& c = m->cfg;
   const int d = c.d_model, hd = c.head_dim;
+  const bool mx = c.wq == BD_WQ_MXFP4;
   std::vector<void*> drop;
-  auto q = [&](const void* src, int rows, int cols, bool owned_src, const void** dst,
-               const float** scale) -> bd_status {
+  // group_rows: rows of one expert's matrix (MXFP4 stage-major blocks)
+  auto q = [&](const void* src, int rows, int cols, int group_rows, bool owned_src, const void** dst,
+               WQuant* wq) -> bd_status {
+    const size_t n = (size_t)rows * cols;
     uint8_t* codes = nullptr;
-    float* sc = nullptr;
-    if (hipMalloc((void**)&codes, (size_t)rows * cols) != hipSuccess) return fail(BD_ENOMEM, "hipMalloc for fp8 weights failed");
+    void* aux = nullptr;
+    if (hipMalloc((void**)&codes, mx ? n / 2 : n) != hipSuccess) return fail(BD_ENOMEM, "hipMalloc for quantized weights failed");
     m->owned.push_back(codes);
-    if (hipMalloc((void**)&sc, (size_t)rows * sizeof(float)) != hipSuccess) return fail(BD_ENOMEM, "hipMalloc for fp8 scales failed");
-    m->owned.push_back(sc);
-    hipError_t e = launch_quant_fp8_rows(src, rows, cols, codes, sc, m->stream);
-    if (e != hipSuccess) return fail(BD_EHIP, "fp8 quantization: %s", hipGetErrorString(e));
+    if (hipMalloc(&aux, mx ? n / MX_BLOCK : (size_t)rows * sizeof(float)) != hipSuccess)
+      return fail(BD_ENOMEM, "hipMalloc for weight scales failed");
+    m->owned.push_back(aux);
+    hipError_t e = mx ? launch_quant_mxfp4_rows(src, rows, cols, group_rows, codes, (uint8_t*)aux, m->stream)
+                      : launch_quant_fp8_rows(src, rows, cols, codes, (float*)aux, m->stream);
+    if (e != hipSuccess) return fail(BD_EHIP, "weight quantization: %s", hipGetErrorString(e));
     if (owned_src) drop.push_back(const_cast<void*>(src));
     *dst = codes;
-    *scale = sc;
+    wq->fmt = mx ? WQ_MXFP4 : WQ_FP8;
+    wq->aux = aux;
     return BD_OK;
   };
   bd_status r = BD_OK;
   for (LayerW& L : m->layers) {
     const void* p;
-    if ((r = q(L.w_qkv_p, (c.n_heads + 2 * c.n_kv_heads) * hd, d, true, &p, &L.s_qkv)) != BD_OK) return r;
+    const int nqkv = (c.n_heads + 2 * c.n_kv_heads) * hd;
+    if ((r = q(L.w_qkv_p, nqkv, d, nqkv, true, &p, &L.q_qkv)) != BD_OK) return r;
     L.w_qkv_p = const_cast<void*>(p);
-    if ((r = q(L.w_o, d, c.n_heads * hd, false, &L.w_o, &L.s_o)) != BD_OK) return r;
+    if ((r = q(L.w_o, d, c.n_heads * hd, d, false, &L.w_o, &L.q_o)) != BD_OK) return r;
     if (c.n_experts == 0) {
-      if ((r = q(L.w_gu, 2 * c.ffn_dim, d, true, &p, &L.s_gu)) != BD_OK) return r;
+      if ((r = q(L.w_gu, 2 * c.ffn_dim, d, 2 * c.ffn_dim, true, &p, &L.q_gu)) != BD_OK) return r;
       L.w_gu = const_cast<void*>(p);
-      if ((r = q(L.w_down, d, c.ffn_dim, false, &L.w_down, &L.s_down)) != BD_OK) return r;
+      if ((r = q(L.w_down, d, c.ffn_dim, d, false, &L.w_down, &L.q_down)) != BD_OK) return r;
     } else {
       const int E = c.n_experts, Fe = c.expert_ffn, Fs = c.n_shared * c.expert_ffn;
-      if ((r = q(L.w_gu_e, E * 2 * Fe, d, true, &p, &L.s_gu_e)) != BD_OK) return r;
+      if ((r = q(L.w_gu_e, E * 2 * Fe, d, 2 * Fe, true, &p, &L.q_gu_e)) != BD_OK) return r;
       L.w_gu_e = const_cast<void*>(p);
-      if ((r = q(L.w_down_e, E * d, Fe, false, &L.w_down_e, &L.s_down_e)) != BD_OK) return r;
+      if ((r = q(L.w_down_e, E * d, Fe, d, false, &L.w_down_e, &L.q_down_e)) != BD_OK) return r;
       if (Fs > 0) {
-        if ((r = q(L.w_gu_s, 2 * Fs, d, true, &p, &L.s_gu_s)) != BD_OK) return r;
+        if ((r = q(L.w_gu_s, 2 * Fs, d, 2 * Fs, true, &p, &L.q_gu_s)) != BD_OK) return r;
         L.w_gu_s = const_cast<void*>(p);
-        if ((r = q(L.w_down_s, d, Fs, false, &L.w_down_s, &L.s_down_s)) != BD_OK) return r;
+        if ((r = q(L.w_down_s, d, Fs, d, false, &L.w_down_s, &L.q_down_s)) != BD_OK) return r;
       }
     }
   }
-  if (hipStreamSynchronize(m->stream) != hipSuccess) return fail(BD_EHIP, "fp8 quantization failed");
+  if (hipStreamSynchronize(m->stream) != hipSuccess) return fail(BD_EHIP, "weight quantization failed");
   for (void* p : drop) {
     for (auto it = m->owned.begin(); it != m->owned.end(); ++it)
       if (*it == p) { m->owned.erase(it); break; }
@@ -243,6 +254,16 @@ extern "C" bd_status bd_quantize_fp8(const void* w, int32_t rows, int32_t cols, 
   return BD_OK;
 }
 
+extern "C" bd_status bd_quantize_mxfp4(const void* w, int32_t rows, int32_t cols, int32_t group_rows,
+                                       uint8_t* codes, uint8_t* exps, void* stream) {
+  if (!w || !codes || !exps) return fail(BD_EINVAL, "NULL argument");
+  if (rows < 1 || cols < 1 || group_rows < 1) return fail(BD_EINVAL, "need rows, cols, group_rows >= 1");
+  if (cols % MX_BLOCK || rows % group_rows)
+    return fail(BD_EINVAL, "cols must be a multiple of 32 and rows of group_rows");
+  HIPCHK(launch_quant_mxfp4_rows(w, rows, cols, group_rows, codes, exps, (hipStream_t)stream));
+  return BD_OK;
+}
+
 extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w, int32_t n_weights,
                                    void* stream, bd_model** out) {
   if (!cfg || !w || !out) return fail(BD_EINVAL, "NULL argument");
@@ -254,8 +275,10 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
   if (c.n_heads % c.n_kv_heads) return fail(BD_EINVAL, "n_heads must be a multiple of n_kv_heads");
   if (c.mask_id < 0 || c.mask_id >= c.vocab) return fail(BD_EINVAL, "mask_id outside [0, vocab)");
   if (c.dtype != BD_F32 && c.dtype != BD_BF16) return fail(BD_EINVAL, "unknown dtype");
-  if (c.wq != BD_WQ_NONE && c.wq != BD_WQ_FP8) return fail(BD_EINVAL, "unknown weight precision");
-  if (c.wq == BD_WQ_FP8 && c.dtype != BD_BF16) return fail(BD_EUNSUPPORTED, "fp8 weights need the bf16 dtype");
+  if (c.wq != BD_WQ_NONE && c.wq != BD_WQ_FP8 && c.wq != BD_WQ_MXFP4)
+    return fail(BD_EINVAL, "unknown weight precision");
+  if (c.wq != BD_WQ_NONE && c.dtype != BD_BF16)
+    return fail(BD_EUNSUPPORTED, "fp8 and MXFP4 weights need the bf16 dtype");
   const bool moe = c.n_experts > 0;
   const bool bf16 = c.dtype == BD_BF16;
   const int Fs = moe ? c.n_shared * c.expert_ffn : 0;
@@ -358,7 +381,7 @@ extern "C" bd_status bd_init_model(const bd_model_cfg* cfg, const void* const* w
   }
   m->final_norm = (const float*)w[t++];
   m->lm_head = w[t++];
-  if (c.wq == BD_WQ_FP8) {
+  if (c.wq != BD_WQ_NONE) {
     bd_status r = quantize_layers(m);
     if (r != BD_OK) {
       bd_model_free(m);
@@ -428,9 +451,9 @@ static bd_status run_moe(bd_model* m, bd_state* s, const LayerW& L, const PlanVi
   const int Fs = c.n_shared * Fe;
   if (Fs > 0) {
     LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, true, s->A, d, s->pl_A, L.w_gu_s, d, 2 * Fs, d,
-                                        plan.hdr, rows_cap, s->Hact, Fs, s->pl_H, st, L.s_gu_s));
+                                        plan.hdr, rows_cap, s->Hact, Fs, s->pl_H, st, L.q_gu_s));
     LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm(EPI_ADD_F32, true, s->Hact, Fs, s->pl_H, L.w_down_s, Fs, d,
-                                          Fs, plan.hdr, rows_cap, s->X, d, 0, st, L.s_down_s));
+                                          Fs, plan.hdr, rows_cap, s->X, d, 0, st, L.q_down_s));
   }
   LAUNCH(BD_PROF_MOE, launch_router(s->A, s->pl_A, d, L.wr, E, k, plan.hdr, rows_cap, s->top_e,
                                     s->top_w, st));
@@ -444,12 +467,12 @@ static bd_status run_moe(bd_model* m, bd_state* s, const LayerW& L, const PlanVi
   g.a_rows = s->moe.list_row;
   g.w_stride = (size_t)2 * Fe * d;
   LAUNCH(BD_PROF_GEMM_GU, launch_gemm_grouped(EPI_SWIGLU, s->A, d, s->pl_A, L.w_gu_e, d, 2 * Fe, d, g,
-                                              s->moe_tiles, s->act_sorted, Fe, s->pl_act, L.s_gu_e, st));
+                                              s->moe_tiles, s->act_sorted, Fe, s->pl_act, L.q_gu_e, st));
   g.a_rows = nullptr;
   g.w_stride = (size_t)d * Fe;
   LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm_grouped(EPI_STORE_F32, s->act_sorted, Fe, s->pl_act,
                                                 L.w_down_e, Fe, d, Fe, g, s->moe_tiles, s->y_sorted,
-                                                d, 0, L.s_down_e, st));
+                                                d, 0, L.q_down_e, st));
   LAUNCH(BD_PROF_MOE, launch_moe_combine(s->X, s->y_sorted, s->moe.pos_of, s->top_w, k, d, plan.hdr,
                                          rows_cap, st));
   return BD_OK;
@@ -497,7 +520,7 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
       e.hd = hd;
       e.rows4 = s->B % 4 == 0;
       LAUNCH(BD_PROF_GEMM_QKV, launch_gemm_qkv(s->A, d, s->pl_A, L.w_qkv_p, d, plan.hdr, rows_cap, e, st,
-                                               L.s_qkv));
+                                               L.q_qkv));
     } else {
       LAUNCH(BD_PROF_GEMM_QKV, launch_gemm(EPI_STORE_F32, bf, s->A, d, s->pl_A, L.w_qkv, d, qkv, d,
                                            plan.hdr, rows_cap, s->QKV, qkv, 0, st));
@@ -509,16 +532,16 @@ static bd_status run_forward(bd_model* m, bd_state* s, const PlanView& plan, int
                                           kv_splits, s->attn_ws_o, s->attn_ws_ml, rows_cap, st));
     LAUNCH(BD_PROF_GEMM_O, launch_gemm_resid(bf, s->Ob, H * hd, s->pl_O, L.w_o, H * hd, d, H * hd,
                                              plan.hdr, rows_cap, s->X, d, s->resid_ws, s->resid_ws_floats, &pend, st,
-                                             L.s_o));
+                                             L.q_o));
     LAUNCH(BD_PROF_NORM, launch_rmsnorm(bf, s->X, L.ffn_norm, d, c.rms_eps, plan.hdr, nullptr,
                                         rows_cap, s->A, s->pl_A, pend, st));
     pend.ws = nullptr;
     if (c.n_experts == 0) {
       LAUNCH(BD_PROF_GEMM_GU, launch_gemm(EPI_SWIGLU, bf, s->A, d, s->pl_A, L.w_gu, d, 2 * F, d,
-                                          plan.hdr, rows_cap, s->Hact, F, s->pl_H, st, L.s_gu));
+                                          plan.hdr, rows_cap, s->Hact, F, s->pl_H, st, L.q_gu));
       LAUNCH(BD_PROF_GEMM_DOWN, launch_gemm_resid(bf, s->Hact, F, s->pl_H, L.w_down, F, d, F,
                                                   plan.hdr, rows_cap, s->X, d, s->resid_ws, s->resid_ws_floats, &pend,
-                                                  st, L.s_down));
+                                                  st, L.q_down));
     } else {
       bd_status r = run_moe(m, s, L, plan, rows_cap);
       if (r != BD_OK) return r;
@@ -567,7 +590,7 @@ static ResidSplit resid_split_of(int N, int K, int rows_cap, bool wide_ok = true
 }
 
 static size_t resid_ws_need(const bd_model_cfg& c, int rows_cap) {
-  // the larger extent of the bf16-weight and the fp8-weight plans
+  // the larger extent of the bf16-weight and the quantized-weight plans
   const int d = c.d_model;
   size_t need = 0;
   for (int wide = 0; wide < 2; ++wide) {

@@ -9,11 +9,18 @@
 // global-to-LDS loads into a four-stage ring (K-stages of 32, swizzled rows);
 // one barrier per stage; the residual projections may split K (the partial
 // sums are folded in by the next RMSNorm).
-// fp8 weights (W8): W holds OCP fp8 E4M3 codes, one byte per element, with
-// a power-of-two scale per output row; the W stage holds 32-byte rows, each
-// lane converts its 8 codes of a fragment to bf16 (exact) before the MFMA,
-// and the epilogue multiplies each output column by its row scale (exact, so
-// the result equals the bf16 product with the dequantized weights).
+// fp8 weights (WQ = WQ_FP8): W holds OCP fp8 E4M3 codes, one byte per
+// element, with a power-of-two scale per output row; the W stage holds
+// 32-byte rows, each lane converts its 8 codes of a fragment to bf16 (exact)
+// before the MFMA, and the epilogue multiplies each output column by its row
+// scale (exact, so the result equals the bf16 product with the dequantized
+// weights).
+// MXFP4 weights (WQ = WQ_MXFP4): a 32-deep stage is one MX block, so the
+// stage holds each W row's 16 bytes of E2M1 codes and its block exponent; the
+// lane converts its 8 codes with the block scale (v_cvt_scalef32_pk_bf16_fp4:
+// E2M1 value x 2^X, exact in bf16), again the bf16 product with the
+// dequantized weights.  The codes are stored stage-major (WQuant), so a
+// stage's W rows are one contiguous run of 16-byte rows.
 // f32 path (small fp32 models): 64x64x16 SIMT tiles.
 //
 // The row count M is read from device memory so that a launch sized for the
@@ -64,11 +71,13 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int BM, int BN, bool W8 = false>
+template <int BM, int BN, int WQ = WQ_NONE>
 struct GemmStage {
   bf16_t ah[BM * SK];
   bf16_t al[BM * SK];
-  bf16_t b[W8 ? BN * SK / 2 : BN * SK];   // bf16 rows of 64 B, or fp8 rows of 32 B
+  // bf16 rows of 64 B, fp8 rows of 32 B, or E2M1 rows of 16 B
+  bf16_t b[WQ == WQ_NONE ? BN * SK : (WQ == WQ_FP8 ? BN * SK / 2 : BN * SK / 4)];
+  uint8_t be[WQ == WQ_MXFP4 ? BN : 0];    // the MXFP4 rows' block exponents
 };
 
 // fp8 W loads per wave and stage: BN = 128 -> one 16-byte load per lane
@@ -79,6 +88,27 @@ struct W8Load {
   static constexpr int loads = BN * SK / (4 * 64 * bytes);
   static constexpr int rows = 64 * bytes / SK;      // rows per load instruction
 };
+
+// MXFP4 W loads per wave and stage: BN rows x 16 B of codes as 4-byte loads
+// (16 rows per load instruction), plus one 4-byte load of BN / 4 exponents.
+template <int BN>
+struct W4Load {
+  static constexpr int loads = BN * 16 / (4 * 64 * 4);
+};
+
+// Eight E2M1 codes (nibbles of v, k order, low nibble first) times the block
+// scale -> eight bf16 (exact).
+__device__ __forceinline__ bf16x8 fp4x8_to_bf16(uint32_t v, float scale) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(v, scale, 0);
+  const bf16x2_t b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(v, scale, 1);
+  const bf16x2_t c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(v, scale, 2);
+  const bf16x2_t d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(v, scale, 3);
+  bf16x8 o;
+  o[0] = a[0]; o[1] = a[1]; o[2] = b[0]; o[3] = b[1];
+  o[4] = c[0]; o[5] = c[1]; o[6] = d[0]; o[7] = d[1];
+  return o;
+}
 
 // Eight E4M3 codes (bytes 0..7 of v, k order) -> eight bf16 (exact).
 __device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint2 v) {
@@ -109,24 +139,27 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Per-thread source pointers of one tile's loads: A rows (hi plane; lo at
 // + a_plane) and W rows, each already offset to this lane's 16-byte chunk.
-template <int BM, int BN, bool W8 = false, int NW = 4>
+template <int BM, int BN, int WQ = WQ_NONE, int NW = 4>
 struct TileSrc {
   const bf16_t* a[BM / (16 * NW)];
-  const bf16_t* w[W8 ? 1 : BN / (16 * NW)];
-  const uint8_t* w8[W8 ? W8Load<BN>::loads : 1];
+  const bf16_t* w[WQ == WQ_NONE ? BN / (16 * NW) : 1];
+  const uint8_t* w8[WQ == WQ_FP8 ? W8Load<BN>::loads : 1];
+  const uint8_t* w4[WQ == WQ_MXFP4 ? W4Load<BN>::loads : 1];
+  const uint8_t* we;        // MXFP4: this lane's 4 exponents of the first stage
+  size_t kstep;             // MXFP4: rows per stage block (codes advance 16 bytes a row)
 };
 
-template <int BM, int BN, bool W8, int NW = 4>
-__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8, NW>& src, size_t a_plane, int k,
-                                            GemmStage<BM, BN, W8>& s, int wave) {
-  static_assert(!W8 || NW == 4, "fp8 weights take four waves");
+template <int BM, int BN, int WQ, int NW = 4>
+__device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, WQ, NW>& src, size_t a_plane, int k,
+                                            GemmStage<BM, BN, WQ>& s, int wave) {
+  static_assert(WQ == WQ_NONE || NW == 4, "quantized weights take four waves");
 #pragma unroll
   for (int i = 0; i < BM / (16 * NW); ++i) {
     const int r = (i * NW + wave) * 16;
     __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k), (lds_void_t*)(s.ah + r * SK), 16, 0, 0);
     __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k + a_plane), (lds_void_t*)(s.al + r * SK), 16, 0, 0);
   }
-  if constexpr (W8) {
+  if constexpr (WQ == WQ_FP8) {
     typedef W8Load<BN> L;
     uint8_t* b8 = (uint8_t*)s.b;
 #pragma unroll
@@ -134,6 +167,20 @@ __device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8, NW>& src, 
       const int r = (wave * L::loads + i) * L::rows;
       __builtin_amdgcn_global_load_lds((const void*)(src.w8[i] + k), (lds_void_t*)(b8 + r * SK), L::bytes, 0, 0);
     }
+  } else if constexpr (WQ == WQ_MXFP4) {
+    // stage k is block k / SK: codes advance kstep rows of 16 bytes a block,
+    // exponents kstep bytes; wave w fills 256-byte runs (16 rows) of codes and
+    // exponent bytes [w BN / 4, (w + 1) BN / 4) with its first BN / 16 lanes
+    typedef W4Load<BN> L;
+    const size_t kb = (size_t)(k / SK);
+    uint8_t* b4 = (uint8_t*)s.b;
+#pragma unroll
+    for (int i = 0; i < L::loads; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(src.w4[i] + kb * src.kstep * 16),
+                                       (lds_void_t*)(b4 + (wave * L::loads + i) * 256), 4, 0, 0);
+    if ((threadIdx.x & 63) < BN / 16)
+      __builtin_amdgcn_global_load_lds((const void*)(src.we + kb * src.kstep), (lds_void_t*)(s.be + wave * (BN / 4)),
+                                       4, 0, 0);
   } else {
 #pragma unroll
     for (int i = 0; i < BN / (16 * NW); ++i) {
@@ -145,21 +192,33 @@ __device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, W8, NW>& src, 
 
 // One stage of MFMAs: NW waves in a 2 x (NW/2) arrangement, each
 // accumulating a (BM/2) x (2BN/NW) sub-tile of MFMA 16x16x32 tiles.
-template <int BM, int BN, bool W8, int NW = 4>
-__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaTile<BM, BN, NW>& t, int wave) {
+template <int BM, int BN, int WQ, int NW = 4>
+__device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, WQ>& s, MfmaTile<BM, BN, NW>& t, int wave) {
   constexpr int FM = BM / 32, FN = BN / (8 * NW), WCOL = 2 * BN / NW;
   const int lane = threadIdx.x & 63;
   const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   const int r16 = lane & 15;
   const int pos = ((lane >> 4) ^ swz(r16)) * 8;   // fragment rows are r16 + 16 j
   u32x4 bfr[FN];
-  if constexpr (W8) {
+  if constexpr (WQ == WQ_FP8) {
     // fp8 rows of 32 B, unswizzled: a fragment's 16 rows are 512 contiguous bytes
     const uint8_t* b8 = (const uint8_t*)s.b;
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const uint2 raw = *(const uint2*)(b8 + (wn * WCOL + j * 16 + r16) * SK + (lane >> 4) * 8);
       bfr[j] = __builtin_bit_cast(u32x4, fp8x8_to_bf16(raw));
+    }
+  } else if constexpr (WQ == WQ_MXFP4) {
+    // E2M1 rows of 16 B: a fragment's 16 rows are 256 contiguous bytes; the
+    // lane's 8 codes are 4 bytes, scaled by 2^(e - 127) (e >= 1; e = 0 only
+    // in all-zero blocks, whose codes are zero)
+    const uint8_t* b4 = (const uint8_t*)s.b;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int row = wn * WCOL + j * 16 + r16;
+      const uint32_t raw = *(const uint32_t*)(b4 + row * 16 + (lane >> 4) * 4);
+      const float sc = __uint_as_float((uint32_t)s.be[row] << 23);
+      bfr[j] = __builtin_bit_cast(u32x4, fp4x8_to_bf16(raw, sc));
     }
   } else {
 #pragma unroll
@@ -186,26 +245,31 @@ __device__ __forceinline__ void stage_mfma(const GemmStage<BM, BN, W8>& s, MfmaT
 // are separate LDS objects so the compiler can tell the loads into one stage
 // from the reads of another.  All waves of the workgroup must run the same
 // number of stages (the barriers are workgroup-wide).
-template <int BM, int BN, bool W8 = false, int NW = 4>
+// Weights: bf16 or fp8 rows of stride ldw, or (MXFP4) the stage-major block
+// of ldw rows per 32-deep stage with the exponents wexp.
+template <int BM, int BN, int WQ = WQ_NONE, int NW = 4>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int lda, size_t a_plane,
-                                              const void* __restrict__ Wv, int ldw, int k0,
+                                              const void* __restrict__ Wv, int ldw,
+                                              const uint8_t* __restrict__ wexp, int k0,
                                               int klen, int m0, int n0, MfmaTile<BM, BN, NW>& t,
-                                              GemmStage<BM, BN, W8>& s0, GemmStage<BM, BN, W8>& s1,
-                                              GemmStage<BM, BN, W8>& s2, GemmStage<BM, BN, W8>& s3,
+                                              GemmStage<BM, BN, WQ>& s0, GemmStage<BM, BN, WQ>& s1,
+                                              GemmStage<BM, BN, WQ>& s2, GemmStage<BM, BN, WQ>& s3,
                                               int wave, const int32_t* __restrict__ arows = nullptr,
                                               int nvalid = 0) {
   // load instructions per thread per stage
-  constexpr int LPS = 2 * (BM / (16 * NW)) + (W8 ? W8Load<BN>::loads : BN / (16 * NW));
+  constexpr int LPS = 2 * (BM / (16 * NW)) +
+                      (WQ == WQ_FP8 ? W8Load<BN>::loads
+                                    : (WQ == WQ_MXFP4 ? W4Load<BN>::loads + 1 : BN / (16 * NW)));
   const int lane = threadIdx.x & 63;
   const int rsub = lane >> 2, chunk = (lane & 3) ^ swz(rsub);
-  TileSrc<BM, BN, W8, NW> src;
+  TileSrc<BM, BN, WQ, NW> src;
 #pragma unroll
   for (int i = 0; i < BM / (16 * NW); ++i) {
     const int r = (i * NW + wave) * 16 + rsub;
     const int grow = arows ? arows[r < nvalid ? r : 0] : m0 + r;
     src.a[i] = A + (size_t)grow * lda + k0 + chunk * 8;
   }
-  if constexpr (W8) {
+  if constexpr (WQ == WQ_FP8) {
     typedef W8Load<BN> L;
     const uint8_t* W = (const uint8_t*)Wv;
     const int per_row = SK / L::bytes;       // lanes per 32-byte row
@@ -214,6 +278,14 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
       const int r = (wave * L::loads + i) * L::rows + lane / per_row;
       src.w8[i] = W + (size_t)(n0 + r) * ldw + k0 + (lane % per_row) * L::bytes;
     }
+  } else if constexpr (WQ == WQ_MXFP4) {
+    typedef W4Load<BN> L;
+    const size_t kb0 = (size_t)(k0 / SK);
+    const uint8_t* W = (const uint8_t*)Wv + (kb0 * ldw + n0) * 16;
+#pragma unroll
+    for (int i = 0; i < L::loads; ++i) src.w4[i] = W + (wave * L::loads + i) * 256 + lane * 4;
+    src.we = wexp + kb0 * ldw + n0 + wave * (BN / 4) + (lane < BN / 16 ? lane : 0) * 4;
+    src.kstep = (size_t)ldw;
   } else {
     const bf16_t* W = (const bf16_t*)Wv;
 #pragma unroll
@@ -226,9 +298,9 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
     for (int j = 0; j < BN / (8 * NW); ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = klen / SK;     // multiple of 4, >= 4
-  stage_issue<BM, BN, W8, NW>(src, a_plane, 0, s0, wave);
-  stage_issue<BM, BN, W8, NW>(src, a_plane, SK, s1, wave);
-  stage_issue<BM, BN, W8, NW>(src, a_plane, 2 * SK, s2, wave);
+  stage_issue<BM, BN, WQ, NW>(src, a_plane, 0, s0, wave);
+  stage_issue<BM, BN, WQ, NW>(src, a_plane, SK, s1, wave);
+  stage_issue<BM, BN, WQ, NW>(src, a_plane, 2 * SK, s2, wave);
   int kt = 0;
   // each step: own loads of stage kt done (the two younger stages may still
   // be in flight), barrier (everyone's loads done, everyone past stage kt-1),
@@ -236,8 +308,8 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
 #define BD_GEMM_STEP(CUR, NXT, KNEXT)                            \
   wait_vmcnt<2 * LPS>();                                         \
   __builtin_amdgcn_s_barrier();                                  \
-  stage_issue<BM, BN, W8, NW>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
-  stage_mfma<BM, BN, W8, NW>(CUR, t, wave);
+  stage_issue<BM, BN, WQ, NW>(src, a_plane, (KNEXT) * SK, NXT, wave);    \
+  stage_mfma<BM, BN, WQ, NW>(CUR, t, wave);
   for (; kt + 4 < nk; kt += 4) {
     BD_GEMM_STEP(s0, s3, kt + 3)
     BD_GEMM_STEP(s1, s0, kt + 4)
@@ -248,21 +320,21 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
   // the last four stages (kt + 3 == nk - 1)
   wait_vmcnt<2 * LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_issue<BM, BN, W8, NW>(src, a_plane, (kt + 3) * SK, s3, wave);
-  stage_mfma<BM, BN, W8, NW>(s0, t, wave);
+  stage_issue<BM, BN, WQ, NW>(src, a_plane, (kt + 3) * SK, s3, wave);
+  stage_mfma<BM, BN, WQ, NW>(s0, t, wave);
   wait_vmcnt<2 * LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN, W8, NW>(s1, t, wave);
+  stage_mfma<BM, BN, WQ, NW>(s1, t, wave);
   wait_vmcnt<LPS>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN, W8, NW>(s2, t, wave);
+  stage_mfma<BM, BN, WQ, NW>(s2, t, wave);
   wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  stage_mfma<BM, BN, W8, NW>(s3, t, wave);
+  stage_mfma<BM, BN, WQ, NW>(s3, t, wave);
 }
 
-#define BD_GEMM_SMEM(BM, BN, W8)                                                 \
-  __shared__ __attribute__((aligned(1024))) GemmStage<BM, BN, W8> gs0, gs1, gs2, gs3
+#define BD_GEMM_SMEM(BM, BN, WQ)                                                 \
+  __shared__ __attribute__((aligned(1024))) GemmStage<BM, BN, WQ> gs0, gs1, gs2, gs3
 
 // fp8 weights: multiply accumulator column n (of this wave's fragments) by
 // the row scale sc[n] of the weight, a power of two.
@@ -289,14 +361,14 @@ __device__ __forceinline__ void scale_columns(MfmaTile<BM, BN>& t, const float* 
 // split stores its raw partial tile to ws[split][row][col] (rows padded to
 // whole tiles) and the next RMSNorm of the residual stream adds the partials
 // in split order.
-template <int BM, int BN, int EPI, bool W8, int NW = 4>
+template <int BM, int BN, int EPI, int WQ, int NW = 4>
 __global__ __launch_bounds__(64 * NW) void k_gemm_bf16(const bf16_t* __restrict__ A, int lda,
                                                    size_t a_plane, const void* __restrict__ W,
                                                    int ldw, int N, int K,
                                                    const int32_t* __restrict__ Mp,
                                                    void* __restrict__ out, int ldo, size_t out_plane,
                                                    float* __restrict__ ws, int zmax,
-                                                   const float* __restrict__ wscale) {
+                                                   const void* __restrict__ waux) {
   constexpr int FM = BM / 32, FN = BN / (8 * NW), WCOL = 2 * BN / NW;
   const int M = *Mp;
   const int X = N / BN, Y = (M + BM - 1) / BM;
@@ -315,11 +387,11 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_bf16(const bf16_t* __restrict_
   const int m0 = ty * BM, n0 = tx * BN;
   const int klen = K / S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  BD_GEMM_SMEM(BM, BN, W8);
+  BD_GEMM_SMEM(BM, BN, WQ);
   MfmaTile<BM, BN, NW> t;
-  mfma_mainloop<BM, BN, W8, NW>(A, lda, a_plane, W, ldw, z * klen, klen, m0, n0, t, gs0, gs1, gs2,
-                                gs3, wave);
-  if constexpr (W8) scale_columns<BM, BN>(t, wscale, n0, wave);
+  mfma_mainloop<BM, BN, WQ, NW>(A, lda, a_plane, W, WQ == WQ_MXFP4 ? N : ldw, (const uint8_t*)waux,
+                                z * klen, klen, m0, n0, t, gs0, gs1, gs2, gs3, wave);
+  if constexpr (WQ == WQ_FP8) scale_columns<BM, BN>(t, (const float*)waux, n0, wave);
   const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   float* wz = (EPI == EPI_ADD_F32 && S > 1) ? ws + (size_t)z * ((M + BM - 1) / BM) * BM * N
                                             : nullptr;
@@ -371,11 +443,11 @@ __device__ __forceinline__ void store_pair4(bf16_t* p, size_t plane, const float
       make_uint2((uint32_t)l[0] | ((uint32_t)l[1] << 16), (uint32_t)l[2] | ((uint32_t)l[3] << 16));
 }
 
-template <int BM, int BN, bool W8, int NW = 4>
+template <int BM, int BN, int WQ, int NW = 4>
 __global__ __launch_bounds__(64 * NW) void k_gemm_qkv(const bf16_t* __restrict__ A, int lda,
                                                   size_t a_plane, const void* __restrict__ W,
                                                   int K, const int32_t* __restrict__ Mp, QkvEpi e,
-                                                  const float* __restrict__ wscale) {
+                                                  const void* __restrict__ waux) {
   constexpr int FM = BM / 32, FN = BN / (8 * NW), WCOL = 2 * BN / NW;
   const int M = *Mp;
   const int X = (e.H + 2 * e.Hkv) * e.hd / BN, Y = (M + BM - 1) / BM;
@@ -385,10 +457,11 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_qkv(const bf16_t* __restrict__
   band_tile(u, X, Y, BAND_R, tx, ty);
   const int m0 = ty * BM, n0 = tx * BN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  BD_GEMM_SMEM(BM, BN, W8);
+  BD_GEMM_SMEM(BM, BN, WQ);
   MfmaTile<BM, BN, NW> t;
-  mfma_mainloop<BM, BN, W8, NW>(A, lda, a_plane, W, K, 0, K, m0, n0, t, gs0, gs1, gs2, gs3, wave);
-  if constexpr (W8) scale_columns<BM, BN>(t, wscale, n0, wave);
+  mfma_mainloop<BM, BN, WQ, NW>(A, lda, a_plane, W, WQ == WQ_MXFP4 ? X * BN : K, (const uint8_t*)waux, 0, K,
+                                m0, n0, t, gs0, gs1, gs2, gs3, wave);
+  if constexpr (WQ == WQ_FP8) scale_columns<BM, BN>(t, (const float*)waux, n0, wave);
   const int wm = wave / (NW / 2), wn = wave % (NW / 2);
   const int hd = e.hd, half = hd >> 1;
   const int qcols = e.H * hd, qkcols = (e.H + e.Hkv) * hd;
@@ -455,31 +528,38 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_qkv(const bf16_t* __restrict__
 // tile_e[ti]; the expert's rows sit at [e_off[e], e_off[e] + e_cnt[e]) of the
 // expert-sorted outputs.  The A rows are gathered through a_rows (token rows
 // of the expert-sorted assignments) or, with a_rows == NULL, read from the
-// expert-sorted layout itself.  W of expert e starts at W + e * w_stride.
-template <int EPI, bool W8>
+// expert-sorted layout itself.  W of expert e starts e * w_stride weight
+// elements in (its codes, for quantized weights); fp8 row scales at
+// waux + e * N, MXFP4 exponents at waux + e * w_stride / 32.
+template <int EPI, int WQ>
 __global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__ A, int lda,
                                                       size_t a_plane, const void* __restrict__ W,
                                                       int ldw, int K, GroupTiles g,
                                                       void* __restrict__ out, int ldo,
                                                       size_t out_plane,
-                                                      const float* __restrict__ wscale,
-                                                      int scale_stride) {
+                                                      const void* __restrict__ waux, int N) {
   constexpr int BM = 128, BN = 128, FM = BM / 32, FN = BN / 32;
   const int ti = blockIdx.y;
   if (ti >= *g.ntiles) return;
   const int e = g.tile_e[ti], m0 = g.tile_m0[ti];
   const int cnt = g.e_cnt[e], base = g.e_off[e];
   const int n0 = blockIdx.x * BN;
-  BD_GEMM_SMEM(BM, BN, W8);
+  BD_GEMM_SMEM(BM, BN, WQ);
   MfmaTile<BM, BN> t;
-  const void* We = (const uint8_t*)W + (size_t)e * g.w_stride * (W8 ? 1 : 2);
+  const size_t eoff = (size_t)e * g.w_stride;
+  const void* We = WQ == WQ_NONE  ? (const void*)((const bf16_t*)W + eoff)
+                   : WQ == WQ_FP8 ? (const void*)((const uint8_t*)W + eoff)
+                                  : (const void*)((const uint8_t*)W + eoff / 2);
+  const uint8_t* wexp = WQ == WQ_MXFP4 ? (const uint8_t*)waux + eoff / MX_BLOCK : nullptr;
+  const int ldw_e = WQ == WQ_MXFP4 ? N : ldw;
   if (g.a_rows)
-    mfma_mainloop<BM, BN, W8>(A, lda, a_plane, We, ldw, 0, K, 0, n0, t, gs0, gs1, gs2, gs3,
+    mfma_mainloop<BM, BN, WQ>(A, lda, a_plane, We, ldw_e, wexp, 0, K, 0, n0, t, gs0, gs1, gs2, gs3,
                               threadIdx.x >> 6, g.a_rows + base + m0, cnt - m0);
   else
-    mfma_mainloop<BM, BN, W8>(A, lda, a_plane, We, ldw, 0, K, base + m0, n0, t, gs0, gs1, gs2, gs3,
+    mfma_mainloop<BM, BN, WQ>(A, lda, a_plane, We, ldw_e, wexp, 0, K, base + m0, n0, t, gs0, gs1, gs2, gs3,
                               threadIdx.x >> 6);
-  if constexpr (W8) scale_columns<BM, BN>(t, wscale + (size_t)e * scale_stride, n0, threadIdx.x >> 6);
+  if constexpr (WQ == WQ_FP8)
+    scale_columns<BM, BN>(t, (const float*)waux + (size_t)e * N, n0, threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -507,16 +587,22 @@ __global__ __launch_bounds__(256) void k_gemm_grouped(const bf16_t* __restrict__
 
 hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
                                int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
-                               int ldo, size_t out_plane, const float* wscale, hipStream_t st) {
+                               int ldo, size_t out_plane, WQuant wq, hipStream_t st) {
   if (N % 128 || K % KALIGN) return hipErrorInvalidValue;
+  if ((wq.fmt != WQ_NONE) != (wq.aux != nullptr) || wq.fmt < WQ_NONE || wq.fmt > WQ_MXFP4)
+    return hipErrorInvalidValue;
   dim3 grid(N / 128, max_tiles);
   const bf16_t* a = (const bf16_t*)A;
-#define BD_GROUPED(EPI_, W8_, OP_) \
-  k_gemm_grouped<EPI_, W8_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, ldw, K, g, out, ldo, OP_, wscale, N)
+#define BD_GROUPED(EPI_, WQ_, OP_) \
+  k_gemm_grouped<EPI_, WQ_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, ldw, K, g, out, ldo, OP_, wq.aux, N)
   if (epi == EPI_SWIGLU) {
-    if (wscale) BD_GROUPED(EPI_SWIGLU, true, out_plane); else BD_GROUPED(EPI_SWIGLU, false, out_plane);
+    if (wq.fmt == WQ_FP8) BD_GROUPED(EPI_SWIGLU, WQ_FP8, out_plane);
+    else if (wq.fmt == WQ_MXFP4) BD_GROUPED(EPI_SWIGLU, WQ_MXFP4, out_plane);
+    else BD_GROUPED(EPI_SWIGLU, WQ_NONE, out_plane);
   } else {
-    if (wscale) BD_GROUPED(EPI_STORE_F32, true, 0); else BD_GROUPED(EPI_STORE_F32, false, 0);
+    if (wq.fmt == WQ_FP8) BD_GROUPED(EPI_STORE_F32, WQ_FP8, 0);
+    else if (wq.fmt == WQ_MXFP4) BD_GROUPED(EPI_STORE_F32, WQ_MXFP4, 0);
+    else BD_GROUPED(EPI_STORE_F32, WQ_NONE, 0);
   }
 #undef BD_GROUPED
   return hipGetLastError();
@@ -542,12 +628,12 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
   int vt, ty;
   band_tile(u, X, Y, BAND_R, vt, ty);
   const int m0 = ty * TBM, n0 = vt * TBN;
-  BD_GEMM_SMEM(TBM, TBN, false);
+  BD_GEMM_SMEM(TBM, TBN, WQ_NONE);
   __shared__ float red_m[2][TBM], red_s[2][TBM];
   __shared__ int32_t red_a[2][TBM];
   MfmaTile<TBM, TBN> t;
-  mfma_mainloop<TBM, TBN, false>(A, d, a_plane, W, d, 0, d, m0, n0, t, gs0, gs1, gs2, gs3,
-                                 threadIdx.x >> 6);
+  mfma_mainloop<TBM, TBN, WQ_NONE>(A, d, a_plane, W, d, nullptr, 0, d, m0, n0, t, gs0, gs1, gs2, gs3,
+                                   threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 #pragma unroll
@@ -754,22 +840,22 @@ __global__ __launch_bounds__(256) void k_lm_merge(const float* __restrict__ pmax
 
 // ------------------------------------------------------------------ launchers
 
-template <int BM, int BN, bool W8, int NW = 4>
+template <int BM, int BN, int WQ, int NW = 4>
 static void launch_bf16_cfg(int epi, dim3 grid, const bf16_t* a, int lda, size_t ap, const void* w,
                             int ldw, int N, int K, const int32_t* M_dev, void* o, int ldo, size_t op,
-                            float* ws, int zmax, const float* wscale, hipStream_t st) {
+                            float* ws, int zmax, const void* waux, hipStream_t st) {
   switch (epi) {
     case EPI_ADD_F32:
-      k_gemm_bf16<BM, BN, EPI_ADD_F32, W8, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws,
-                                                                 zmax, wscale);
+      k_gemm_bf16<BM, BN, EPI_ADD_F32, WQ, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op, ws,
+                                                                 zmax, waux);
       break;
     case EPI_SWIGLU:
-      k_gemm_bf16<BM, BN, EPI_SWIGLU, W8, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
-                                                                nullptr, 1, wscale);
+      k_gemm_bf16<BM, BN, EPI_SWIGLU, WQ, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
+                                                                nullptr, 1, waux);
       break;
     default:
-      k_gemm_bf16<BM, BN, EPI_STORE_F32, W8, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
-                                                                   nullptr, 1, wscale);
+      k_gemm_bf16<BM, BN, EPI_STORE_F32, WQ, NW><<<grid, 64 * NW, 0, st>>>(a, lda, ap, w, ldw, N, K, M_dev, o, ldo, op,
+                                                                   nullptr, 1, waux);
       break;
   }
 }
@@ -802,27 +888,31 @@ GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid, bool wi
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
                                int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
-                               hipStream_t st, const float* wscale) {
+                               hipStream_t st, WQuant wq) {
   const bool big = p.bm == 128 && p.bn == 128, small = p.bm == 64 && p.bn == 64;
   const bool wide = p.bm == 128 && p.bn == 256;
   if ((!big && !small && !wide) || p.zmax < 1 || p.zmax > 8) return hipErrorInvalidValue;
-  if (wide && wscale) return hipErrorInvalidValue;       // no fp8-weight variant of the wide tile
+  if ((wq.fmt != WQ_NONE) != (wq.aux != nullptr) || wq.fmt < WQ_NONE || wq.fmt > WQ_MXFP4)
+    return hipErrorInvalidValue;
+  if (wide && wq.fmt != WQ_NONE) return hipErrorInvalidValue;   // no quantized variant of the wide tile
   if (N % p.bn || K % KALIGN) return hipErrorInvalidValue;
   if (p.zmax > 1 && (epi != EPI_ADD_F32 || !ws)) return hipErrorInvalidValue;
   // 1-D grid: every (split, column tile, row tile) of the row capacity, + 7
   // (see xcd_item)
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) * p.zmax + 7);
   const bf16_t* a = (const bf16_t*)A;
-#define BD_CFG(BM_, BN_, W8_) \
-  launch_bf16_cfg<BM_, BN_, W8_>(epi, grid, a, lda, a_plane, W, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, \
-                                 wscale, st)
-  if (wscale) {
-    if (big) BD_CFG(128, 128, true); else BD_CFG(64, 64, true);
+#define BD_CFG(BM_, BN_, WQ_) \
+  launch_bf16_cfg<BM_, BN_, WQ_>(epi, grid, a, lda, a_plane, W, ldw, N, K, M_dev, out, ldo, out_plane, ws, p.zmax, \
+                                 wq.aux, st)
+  if (wq.fmt == WQ_FP8) {
+    if (big) BD_CFG(128, 128, WQ_FP8); else BD_CFG(64, 64, WQ_FP8);
+  } else if (wq.fmt == WQ_MXFP4) {
+    if (big) BD_CFG(128, 128, WQ_MXFP4); else BD_CFG(64, 64, WQ_MXFP4);
   } else {
-    if (wide) launch_bf16_cfg<128, 256, false, 8>(epi, grid, a, lda, a_plane, W, ldw, N, K, M_dev, out, ldo,
-                                                   out_plane, ws, p.zmax, wscale, st);
-    else if (big) BD_CFG(128, 128, false);
-    else BD_CFG(64, 64, false);
+    if (wide) launch_bf16_cfg<128, 256, WQ_NONE, 8>(epi, grid, a, lda, a_plane, W, ldw, N, K, M_dev, out, ldo,
+                                                     out_plane, ws, p.zmax, nullptr, st);
+    else if (big) BD_CFG(128, 128, WQ_NONE);
+    else BD_CFG(64, 64, WQ_NONE);
   }
 #undef BD_CFG
   return hipGetLastError();
@@ -856,12 +946,12 @@ GemmPlan plan_resid(int N, int K, int rows_cap, bool wide_ok) {
 hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                              int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
                              int ldx, float* ws, size_t ws_floats, ResidSplit* fold, hipStream_t st,
-                             const float* wscale) {
+                             WQuant wq) {
   fold->ws = nullptr;
   if (!is_bf16 || !ws)
     return launch_gemm(EPI_ADD_F32, is_bf16, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap, X, ldx, 0, st,
-                       wscale);
-  const GemmPlan p = plan_resid(N, K, rows_cap, wscale == nullptr);
+                       wq);
+  const GemmPlan p = plan_resid(N, K, rows_cap, wq.fmt == WQ_NONE);
   ResidSplit r{};
   r.nx = N / p.bn;
   r.bm = p.bm;
@@ -869,7 +959,7 @@ hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plan
   r.zmax = p.zmax;
   if (resid_extent_max(rows_cap, N, r) > ws_floats) return hipErrorInvalidValue;
   hipError_t e = launch_gemm_planned(p, EPI_ADD_F32, A, lda, a_plane, W, ldw, N, K, M_dev, rows_cap,
-                                     X, ldx, 0, ws, st, wscale);
+                                     X, ldx, 0, ws, st, wq);
   if (e != hipSuccess) return e;
   r.ws = ws;
   r.Mp = M_dev;
@@ -879,9 +969,11 @@ hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plan
 
 hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W, int K,
                            const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st,
-                           const float* wscale) {
+                           WQuant wq) {
   const int N = (e.H + 2 * e.Hkv) * e.hd;
   if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
+  if ((wq.fmt != WQ_NONE) != (wq.aux != nullptr) || wq.fmt < WQ_NONE || wq.fmt > WQ_MXFP4)
+    return hipErrorInvalidValue;
   // bf16 weights over windows that fill at least 512 wide tiles: 128x256
   // tiles with 8 waves (3328 x 3072 x 2048: 111 us against 119 in 128x128
   // tiles; per decode 428 -> 383 ms on the multi-block window).  Smaller
@@ -889,17 +981,19 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
   // finer tiling: wide tiles there ran 50% slower (long-prefix 2048-row and
   // MoE 4096-row windows), leaving CUs idle.
   GemmPlan p = plan_gemm(true, N, K, rows_cap, false, false);
-  if (!wscale && N % 256 == 0 && (N / 256) * cdiv(rows_cap, 128) >= 512) p = GemmPlan{128, 256, 1};
+  if (wq.fmt == WQ_NONE && N % 256 == 0 && (N / 256) * cdiv(rows_cap, 128) >= 512) p = GemmPlan{128, 256, 1};
   if (N % p.bn) return hipErrorInvalidValue;
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) + 7);
   const bf16_t* a = (const bf16_t*)A;
-#define BD_QKV(BM_, W8_) k_gemm_qkv<BM_, BM_, W8_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, wscale)
-  if (wscale) {
-    if (p.bm == 128) BD_QKV(128, true); else BD_QKV(64, true);
+#define BD_QKV(BM_, WQ_) k_gemm_qkv<BM_, BM_, WQ_><<<grid, 256, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, wq.aux)
+  if (wq.fmt == WQ_FP8) {
+    if (p.bm == 128) BD_QKV(128, WQ_FP8); else BD_QKV(64, WQ_FP8);
+  } else if (wq.fmt == WQ_MXFP4) {
+    if (p.bm == 128) BD_QKV(128, WQ_MXFP4); else BD_QKV(64, WQ_MXFP4);
   } else if (p.bn == 256) {
-    k_gemm_qkv<128, 256, false, 8><<<grid, 512, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, wscale);
+    k_gemm_qkv<128, 256, WQ_NONE, 8><<<grid, 512, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, nullptr);
   } else {
-    if (p.bm == 128) BD_QKV(128, false); else BD_QKV(64, false);
+    if (p.bm == 128) BD_QKV(128, WQ_NONE); else BD_QKV(64, WQ_NONE);
   }
 #undef BD_QKV
   return hipGetLastError();
@@ -907,11 +1001,11 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
 
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       size_t out_plane, hipStream_t st, const float* wscale) {
+                       size_t out_plane, hipStream_t st, WQuant wq) {
   if (is_bf16)
-    return launch_gemm_planned(plan_gemm(true, N, K, rows_cap, false, wscale == nullptr), epi, A, lda, a_plane,
-                               W, ldw, N, K, M_dev, rows_cap, out, ldo, out_plane, nullptr, st, wscale);
-  if (wscale) return hipErrorInvalidValue;
+    return launch_gemm_planned(plan_gemm(true, N, K, rows_cap, false, wq.fmt == WQ_NONE), epi, A, lda, a_plane,
+                               W, ldw, N, K, M_dev, rows_cap, out, ldo, out_plane, nullptr, st, wq);
+  if (wq.fmt != WQ_NONE) return hipErrorInvalidValue;
   if (N % SBN || K % SBK) return hipErrorInvalidValue;
   dim3 grid(N / SBN, cdiv(rows_cap, SBM));
   const float* a = (const float*)A;

@@ -97,6 +97,20 @@ size_t resid_extent(int M, int N, const ResidSplit& r);
 // workspace a state must hold for that projection.
 size_t resid_extent_max(int rows_cap, int N, const ResidSplit& r);
 
+// Quantized projection weights (bf16 models).  fmt WQ_NONE (aux NULL): W
+// holds bf16 [N][K].  WQ_FP8: W holds OCP fp8 E4M3 codes [N][K] and aux the
+// float power-of-two scale of each row [N].  WQ_MXFP4: W holds E2M1 codes
+// stage-major, [K/32][N][16 bytes] (element 2j of a 32-element block in the
+// low nibble of byte j, element 2j + 1 in the high nibble), and aux the E8M0
+// block exponents [K/32][N] (scale 2^(e - 127)); a matrix of grouped experts
+// holds one such block per expert, expert after expert.
+enum { WQ_NONE = 0, WQ_FP8 = 1, WQ_MXFP4 = 2 };
+struct WQuant {
+  int fmt = WQ_NONE;
+  const void* aux = nullptr;
+};
+constexpr int MX_BLOCK = 32;
+
 // ---- launchers (defined in the .hip files) ---------------------------------
 // C[M][N] (+)= A[M][K] . W[N][K]^T with M read from *M_dev; grid covers rows_cap.
 // bf16 models: A is a bf16 plane pair (hi at A, lo at A + a_plane elements),
@@ -104,11 +118,11 @@ size_t resid_extent_max(int rows_cap, int N, const ResidSplit& r);
 //   EPI_STORE_F32 / EPI_ADD_F32: out fp32 [M][ldo]
 //   EPI_SWIGLU: silu(gate) * up [M][ldo] (W packed gate/up in 16-row groups),
 //   as a bf16 plane pair (out_plane) for bf16 models, fp32 otherwise
-// wscale (bf16 models only): NULL for bf16 weights; otherwise W holds fp8
-// E4M3 codes [N][K] and wscale[N] the power-of-two scale of each row.
+// wq (bf16 models only): the weight format (WQuant); ldw is W's row stride in
+// elements for bf16 and fp8 weights and unused for MXFP4 (N rows per block).
 hipError_t launch_gemm(int epi, bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                        int ldw, int N, int K, const int32_t* M_dev, int rows_cap, void* out, int ldo,
-                       size_t out_plane, hipStream_t st, const float* wscale = nullptr);
+                       size_t out_plane, hipStream_t st, WQuant wq = WQuant{});
 // Expert tiles of a grouped GEMM (all device pointers).
 struct GroupTiles {
   const int32_t* tile_e;    // [max_tiles] expert of each tile
@@ -117,14 +131,15 @@ struct GroupTiles {
   const int32_t* e_off;     // [E] first expert-sorted row of each expert
   const int32_t* e_cnt;     // [E] rows of each expert
   const int32_t* a_rows;    // optional [assignments] token row of each sorted row
-  size_t w_stride;          // elements between consecutive experts' weights
+  size_t w_stride;          // weight elements per expert (N x K)
 };
 constexpr int GROUP_BM = 128;
 // out rows are expert-sorted rows; EPI_SWIGLU writes bf16 planes, EPI_STORE_F32 fp32.
-// wscale: as launch_gemm, [E][N] (expert e's scales at wscale + e N).
+// wq: as launch_gemm; fp8 row scales [E][N], MXFP4 codes and exponents one
+// stage-major block per expert.
 hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, const void* W,
                                int ldw, int N, int K, const GroupTiles& g, int max_tiles, void* out,
-                               int ldo, size_t out_plane, const float* wscale, hipStream_t st);
+                               int ldo, size_t out_plane, WQuant wq, hipStream_t st);
 
 // MoE routing: softmax over E router logits (fp32 weights [E][d]), top_k
 // experts (lowest id among equals), weights renormalised.
@@ -158,7 +173,7 @@ GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid = false,
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
                                int rows_cap, void* out, int ldo, size_t out_plane, float* ws,
-                               hipStream_t st, const float* wscale = nullptr);
+                               hipStream_t st, WQuant wq = WQuant{});
 // Plan of a residual projection (O and down of bf16 models): tile shape and
 // the largest K-split (zmax).
 GemmPlan plan_resid(int N, int K, int rows_cap, bool wide_ok);
@@ -171,7 +186,7 @@ GemmPlan plan_resid(int N, int K, int rows_cap, bool wide_ok);
 hipError_t launch_gemm_resid(bool is_bf16, const void* A, int lda, size_t a_plane, const void* W,
                              int ldw, int N, int K, const int32_t* M_dev, int rows_cap, float* X,
                              int ldx, float* ws, size_t ws_floats, ResidSplit* fold, hipStream_t st,
-                             const float* wscale = nullptr);
+                             WQuant wq = WQuant{});
 
 // LM head: per-row softmax statistics over the vocabulary of
 // z = scale * (A . W^T), mask column suppressed.  Writes per-(tile,row)
@@ -299,6 +314,15 @@ hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 // fp8 E4M3 codes of a bf16 matrix [rows][cols], one power-of-two scale per
 // row (scale[row] = 2^E, the smallest with max |w| / 2^E <= 448).
 hipError_t launch_quant_fp8_rows(const void* W, int rows, int cols, uint8_t* Q, float* scale, hipStream_t st);
+// MXFP4 (E2M1 codes, one E8M0 exponent per 32 consecutive elements of a row)
+// of a bf16 matrix [rows][cols], cols % 32 == 0, in the stage-major layout of
+// WQuant, the rows taken in groups of group_rows (rows % group_rows == 0), each
+// group its own block: codes[g][cols/32][group_rows][16], exps[g][cols/32][group_rows].
+// Exponent X = floor(log2 max|w|) - 2 over the block (-127 for an all-zero
+// block, clamped to [-127, 127]); element code = the E2M1 value nearest to
+// w / 2^X, ties to the even mantissa, magnitudes above 6 saturating.
+hipError_t launch_quant_mxfp4_rows(const void* W, int rows, int cols, int group_rows, uint8_t* codes,
+                                   uint8_t* exps, hipStream_t st);
 
 struct InitArgs {
   PlanView plan;            // step plan to build
@@ -337,7 +361,7 @@ struct QkvEpi {
 };
 hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W, int K,
                            const int32_t* M_dev, int rows_cap, const QkvEpi& e, hipStream_t st,
-                           const float* wscale = nullptr);
+                           WQuant wq = WQuant{});
 // Copy of a [(H + 2 Hkv) hd][d] QKV weight with the q and k head rows
 // pair-interleaved (see QkvEpi); v rows unchanged.
 hipError_t launch_permute_qk_rows(const void* W, void* out, int H, int Hkv, int hd, size_t row_bytes,

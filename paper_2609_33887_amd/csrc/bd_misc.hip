@@ -661,6 +661,76 @@ hipError_t launch_quant_fp8_rows(const void* W, int rows, int cols, uint8_t* Q, 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ MXFP4 weights
+// Nearest E2M1 code (ties to even, magnitudes above 6 saturating): the
+// spacing of representable values is 2^(floor(log2|v|) - 1) from 1 up and 0.5
+// below; the rounded magnitude q (at most 6) is then split into exponent and
+// mantissa fields.  Exact in fp32 except the one rounding of rintf.
+__device__ __forceinline__ uint32_t e2m1_code(float v) {
+  const float a = fabsf(v);
+  uint32_t code = 0;
+  if (a > 0.f) {
+    int ea;
+    (void)frexpf(a, &ea);                       // a = f 2^ea, 0.5 <= f < 1
+    const int qe = a >= 1.f ? ea - 2 : -1;
+    const float q = fminf(ldexpf(rintf(ldexpf(a, -qe)), qe), 6.f);
+    if (q >= 1.f) {
+      int eq;
+      (void)frexpf(q, &eq);
+      code = ((uint32_t)eq << 1) | (uint32_t)(ldexpf(q, 2 - eq) - 2.f);
+    } else {
+      code = (uint32_t)(q * 2.f);
+    }
+  }
+  return v < 0.f ? (code | 8u) : code;
+}
+
+// One thread per (row group, block, row): the block's largest magnitude
+// amax = f 2^x gives the exponent X = x - 3 = floor(log2 amax) - 2 (-127 for
+// a zero block; clamped to E8M0's [-127, 127]), then each element is coded as
+// w / 2^X (exact: a power-of-two scaling of a bf16 value).  Threads of
+// consecutive rows write consecutive 16-byte code rows.
+__global__ __launch_bounds__(256) void k_quant_mxfp4_rows(const bf16_t* __restrict__ W, int rows, int cols,
+                                                          int group_rows, uint8_t* __restrict__ codes,
+                                                          uint8_t* __restrict__ exps) {
+  const int nb = cols / MX_BLOCK;
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (size_t)rows * nb) return;
+  const int r = (int)(idx % group_rows);
+  const size_t gk = idx / group_rows;             // g * nb + kb
+  const int kb = (int)(gk % nb), g = (int)(gk / nb);
+  const bf16_t* w = W + ((size_t)g * group_rows + r) * cols + (size_t)kb * MX_BLOCK;
+  float v[MX_BLOCK];
+  float amax = 0.f;
+#pragma unroll
+  for (int j = 0; j < MX_BLOCK; ++j) {
+    v[j] = bf2f_m(w[j]);
+    amax = fmaxf(amax, fabsf(v[j]));
+  }
+  int X = -127;
+  if (amax > 0.f) {
+    int x;
+    (void)frexpf(amax, &x);
+    X = x - 3;
+    X = X < -127 ? -127 : (X > 127 ? 127 : X);
+  }
+  uint32_t packed[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int j = 0; j < MX_BLOCK; ++j) packed[j >> 3] |= e2m1_code(ldexpf(v[j], -X)) << (4 * (j & 7));
+  *(uint4*)(codes + idx * 16) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+  exps[idx] = (uint8_t)(X + 127);
+}
+
+hipError_t launch_quant_mxfp4_rows(const void* W, int rows, int cols, int group_rows, uint8_t* codes,
+                                   uint8_t* exps, hipStream_t st) {
+  if (rows < 1 || cols < MX_BLOCK || cols % MX_BLOCK || group_rows < 1 || rows % group_rows)
+    return hipErrorInvalidValue;
+  const size_t n = (size_t)rows * (cols / MX_BLOCK);
+  k_quant_mxfp4_rows<<<(unsigned)((n + 255) / 256), 256, 0, st>>>((const bf16_t*)W, rows, cols, group_rows, codes,
+                                                                  exps);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ debug
 __global__ void k_scatter_logits(const float* __restrict__ logits, const int32_t* __restrict__ hdr,
                                  const int32_t* __restrict__ lm_row,

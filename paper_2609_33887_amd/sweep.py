@@ -85,8 +85,9 @@ def redline_sweep(model, prompts, G, B, candidates, reference, alpha, delta, tai
 
 def weight_bytes(w, wq=None) -> int:
     """Weight memory of a model as the library holds it: decoder-layer
-    projections in bf16 (2 bytes) or fp8 (1 byte plus a 4-byte scale per
-    row); embeddings and LM head in bf16; norms and router in fp32."""
+    projections in bf16 (2 bytes), fp8 (1 byte plus a 4-byte scale per row)
+    or MXFP4 (half a byte plus a 1-byte exponent per 32 elements);
+    embeddings and LM head in bf16; norms and router in fp32."""
     d, hd = w.d_model, w.head_dim
     proj = [((w.n_heads + 2 * w.n_kv_heads) * hd, d), (d, w.n_heads * hd)]
     if w.n_experts == 0:
@@ -96,7 +97,12 @@ def weight_bytes(w, wq=None) -> int:
         proj += [(w.n_experts * 2 * Fe, d), (w.n_experts * d, Fe)]
         if Fs:
             proj += [(2 * Fs, d), (d, Fs)]
-    per_row = (lambda r, c: r * c + 4 * r) if wq == "fp8" else (lambda r, c: 2 * r * c)
+    if wq == "fp8":
+        per_row = lambda r, c: r * c + 4 * r
+    elif wq == "mxfp4":
+        per_row = lambda r, c: r * c // 2 + r * c // 32
+    else:
+        per_row = lambda r, c: 2 * r * c
     layer = sum(per_row(r, c) for r, c in proj) + 4 * 2 * d + (4 * w.n_experts * d if w.n_experts else 0)
     return w.n_layers * layer + 2 * 2 * w.vocab * d + 4 * d
 
@@ -104,7 +110,7 @@ def weight_bytes(w, wq=None) -> int:
 def precision_sweep(w, models, prompts, G, B, reference, candidates, alpha, delta, tail=16, batch=64,
                     progress=None, method="holm"):
     """reference / candidates: (precision, decode config) with precision a
-    key of ``models`` ("bf16" or "fp8").  Correctness as in redline_sweep;
+    key of ``models`` ("bf16", "fp8" or "mxfp4").  Correctness as in redline_sweep;
     the cost measure is the weight-memory reduction against the reference
     (larger is better), so the deployed configuration is the valid one with
     the least weight memory (first listed among equals)."""
@@ -146,9 +152,9 @@ def main():
     prompts = make_prompts(w, args.prompts)
     say = lambda m: print(m, file=sys.stderr, flush=True)
     if args.grid == "precision":
-        models = {"bf16": model, "fp8": bd.Model(w, weights, wq="fp8")}
+        models = {"bf16": model, "fp8": bd.Model(w, weights, wq="fp8"), "mxfp4": bd.Model(w, weights, wq="mxfp4")}
         ref = ("bf16", (0.9, w.n_inflight))
-        cands = [("fp8", (t, w.n_inflight)) for t in (0.9, 0.8)]
+        cands = [(prec, (t, w.n_inflight)) for prec in ("fp8", "mxfp4") for t in (0.9, 0.8)]
         r = precision_sweep(w, models, prompts, w.gen_len, w.block_size, ref, cands, args.alpha, args.delta,
                             batch=w.batch, progress=say, method=args.method)
         print(json.dumps({"workload": w.name, "prompts": args.prompts, "alpha": args.alpha,

@@ -255,7 +255,8 @@ def test_weight_bytes_counts_every_tensor():
     """The weight-memory cost of the precision sweep against a count over
     the ABI tensor list: bf16 matrices 2 bytes, fp32 norms and router 4;
     with fp8 the decoder-layer projections take 1 byte plus a 4-byte scale
-    per output row."""
+    per output row, with MXFP4 half a byte plus a 1-byte exponent per 32
+    elements."""
     import numpy as np
     from bd_synth import Workload, tensor_specs
     from oracle.quant import quantized_layer_slots
@@ -267,7 +268,7 @@ def test_weight_bytes_counts_every_tensor():
                      **kw)
         specs = tensor_specs(w)
         slots = set(quantized_layer_slots(w))
-        bf16 = fp8 = 0
+        bf16 = fp8 = mx = 0
         for i, (name, shape, kind) in enumerate(specs):
             n = int(np.prod(shape))
             if n == 0:
@@ -275,8 +276,10 @@ def test_weight_bytes_counts_every_tensor():
             size = 4 * n if kind in ("norm", "router") else 2 * n
             bf16 += size
             fp8 += (n + 4 * (n // shape[-1])) if i in slots else size
+            mx += (n // 2 + n // 32) if i in slots else size
         assert weight_bytes(w) == bf16
         assert weight_bytes(w, "fp8") == fp8
+        assert weight_bytes(w, "mxfp4") == mx
 
 
 def test_argument_errors_before_any_device_work():

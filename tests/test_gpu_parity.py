@@ -84,8 +84,9 @@ _prefills = {}
 
 
 def get_model(w, wq=None):
-    """The GPU model and the weights the oracle uses: for fp8 models the
-    oracle's own quantization of the layer projections, dequantized."""
+    """The GPU model and the weights the oracle uses: for fp8 and MXFP4
+    models the oracle's own quantization of the layer projections,
+    dequantized."""
     from paper_2609_33887_amd import bd
     key = (w.name, w.seed, wq)
     if key not in _models:
@@ -102,6 +103,9 @@ def get_model(w, wq=None):
         if wq == "fp8":
             from oracle.quant import fp8_weights
             ws = fp8_weights(w, ws)
+        elif wq == "mxfp4":
+            from oracle.quant import mxfp4_weights
+            ws = mxfp4_weights(w, ws)
         _models[key] = (model, ws)
     return _models[key]
 
@@ -317,36 +321,102 @@ def test_dense_1024_fp8_full_size():
     run_parity(workload(1), 0.9, seq_ids=[3], logits=True, logit_every=8, wq="fp8")
 
 
+def _unpack_mxfp4(codes, exps):
+    """Library layout (codes [G][nb][R][16], exps [G][nb][R]) -> codes
+    [rows][cols] one per element and exponents X [rows][nb]."""
+    G, nb, R, _ = codes.shape
+    lo, hi = codes & 15, codes >> 4
+    el = np.stack([lo, hi], axis=-1).reshape(G, nb, R, 32)          # element 2k, 2k + 1
+    c = el.transpose(0, 2, 1, 3).reshape(G * R, nb * 32)
+    x = exps.astype(np.int64).transpose(0, 2, 1).reshape(G * R, nb) - 127
+    return c, x
+
+
+def test_quantize_mxfp4_matches_oracle():
+    """bd_quantize_mxfp4 against oracle.quant.quantize_mxfp4_rows, code for
+    code and exponent for exponent: random bf16 rows at four magnitudes,
+    all-zero blocks, every rounding midpoint between neighbouring E2M1 values
+    at block scale 1 (ties to the even mantissa), magnitudes above 6 that
+    saturate, and a matrix taken in two groups of rows (one block per group,
+    as the library keeps stacked experts)."""
+    from paper_2609_33887_amd import bd
+    from oracle.quant import quantize_mxfp4_rows
+    from bd_synth import f32_to_bf16_bits
+    _need_gpu()
+    rng = np.random.default_rng(43)
+    cols = 256
+    rows = [rng.normal(0, s, cols) for s in (0.02, 1.0, 1e-4, 37.0)]
+    z = rng.normal(0, 1.0, cols)
+    z[32:64] = 0.0
+    z[128:160] = 0.0
+    rows.append(z)
+    rows.append(np.zeros(cols))
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0])
+    r = np.zeros(cols)
+    for b in range(cols // 32):
+        blk = np.concatenate([mids, -mids, [6.0 if b % 2 else 4.0], [6.5, 7.0, 7.5][: b % 3]])
+        r[32 * b: 32 * b + len(blk)] = blk * 2.0 ** (b - 3)
+    rows.append(r)
+    rows.append(-r[::-1])
+    W = np.stack(rows)
+    bits = f32_to_bf16_bits(W.astype(np.float32))
+    wb = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    oc, ox = quantize_mxfp4_rows(wb)
+    for group_rows in (W.shape[0], W.shape[0] // 2):
+        codes, exps = bd.quantize_mxfp4(bits, group_rows)
+        c, x = _unpack_mxfp4(codes, exps)
+        np.testing.assert_array_equal(x, ox)
+        np.testing.assert_array_equal(c, oc)
+
+
+@pytest.mark.parametrize("name", ["mha64", "gqa128_ragged", "moe", "stream128"])
+@pytest.mark.parametrize("tau", [0.9, 0.7])
+def test_small_models_mxfp4(name, tau):
+    """MXFP4 decoder-layer weights (E2M1 with an E8M0 exponent per 32
+    elements): the GPU decode against the oracle run on the oracle's own
+    MXFP4 quantization of the weights, at the bf16 tolerances."""
+    run_parity(SMALL[name], tau, wq="mxfp4")
+
+
+def test_dense_1024_mxfp4_full_size():
+    """Full-size dense model with MXFP4 layer weights at tau 0.9: the GPU
+    decodes the batch, the oracle replays sequence 3."""
+    run_parity(workload(1), 0.9, seq_ids=[3], logits=True, logit_every=8, wq="mxfp4")
+
+
 def test_precision_sweep_matches_oracle():
     """Redline over the precision axis on the small MHA model, 48 calibration
     prompts: bf16 weights at acc 0.9 as the reference, fp8 layer weights at
-    acc 0.9 and 0.8 as candidates, cost = weight-memory reduction.  Counts,
-    valid set and the deployed configuration equal the oracle's on the
-    GPU-decoded matrix (each fp8 decode is checked against the oracle by
-    test_small_models_fp8)."""
+    acc 0.9 and 0.8 and MXFP4 layer weights at acc 0.9 as candidates, cost =
+    weight-memory reduction.  Counts, valid set and the deployed
+    configuration equal the oracle's on the GPU-decoded matrix (each
+    quantized decode is checked against the oracle by test_small_models_fp8
+    and test_small_models_mxfp4)."""
     from paper_2609_33887_amd import bd
     from paper_2609_33887_amd.sweep import precision_sweep, weight_bytes
     from oracle import redline as orl
     _need_gpu()
     w = SMALL["mha64"]
-    models = {"bf16": get_model(w)[0], "fp8": get_model(w, "fp8")[0]}
+    models = {"bf16": get_model(w)[0], "fp8": get_model(w, "fp8")[0], "mxfp4": get_model(w, "mxfp4")[0]}
     prompts = make_prompts(w, 48)
     r = precision_sweep(w, models, prompts, w.gen_len, w.block_size, ("bf16", (0.9, 2)),
-                        [("fp8", (0.9, 2)), ("fp8", (0.8, 2))], 0.10, 0.10, tail=8, batch=16, progress=_say)
-    assert r["weight_bytes"][1] < r["weight_bytes"][0] == weight_bytes(w)
+                        [("fp8", (0.9, 2)), ("fp8", (0.8, 2)), ("mxfp4", (0.9, 2))], 0.10, 0.10, tail=8,
+                        batch=16, progress=_say)
+    assert r["weight_bytes"][3] < r["weight_bytes"][1] < r["weight_bytes"][0] == weight_bytes(w)
     o = orl.select(r["correct"], r["cost"], 0, 0.10, 0.10)
     assert r["V"].tolist() == o.V.tolist() and r["valid"].tolist() == o.valid.tolist()
     assert r["selected"] == o.selected
     _say(f"  V {r['V'].tolist()} valid {r['valid'].tolist()} deployed {r['labels'][r['selected']]}")
 
 
-def test_fp8_model_errors():
+def test_quantized_model_errors():
     from paper_2609_33887_amd import bd
     _need_gpu()
     w = SMALL["f32_gqa"]
-    with pytest.raises(bd.BDError) as e:
-        bd.Model(w, make_weights(w), wq="fp8")
-    assert e.value.status == bd.BD_EUNSUPPORTED
+    for wq in ("fp8", "mxfp4"):
+        with pytest.raises(bd.BDError) as e:
+            bd.Model(w, make_weights(w), wq=wq)
+        assert e.value.status == bd.BD_EUNSUPPORTED
     w = SMALL["mha64"]
     cfg = bd.model_cfg_from(w)
     cfg.wq = 7
@@ -356,6 +426,14 @@ def test_fp8_model_errors():
     with pytest.raises(bd.BDError) as e:
         bd.bd_quantize_fp8(0, 4, 4, 0, 0)
     assert e.value.status == bd.BD_EINVAL
+    import torch
+    buf = torch.zeros(4096, dtype=torch.uint8, device="cuda:0")
+    p = buf.data_ptr()
+    for args in ((0, 4, 64, 4, p, p), (p, 4, 64, 4, 0, p), (p, 4, 48, 4, p, p), (p, 6, 64, 4, p, p),
+                 (p, 0, 64, 1, p, p), (p, 4, 64, 0, p, p)):
+        with pytest.raises(bd.BDError) as e:
+            bd.bd_quantize_mxfp4(*args)
+        assert e.value.status == bd.BD_EINVAL
 
 
 def test_tiny_256_f32():
