@@ -9,7 +9,8 @@
 // each 32-key group in the slot order of vt_slot): one workgroup =
 // 16 NW queries of one (sequence, kv head) -- window rows x the q-heads that
 // share the kv head -- as NW wave64s x 16 queries (NW = 2 when a window
-// holds at most 32 such queries, else 4); a wave with no query of its own
+// holds at most 32 such queries, 8 for 512 or more over long key ranges,
+// else 4); a wave with no query of its own
 // only helps stage the tiles.  Key tiles of 64
 // positions stream from HBM through LDS with 16-byte coalesced loads (K rows
 // and V^T tile rows, each tile a contiguous block), and the wave computes
@@ -371,19 +372,27 @@ __global__ __launch_bounds__(256) void k_attn_f32(const float* __restrict__ Q,
   for (int e = 0; e < per; ++e) o[lane * per + e] = acc[e] / l;
 }
 
-// waves per workgroup for a window of win_cap rows (see k_attn_bf16)
-static int attention_waves(int win_cap, int H, int Hkv) { return (H / Hkv) * win_cap <= 32 ? 2 : 4; }
+// waves per workgroup for a window of win_cap rows over a key capacity of
+// maxpos (see k_attn_bf16): 8 waves (128 queries per staged K/V tile) where a
+// kv head has at least 512 window queries over at least 4096 keys -- the
+// long-prefix decode's attention ran 7% faster than with 4 waves (484 -> 449
+// ms per decode), the multi-block one (2048 keys) 2.5% slower
+static int attention_waves(int win_cap, int H, int Hkv, int maxpos) {
+  const int q = (H / Hkv) * win_cap;
+  return q <= 32 ? 2 : (q >= 512 && maxpos >= 4096 ? 8 : 4);
+}
 
 int attention_splits(int b, int win_cap, int rows_est, int H, int Hkv, int hd, int maxpos) {
   // the launch shape follows win_cap (the largest window); the work estimate
   // follows rows_est, the rows a window usually holds
-  const int nw = attention_waves(win_cap, H, Hkv);
+  const int nw = attention_waves(win_cap, H, Hkv, maxpos);
   const int wgs = (((H / Hkv) * rows_est + 16 * nw - 1) / (16 * nw)) * Hkv * b;
   // workgroups resident per CU (LDS-bound: 37 KB per workgroup at hd 64,
-  // 72 KB at hd 128; 3 of the 4-wave hd-64 kind): split the key range until
+  // 72 KB at hd 128; registers hold the 4-wave hd-64 kind to 3 and the
+  // 8-wave kinds to 1): split the key range until
   // the grid fills one resident round of 256 CUs, while every split keeps
   // >= 2 key tiles of the longest range
-  const int round = (hd == 64 ? (nw == 2 ? 4 : 3) : 2) * 256;
+  const int round = (nw == 8 ? 1 : (hd == 64 ? (nw == 2 ? 4 : 3) : 2)) * 256;
   int splits = 1;
   while (wgs * (splits + 1) <= round && maxpos / (AK * (splits + 1)) >= 2 && splits < 16) ++splits;
   return splits;
@@ -401,7 +410,7 @@ hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const K
     const bf16_t* k = (const bf16_t*)kv.K;
     const bf16_t* v = (const bf16_t*)kv.V;
     if (kv_splits < 1 || (kv_splits > 1 && (!ws_o || !ws_ml))) return hipErrorInvalidValue;
-    const int nw = attention_waves(win_cap, H, Hkv);
+    const int nw = attention_waves(win_cap, H, Hkv, kv.maxpos);
     const int nqt = ((H / Hkv) * win_cap + 16 * nw - 1) / (16 * nw);
     const int grid = b * Hkv * kv_splits * nqt + 7;
 #define BD_ATTN(HD_, NW_)                                                                     \
@@ -410,9 +419,9 @@ hipError_t launch_attention(bool is_bf16, const void* Q, size_t q_plane, const K
       plan.seq_row_start, plan.seq_win_len, plan.seq_win_start, H, Hkv, kv.maxpos, B,         \
       scale_log2, kv_splits, ws_o, ws_ml, rows_cap, b, nqt)
     if (hd == 128) {
-      if (nw == 2) BD_ATTN(128, 2); else BD_ATTN(128, 4);
+      if (nw == 2) BD_ATTN(128, 2); else if (nw == 8) BD_ATTN(128, 8); else BD_ATTN(128, 4);
     } else {
-      if (nw == 2) BD_ATTN(64, 2); else BD_ATTN(64, 4);
+      if (nw == 2) BD_ATTN(64, 2); else if (nw == 8) BD_ATTN(64, 8); else BD_ATTN(64, 4);
     }
 #undef BD_ATTN
     if (kv_splits > 1) {

@@ -161,6 +161,26 @@ def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=No
     return tr, reps[modes[0]]
 
 
+# Long key ranges with at least 512 window queries per kv head (four q-heads
+# per kv head, blocks of 64, two in flight, 4096-token prompts): the
+# attention's 8-wave workgroups, at head_dim 128 and 64
+LONG_SMALL = {
+    "prefix8w": small("prefix8w", seed=103, n_heads=8, n_kv_heads=2, head_dim=128, batch=2, prompt_len=4096,
+                      block_size=64, n_inflight=2, gen_len=128),
+    "prefix8w64": small("prefix8w64", seed=104, n_heads=8, n_kv_heads=2, head_dim=64, batch=2,
+                        prompt_len=4096, block_size=64, n_inflight=2, gen_len=128),
+}
+
+
+@pytest.mark.parametrize("name", list(LONG_SMALL))
+def test_small_long_prefix_eight_waves(name):
+    """Small models whose windows hold 1,024 queries per kv head over 4,224
+    keys, decoded at tau 0.9: the attention takes its 8-wave workgroups
+    (long-prefix regime); the GPU decodes both sequences, the plain f64
+    oracle replays sequence 1 (about 15 s of oracle time)."""
+    run_parity(LONG_SMALL[name], 0.9, seq_ids=[1])
+
+
 @pytest.mark.parametrize("name", list(SMALL))
 @pytest.mark.parametrize("tau", [0.95, 0.9, 0.8, 0.7])
 def test_small_models(name, tau):
