@@ -88,6 +88,12 @@ def capture_gpu_trace(model, prompts, G, tau, nb, B, logits_for=(), max_steps=No
 class Report:
     max_conf_diff: float = 0.0
     max_logit_diff: float = 0.0
+    # the same maxima over the compared steps whose routing had no near-tie
+    # (MoE: every row's k-th and (k+1)-th router logits more than ROUTER_NEAR
+    # apart in the oracle's forward; equal to the above for dense models)
+    max_conf_diff_routed: float = 0.0
+    max_logit_diff_routed: float = 0.0
+    route_near_steps: int = 0        # compared steps with a routing near-tie that still passed
     t1: int = 0
     t2: int = 0
     t3: int = 0
@@ -203,6 +209,11 @@ def lockstep(oracle_model, prompts, seq_ids, trace: GpuTrace, G, tau, nb, B, con
                 rep.positions += len(masked)
                 rep.max_conf_diff = max(rep.max_conf_diff, cdiff)
                 rep.max_logit_diff = max(rep.max_logit_diff, ldiff)
+                if near_route:
+                    rep.route_near_steps += 1
+                else:
+                    rep.max_conf_diff_routed = max(rep.max_conf_diff_routed, cdiff)
+                    rep.max_logit_diff_routed = max(rep.max_logit_diff_routed, ldiff)
             d.count_participation(masked[gsel])
             d.apply(masked[gsel], gtoks[gsel], step)
             step += 1

@@ -148,6 +148,9 @@ def run_parity(w, tau, seq_ids=None, logits=True, max_steps=None, logit_steps=No
         _say(f"  oracle {mode}: positions={rep.positions} max|dconf|={rep.max_conf_diff:.3g} "
              f"max|dlogit|={rep.max_logit_diff:.3g} near-ties T1={rep.t1} T2={rep.t2} T3={rep.t3} "
              f"T4(steps)={rep.t4} complete={rep.complete} TPF={w.gen_len * w.batch / tr.forwards.sum():.4f}")
+        if rep.route_near_steps:
+            _say(f"  steps with a routing near-tie (passed): {rep.route_near_steps}; without: max|dconf|="
+                 f"{rep.max_conf_diff_routed:.3g} max|dlogit|={rep.max_logit_diff_routed:.3g}")
         assert not rep.failures, rep.failures[:5]
         assert rep.max_conf_diff <= ctol
         assert rep.max_logit_diff <= ltol
