@@ -974,14 +974,18 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
   if (e.hd % 16 || e.kv.vstride % 64 || K % KALIGN) return hipErrorInvalidValue;
   if ((wq.fmt != WQ_NONE) != (wq.aux != nullptr) || wq.fmt < WQ_NONE || wq.fmt > WQ_MXFP4)
     return hipErrorInvalidValue;
-  // bf16 weights over windows that fill at least 512 wide tiles: 128x256
-  // tiles with 8 waves (3328 x 3072 x 2048: 111 us against 119 in 128x128
-  // tiles; per decode 428 -> 383 ms on the multi-block window).  Smaller
-  // windows, whose live rows often fall well below the capacity, keep the
-  // finer tiling: wide tiles there ran 50% slower (long-prefix 2048-row and
-  // MoE 4096-row windows), leaving CUs idle.
+  // bf16 weights where the product would fill at least 512 tiles of 128 x 256
+  // over the row capacity (the 6144-row multi-block window of a 3072-wide
+  // QKV): 128x128 tiles with 8 waves of 64 x 32.  Per
+  // decode, QKV took 428 ms in 4-wave 128x128 tiles, 383 in 8-wave 128x256
+  // tiles (312 tiles for 256 CUs: a nearly empty second round) and 335 in
+  // 8-wave 128x128 tiles (624 tiles, three half-length rounds).  The MoE
+  // (4096-row) and long-prefix (2048-row) windows, whose live rows fall well
+  // below the capacity, keep the 4-wave tiling: 8-wave tiles there ran 13%
+  // slower and no faster.
   GemmPlan p = plan_gemm(true, N, K, rows_cap, false, false);
-  if (wq.fmt == WQ_NONE && N % 256 == 0 && (N / 256) * cdiv(rows_cap, 128) >= 512) p = GemmPlan{128, 256, 1};
+  const bool eight = wq.fmt == WQ_NONE && N % 256 == 0 && (N / 256) * cdiv(rows_cap, 128) >= 512;
+  if (eight) p = GemmPlan{128, 128, 1};
   if (N % p.bn) return hipErrorInvalidValue;
   dim3 grid((N / p.bn) * cdiv(rows_cap, p.bm) + 7);
   const bf16_t* a = (const bf16_t*)A;
@@ -990,8 +994,8 @@ hipError_t launch_gemm_qkv(const void* A, int lda, size_t a_plane, const void* W
     if (p.bm == 128) BD_QKV(128, WQ_FP8); else BD_QKV(64, WQ_FP8);
   } else if (wq.fmt == WQ_MXFP4) {
     if (p.bm == 128) BD_QKV(128, WQ_MXFP4); else BD_QKV(64, WQ_MXFP4);
-  } else if (p.bn == 256) {
-    k_gemm_qkv<128, 256, WQ_NONE, 8><<<grid, 512, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, nullptr);
+  } else if (eight) {
+    k_gemm_qkv<128, 128, WQ_NONE, 8><<<grid, 512, 0, st>>>(a, lda, a_plane, W, K, M_dev, e, nullptr);
   } else {
     if (p.bm == 128) BD_QKV(128, WQ_NONE); else BD_QKV(64, WQ_NONE);
   }
