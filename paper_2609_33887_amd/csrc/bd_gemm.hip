@@ -3,12 +3,14 @@
 // All products are C = A . W^T with A [rows][K] (activations, row-major) and
 // W [N][K] (weights stored [out][in]), so both operands are K-contiguous.
 //
-// bf16 path (bf16 weights, activations as bf16 hi/lo plane pairs): 128x128
-// or 64x64 workgroup tiles, 4 wave64s in a 2x2 arrangement, MFMA 16x16x32
-// bf16 with fp32 accumulate.  Operands reach LDS through direct
-// global-to-LDS loads into a four-stage ring (K-stages of 32, swizzled rows);
-// one barrier per stage; the residual projections may split K (the partial
-// sums are folded in by the next RMSNorm).
+// bf16 path (bf16 weights, activations as bf16 hi/lo plane pairs): workgroup
+// tiles of 128x256 (8 wave64s of 64x64), 128x128 (4 waves of 64x64, or 8 of
+// 64x32) or 64x64 (4 waves of 32x32), the waves in a 2 x (waves / 2)
+// arrangement, MFMA 16x16x32 bf16 with fp32 accumulate (plan_gemm and the
+// launchers choose).  Operands reach LDS through direct global-to-LDS loads
+// into a four-stage ring (K-stages of 32, swizzled rows); one barrier per
+// stage; the residual projections may split K (the partial sums are folded
+// in by the next RMSNorm).
 // fp8 weights (WQ = WQ_FP8): W holds OCP fp8 E4M3 codes, one byte per
 // element, with a power-of-two scale per output row; the W stage holds
 // 32-byte rows, each lane converts its 8 codes of a fragment to bf16 (exact)
