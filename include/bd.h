@@ -197,7 +197,11 @@ bd_status bd_quantize_mxfp4(const void* w_dev, int32_t rows, int32_t cols, int32
  *  Errors: BD_EINVAL if b < 1, P < 0, G < 1, B < 1, n_inflight < 1,
  *  P % B != 0, G % B != 0, tau is NaN, skip_masked not 0 or 1, or a prompt
  *  id is outside [0, vocab)
- *  (checked on the device; reported by the next synchronising call).
+ *  (checked on the device; reported by the next synchronising call);
+ *  BD_EUNSUPPORTED for b > 256, n_inflight > 8, or (bf16 MoE models) an
+ *  activation plane of 4 GiB or more (rows x d_model x 2 bytes, rows the
+ *  larger of b P and 2 b n_inflight B rounded up to 256: the expert product
+ *  addresses its gathered rows by 32-bit offsets).
  */
 bd_status bd_prefill(bd_model* model, const int32_t* prompt_dev, int32_t b, int32_t P, int32_t G,
                      const bd_decode_cfg* cfg, bd_state** out);

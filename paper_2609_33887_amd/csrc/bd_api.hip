@@ -684,6 +684,11 @@ static bd_status state_layout(const bd_model* m, int32_t b, int32_t P, int32_t G
   const int d = c.d_model, H = c.n_heads, Hkv = c.n_kv_heads, hd = c.head_dim;
   const int qkv = (H + 2 * Hkv) * hd;
   const int ntiles = c.vocab / (m->bf16 ? 128 : 64);
+  // the expert gate/up product gathers its token rows by 32-bit byte
+  // offsets from the start of an activation plane
+  if (c.n_experts > 0 && m->bf16 && (size_t)s->rows_cap * d * 2 >= ((size_t)1 << 32))
+    return fail(BD_EUNSUPPORTED, "MoE activation plane of %zu bytes: at most 4 GiB (fewer sequences or a shorter prompt)",
+                (size_t)s->rows_cap * d * 2);
   bd_status r = BD_OK;
 #define ALLOC(ptr, bytes)                                                  \
   do {                                                                     \

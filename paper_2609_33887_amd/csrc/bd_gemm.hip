@@ -57,10 +57,15 @@ __device__ __forceinline__ void store_pair(bf16_t* p, size_t plane, float x) {
 // forward are the Q/K/V values stored in the KV cache.
 //
 // Main loop: K advances in stages of SK = 32 through a ring of four LDS
-// stages filled by direct global-to-LDS 16-byte loads (no register staging,
+// stages filled by direct buffer-to-LDS 16-byte loads (no register staging,
 // no LDS store instructions); three stages are in flight while the fourth is
 // consumed, and one barrier per stage both publishes the stage and retires
-// the one the next loads overwrite.  A wave's load instruction writes 1 KiB of
+// the one the next loads overwrite.  The bf16 operands go through buffer
+// resources rather than global (flat) addresses: the compiler counts a flat
+// load into LDS as pending LDS traffic too, which turned every LDS wait of
+// the loop into a full drain; with buffer loads the waits count the
+// fragment reads down, and the 32-bit lane offsets replace 64-bit address
+// arithmetic (130 instead of 152 VGPRs in the 128x256 tile).  A wave's load instruction writes 1 KiB of
 // LDS = 16 rows x 64 B, lane l at byte 16 l; in LDS the 16-byte chunk c of row r
 // sits at position c ^ swz(r), swz(r) = (r >> 1) & 3.  A fragment read (lane
 // l: row l & 15, chunk l >> 4) is then free of bank conflicts: measured with
@@ -72,6 +77,10 @@ constexpr int SK = 32;       // K per pipeline stage (KALIGN = 4 stages)
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 3; }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Fourth word of a raw buffer resource on gfx9-family parts: 32-bit data
+// format (a zero format reads zeros), no index stride, no swizzle.
+constexpr int BUF_DWORD3 = 0x00020000;
 
 template <int BM, int BN, int WQ = WQ_NONE>
 struct GemmStage {
@@ -132,19 +141,25 @@ struct MfmaTile {
   floatx4 acc[BM / 32][BN / (8 * NW)];
 };
 
-// s_waitcnt vmcnt(N) leaving the other counters alone (gfx9 encoding)
+// s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding): before a stage barrier the
+// wave's global->LDS loads but the N youngest have landed and all of its LDS
+// reads have returned, so that no wave overwrites a stage another still
+// reads (the barrier itself waits for neither)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
 }
 
 // Per-thread source pointers of one tile's loads: A rows (hi plane; lo at
 // + a_plane) and W rows, each already offset to this lane's 16-byte chunk.
 template <int BM, int BN, int WQ = WQ_NONE, int NW = 4>
 struct TileSrc {
-  const bf16_t* a[BM / (16 * NW)];
-  const bf16_t* w[WQ == WQ_NONE ? BN / (16 * NW) : 1];
+  // A planes and bf16 W through buffer resources (the range check off): the
+  // lane's byte offset from the resource base; the stage adds 2 k bytes
+  __amdgpu_buffer_rsrc_t ra_h, ra_l, rw;
+  uint32_t a[BM / (16 * NW)];
+  uint32_t w[WQ == WQ_NONE ? BN / (16 * NW) : 1];
   const uint8_t* w8[WQ == WQ_FP8 ? W8Load<BN>::loads : 1];
   const uint8_t* w4[WQ == WQ_MXFP4 ? W4Load<BN>::loads : 1];
   const uint8_t* we;        // MXFP4: this lane's 4 exponents of the first stage
@@ -158,8 +173,8 @@ __device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, WQ, NW>& src, 
 #pragma unroll
   for (int i = 0; i < BM / (16 * NW); ++i) {
     const int r = (i * NW + wave) * 16;
-    __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k), (lds_void_t*)(s.ah + r * SK), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(src.a[i] + k + a_plane), (lds_void_t*)(s.al + r * SK), 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(src.ra_h, (lds_void_t*)(s.ah + r * SK), 16, src.a[i], 2 * k, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(src.ra_l, (lds_void_t*)(s.al + r * SK), 16, src.a[i], 2 * k, 0, 0);
   }
   if constexpr (WQ == WQ_FP8) {
     typedef W8Load<BN> L;
@@ -187,7 +202,7 @@ __device__ __forceinline__ void stage_issue(const TileSrc<BM, BN, WQ, NW>& src, 
 #pragma unroll
     for (int i = 0; i < BN / (16 * NW); ++i) {
       const int r = (i * NW + wave) * 16;
-      __builtin_amdgcn_global_load_lds((const void*)(src.w[i] + k), (lds_void_t*)(s.b + r * SK), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src.rw, (lds_void_t*)(s.b + r * SK), 16, src.w[i], 2 * k, 0, 0);
     }
   }
 }
@@ -265,11 +280,16 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
   const int lane = threadIdx.x & 63;
   const int rsub = lane >> 2, chunk = (lane & 3) ^ swz(rsub);
   TileSrc<BM, BN, WQ, NW> src;
+  // resources start at the tile's first row (gathered rows: at row 0, so a
+  // plane's rows x lda x 2 bytes must stay below 4 GiB, checked on the host)
+  const bf16_t* ab = A + (arows ? (size_t)0 : (size_t)m0 * lda) + k0;
+  src.ra_h = __builtin_amdgcn_make_buffer_rsrc((void*)ab, 0, -1, BUF_DWORD3);
+  src.ra_l = __builtin_amdgcn_make_buffer_rsrc((void*)(ab + a_plane), 0, -1, BUF_DWORD3);
 #pragma unroll
   for (int i = 0; i < BM / (16 * NW); ++i) {
     const int r = (i * NW + wave) * 16 + rsub;
-    const int grow = arows ? arows[r < nvalid ? r : 0] : m0 + r;
-    src.a[i] = A + (size_t)grow * lda + k0 + chunk * 8;
+    const int grow = arows ? arows[r < nvalid ? r : 0] : r;
+    src.a[i] = ((uint32_t)grow * (uint32_t)lda + chunk * 8) * 2u;
   }
   if constexpr (WQ == WQ_FP8) {
     typedef W8Load<BN> L;
@@ -289,10 +309,10 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
     src.we = wexp + kb0 * ldw + n0 + wave * (BN / 4) + (lane < BN / 16 ? lane : 0) * 4;
     src.kstep = (size_t)ldw;
   } else {
-    const bf16_t* W = (const bf16_t*)Wv;
+    src.rw = __builtin_amdgcn_make_buffer_rsrc((void*)((const bf16_t*)Wv + (size_t)n0 * ldw + k0), 0, -1, BUF_DWORD3);
 #pragma unroll
     for (int i = 0; i < BN / (16 * NW); ++i)
-      src.w[i] = W + (size_t)(n0 + (i * NW + wave) * 16 + rsub) * ldw + k0 + chunk * 8;
+      src.w[i] = ((uint32_t)((i * NW + wave) * 16 + rsub) * (uint32_t)ldw + chunk * 8) * 2u;
   }
 #pragma unroll
   for (int i = 0; i < BM / 32; ++i)
@@ -300,6 +320,9 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int 
     for (int j = 0; j < BN / (8 * NW); ++j) t.acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = klen / SK;     // multiple of 4, >= 4
+  // no scalar load left in flight: the loop's LDS waits can then count the
+  // fragment reads down instead of draining them
+  __builtin_amdgcn_s_waitcnt(0xC07F);
   stage_issue<BM, BN, WQ, NW>(src, a_plane, 0, s0, wave);
   stage_issue<BM, BN, WQ, NW>(src, a_plane, SK, s1, wave);
   stage_issue<BM, BN, WQ, NW>(src, a_plane, 2 * SK, s2, wave);

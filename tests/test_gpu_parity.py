@@ -619,6 +619,16 @@ def test_error_paths():
         st.commit(want_done=True)
     assert e.value.status == bd.BD_EINVAL
     st.close()
+    # bf16 MoE: the expert gate/up product addresses its gathered rows by
+    # 32-bit offsets, so a 4 GiB activation plane (256 x 32768 rows of
+    # d_model 256) is refused before anything is allocated or read
+    import torch
+    moe_model, _ = get_model(SMALL["moe"])
+    big = torch.zeros((256, 32768), dtype=torch.int32, device="cuda")
+    with pytest.raises(bd.BDError) as e:
+        bd.bd_prefill(moe_model.handle, big.data_ptr(), 256, 32768, 16, bd.decode_cfg(0.9, 2, 16))
+    assert e.value.status == bd.BD_EUNSUPPORTED
+    assert "4 GiB" in str(e.value)
 
 
 def test_moe_2048_redline_sweep_matches_oracle():
