@@ -35,6 +35,9 @@ __device__ __forceinline__ bf16_t f2bf_a(float f) {
 }
 
 constexpr int AK = 64;    // keys per tile
+// Fourth word of a raw buffer resource (gfx9 family): 32-bit data format (a
+// zero format reads zeros), no index stride.
+constexpr int ATT_BUF_DWORD3 = 0x00020000;
 
 typedef __bf16 bf16x2_a __attribute__((ext_vector_type(2)));
 typedef float floatx2_a __attribute__((ext_vector_type(2)));
@@ -130,25 +133,39 @@ __global__ __launch_bounds__(64 * NW) void k_attn_bf16(const bf16_t* __restrict_
   float m_run = -INFINITY, l_part = 0.f;
 
   // register prefetch of the next K/V tile (both planes) overlaps the loads
-  // with the MFMAs of the current tile.  K: chunk ci = (key, 8 dims); keys
-  // >= kend (past the slice's written rows, possibly past the slice) read
-  // row kend - 1 instead, whose finite score every query masks.  V^T: chunk
-  // ci = (dim, 8 keys); a tile never reaches past vstride and the keys past
-  // kend there are finite cache contents that meet zero probabilities.
+  // with the MFMAs of the current tile.  K: chunk ci = (key, 8 dims), read
+  // through a buffer resource that starts at the tile's first key and ends
+  // at key kend, so keys >= kend (past the slice's written rows, possibly
+  // past the slice) read zeros, finite scores that every query masks.  V^T:
+  // chunk ci = (dim, 8 keys) of the tile's [HD][64] block; a tile never
+  // reaches past vstride and the keys past kend there are finite cache
+  // contents that meet zero probabilities.  The lanes' byte offsets inside a
+  // tile do not change from tile to tile.
   u32x4 pkh[NCH], pkl[NCH], pvh[NCH], pvl[NCH];
-#define BD_FETCH(K0)                                                            \
-  do {                                                                          \
-    _Pragma("unroll") for (int it = 0; it < NCH; ++it) {                        \
-      const int ci = tid + NT * it;                                             \
-      const int key = ci / (HD / 8), dc = (ci % (HD / 8)) * 8;                  \
-      const size_t o = (size_t)min((K0) + key, kend - 1) * HD + dc;             \
-      pkh[it] = *(const u32x4*)(Kp + o);                                        \
-      pkl[it] = *(const u32x4*)(Kp + o + k_plane);                              \
-      const int dim = ci / (AK / 8), kc8 = (ci % (AK / 8)) * 8;                 \
-      const size_t ov = vt_row((K0), dim, HD) + kc8;                            \
-      pvh[it] = *(const u32x4*)(Vp + ov);                                       \
-      pvl[it] = *(const u32x4*)(Vp + ov + v_plane);                             \
-    }                                                                           \
+  uint32_t kof[NCH], vof[NCH];
+#pragma unroll
+  for (int it = 0; it < NCH; ++it) {
+    const int ci = tid + NT * it;
+    kof[it] = (uint32_t)((ci / (HD / 8)) * HD + (ci % (HD / 8)) * 8) * 2u;
+    vof[it] = (uint32_t)((ci / (AK / 8)) * AK + (ci % (AK / 8)) * 8) * 2u;
+  }
+#define BD_FETCH(K0)                                                                              \
+  do {                                                                                            \
+    const bf16_t* kb_ = Kp + (size_t)(K0) * HD;                                                   \
+    const bf16_t* vb_ = Vp + (size_t)(K0) * HD;                                                   \
+    const int nrec_ = max(kend - (K0), 0) * HD * 2;                                               \
+    const __amdgpu_buffer_rsrc_t rkh_ = __builtin_amdgcn_make_buffer_rsrc((void*)kb_, 0, nrec_, ATT_BUF_DWORD3); \
+    const __amdgpu_buffer_rsrc_t rkl_ =                                                           \
+        __builtin_amdgcn_make_buffer_rsrc((void*)(kb_ + k_plane), 0, nrec_, ATT_BUF_DWORD3);      \
+    const __amdgpu_buffer_rsrc_t rvh_ = __builtin_amdgcn_make_buffer_rsrc((void*)vb_, 0, AK * HD * 2, ATT_BUF_DWORD3); \
+    const __amdgpu_buffer_rsrc_t rvl_ =                                                           \
+        __builtin_amdgcn_make_buffer_rsrc((void*)(vb_ + v_plane), 0, AK * HD * 2, ATT_BUF_DWORD3); \
+    _Pragma("unroll") for (int it = 0; it < NCH; ++it) {                                          \
+      pkh[it] = __builtin_amdgcn_raw_buffer_load_b128(rkh_, kof[it], 0, 0);                       \
+      pkl[it] = __builtin_amdgcn_raw_buffer_load_b128(rkl_, kof[it], 0, 0);                       \
+      pvh[it] = __builtin_amdgcn_raw_buffer_load_b128(rvh_, vof[it], 0, 0);                       \
+      pvl[it] = __builtin_amdgcn_raw_buffer_load_b128(rvl_, vof[it], 0, 0);                       \
+    }                                                                                             \
   } while (0)
   if (t_lo < t_hi) BD_FETCH(t_lo * AK);
   for (int kt = t_lo; kt < t_hi; ++kt) {
