@@ -65,10 +65,11 @@ __device__ __forceinline__ void store_pair(bf16_t* p, size_t plane, float x) {
 // load into LDS as pending LDS traffic too, which turned every LDS wait of
 // the loop into a full drain; with buffer loads the waits count the
 // fragment reads down, and the 32-bit lane offsets replace 64-bit address
-// arithmetic (130 instead of 152 VGPRs in the 128x256 tile).  A wave's load instruction writes 1 KiB of
-// LDS = 16 rows x 64 B, lane l at byte 16 l; in LDS the 16-byte chunk c of row r
-// sits at position c ^ swz(r), swz(r) = (r >> 1) & 3.  A fragment read (lane
-// l: row l & 15, chunk l >> 4) is then free of bank conflicts: measured with
+// arithmetic (130 instead of 152 VGPRs in the 128x256 tile).  A wave's load
+// instruction writes 1 KiB of LDS = 16 rows x 64 B, lane l at byte 16 l; in
+// LDS the 16-byte chunk c of row r sits at position c ^ swz(r),
+// swz(r) = (r >> 1) & 3.  A fragment read (lane l: row l & 15, chunk l >> 4)
+// is then free of bank conflicts: measured with
 // the LDS bank-conflict counter on gfx950, this pattern reads 141 B/clk per CU
 // with no conflict cycles, where the earlier (r >> 1) & 3 ^ (r >> 3) & 1 had
 // two-way conflicts (106 B/clk) and unswizzled rows 114 B/clk.
@@ -151,8 +152,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
 }
 
-// Per-thread source pointers of one tile's loads: A rows (hi plane; lo at
-// + a_plane) and W rows, each already offset to this lane's 16-byte chunk.
+// Per-thread sources of one tile's loads: the lane's 16-byte chunk of its A
+// rows (hi and lo planes) and W rows, as byte offsets into buffer resources
+// for A and bf16 W, as pointers for quantized W.
 template <int BM, int BN, int WQ = WQ_NONE, int NW = 4>
 struct TileSrc {
   // A planes and bf16 W through buffer resources (the range check off): the
