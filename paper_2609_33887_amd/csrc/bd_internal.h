@@ -168,7 +168,8 @@ struct GemmPlan {
 };
 // wide_ok: the 128x256 tile may be chosen (bf16 weights, k_gemm_bf16 kernels)
 GemmPlan plan_gemm(bool is_bf16, int N, int K, int rows_cap, bool resid = false, bool wide_ok = false);
-// bf16 GEMM with an explicit plan (128x256, 128x128 or 64x64; K % KALIGN == 0;
+// bf16 GEMM with an explicit plan (128x256, 128x128, 64x128 (plain products,
+// bf16 weights) or 64x64; K % KALIGN == 0;
 // zmax > 1 only for EPI_ADD_F32 with a residual-split workspace ws).
 hipError_t launch_gemm_planned(const GemmPlan& p, int epi, const void* A, int lda, size_t a_plane,
                                const void* W, int ldw, int N, int K, const int32_t* M_dev,
