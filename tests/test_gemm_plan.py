@@ -80,6 +80,31 @@ def test_plain_projections_do_not_split():
                 assert zmax == 1 and wsf == 0 and N % bn == 0
 
 
+def test_plain_projection_tiles():
+    """Tile choice of plain (non-residual) bf16 projections: 128 x 256 on
+    windows of at least 2,048 rows for products at least 8,192 wide, 128 x 128
+    when that grid has at least 1,024 workgroups over the row capacity,
+    64 x 128 on windows of at most 1,024 rows, else 64 x 64 (the query takes
+    N and K multiples of 128 only)."""
+    from paper_2609_33887_amd import bd
+    # the dense-1024 step window (16 sequences x 64 rows): gate/up 8,192 wide
+    assert bd.bd_plan_projection(8192, 1024, 1024, False)[:2] == (64, 128)
+    # the same product on the MoE step window (4,096 rows): wide tiles; a
+    # product half as wide there: a 128 x 128 grid of 32 x 32 = 1,024
+    # workgroups
+    assert bd.bd_plan_projection(8192, 1024, 4096, False)[:2] == (128, 256)
+    assert bd.bd_plan_projection(4096, 1024, 4096, False)[:2] == (128, 128)
+    # a narrow product on that window: 22 x 32 = 704 128 x 128 workgroups,
+    # too few, and the window is over 1,024 rows
+    assert bd.bd_plan_projection(2816, 2048, 4096, False)[:2] == (64, 64)
+    # the multi-block window (6,144 rows): gate/up 16,384 wide
+    assert bd.bd_plan_projection(16384, 2048, 6144, False)[:2] == (128, 256)
+    for rc in (256, 512, 768, 1024):
+        for N in (128, 256, 1024, 3072):
+            bm, bn, zmax, _ = bd.bd_plan_projection(N, 1024, rc, False)
+            assert (bm, bn) == (64, 128) and zmax == 1
+
+
 def test_retired_192_row_tile_exceeds_the_old_fixed_workspace():
     """The removed 192 x 128 tile took the 512-workgroup target (every tile
     height but 128 did), so on the dense-1024 down projection (N 1024,
