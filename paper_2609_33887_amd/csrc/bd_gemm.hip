@@ -646,14 +646,15 @@ hipError_t launch_gemm_grouped(int epi, const void* A, int lda, size_t a_plane, 
 // Fused LM head: for its 128 vocabulary columns the workgroup reduces each row
 // to (max z, sum exp(z - max), lowest argmax) and writes one partial per
 // (column tile, row); logits never leave registers.
-__global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__ A, int d,
+template <int TBN, int NW>
+__global__ __launch_bounds__(64 * NW) void k_lm_head_bf16(const bf16_t* __restrict__ A, int d,
                                                       size_t a_plane,
                                                       const bf16_t* __restrict__ W, int V, int mask_id,
                                                       float scale, const int32_t* __restrict__ Mp,
                                                       int rows_cap, float* __restrict__ pmax,
                                                       float* __restrict__ psum,
                                                       int32_t* __restrict__ parg) {
-  constexpr int TBM = 128, TBN = 128;
+  constexpr int TBM = 128, FN = TBN / (8 * NW), WCOL = 2 * TBN / NW, NP = NW / 2;
   const int M = *Mp;
   // items in bands of row tiles (band_tile): an XCD's concurrent workgroups
   // share a few row tiles of the operand and a few vocabulary tiles of the head
@@ -664,23 +665,24 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
   band_tile(u, X, Y, BAND_R, vt, ty);
   const int m0 = ty * TBM, n0 = vt * TBN;
   BD_GEMM_SMEM(TBM, TBN, WQ_NONE);
-  __shared__ float red_m[2][TBM], red_s[2][TBM];
-  __shared__ int32_t red_a[2][TBM];
-  MfmaTile<TBM, TBN> t;
-  mfma_mainloop<TBM, TBN, WQ_NONE>(A, d, a_plane, W, d, nullptr, 0, d, m0, n0, t, gs0, gs1, gs2, gs3,
-                                   threadIdx.x >> 6);
+  // per-row partials of the NP column groups of waves
+  __shared__ float red_m[NP][TBM], red_s[NP][TBM];
+  __shared__ int32_t red_a[NP][TBM];
+  MfmaTile<TBM, TBN, NW> t;
+  mfma_mainloop<TBM, TBN, WQ_NONE, NW>(A, d, a_plane, W, d, nullptr, 0, d, m0, n0, t, gs0, gs1, gs2, gs3,
+                                       threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / NP, wn = wave % NP;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      float v[4];
+      float v[FN];
       float mx = -INFINITY;
       int arg = 0x7fffffff;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int n = n0 + wn * 64 + j * 16 + (lane & 15);
+      for (int j = 0; j < FN; ++j) {
+        const int n = n0 + wn * WCOL + j * 16 + (lane & 15);
         v[j] = (n == mask_id) ? -INFINITY : scale * t.acc[i][j][r];
         if (v[j] > mx) { mx = v[j]; arg = n; }
       }
@@ -692,7 +694,7 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
       }
       float s = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) s += expf(v[j] - mx);
+      for (int j = 0; j < FN; ++j) s += expf(v[j] - mx);
 #pragma unroll
       for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
       if ((lane & 15) == 0) {
@@ -707,10 +709,16 @@ __global__ __launch_bounds__(256) void k_lm_head_bf16(const bf16_t* __restrict__
   if (threadIdx.x < TBM) {
     const int rl = threadIdx.x, m = m0 + rl;
     if (m < M) {
-      const float ma = red_m[0][rl], mb = red_m[1][rl];
-      const float mm = fmaxf(ma, mb);
-      const float s = red_s[0][rl] * expf(ma - mm) + red_s[1][rl] * expf(mb - mm);
-      const int a = (ma >= mb) ? red_a[0][rl] : red_a[1][rl];
+      // column groups in order: the first group holding the maximum gives
+      // the (lowest) argmax
+      float mm = red_m[0][rl];
+      int a = red_a[0][rl];
+#pragma unroll
+      for (int p = 1; p < NP; ++p)
+        if (red_m[p][rl] > mm) { mm = red_m[p][rl]; a = red_a[p][rl]; }
+      float s = 0.f;
+#pragma unroll
+      for (int p = 0; p < NP; ++p) s += red_s[p][rl] * expf(red_m[p][rl] - mm);
       const size_t o = (size_t)vt * rows_cap + m;
       pmax[o] = mm;
       psum[o] = s;
@@ -1073,10 +1081,15 @@ hipError_t launch_lm_head(bool is_bf16, const void* A, int d, size_t a_plane, co
   int ntiles;
   if (is_bf16) {
     if (V % 128 || d % KALIGN) return hipErrorInvalidValue;
-    ntiles = V / 128;
+    const bool wide = V % 256 == 0 && rows_cap >= 2048;
+    ntiles = V / (wide ? 256 : 128);
     dim3 grid(ntiles * cdiv(rows_cap, 128) + 7);
-    k_lm_head_bf16<<<grid, 256, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, V, mask_id, scale, M_dev,
-                                        rows_cap, part_max, part_sum, part_arg);
+    if (wide)
+      k_lm_head_bf16<256, 8><<<grid, 512, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, V, mask_id,
+                                                   scale, M_dev, rows_cap, part_max, part_sum, part_arg);
+    else
+      k_lm_head_bf16<128, 4><<<grid, 256, 0, st>>>((const bf16_t*)A, d, a_plane, (const bf16_t*)W, V, mask_id,
+                                                   scale, M_dev, rows_cap, part_max, part_sum, part_arg);
   } else {
     if (V % SBN || d % SBK) return hipErrorInvalidValue;
     ntiles = V / SBN;
